@@ -1,0 +1,302 @@
+// Steps 1-2 of the planner: expert-load histogram and the load marginals.
+//
+// Sec. 3.1 / A.1 define n_re (tokens rank r sends to expert e), the rank load
+// l_r = sum_{e in E_r} sum_r' n_r'e, the mean, excess/spare and rho; Sec. A.3
+// defines the spill of each expert by cumulative-excess differencing over the
+// experts of a rank sorted by ascending load.  All of it is integer work and
+// is exact; rho and alpha are one rounded fp64 division each.
+//
+// Kernels
+//   home_csr_kernel    (1 block)      rank -> experts lists of the home map.
+//   histogram_kernel   (B*R blocks)   one (problem, source rank) row per block;
+//                                     streams the ids once (HBM-bound) into LDS
+//                                     counters privatised per lane group.
+//   marginals_kernel   (B blocks)     reads n once; loads, mean, excess/spare,
+//                                     rho, alpha, spill.
+#include "common.h"
+
+namespace taot {
+namespace {
+
+constexpr int kCsrThreads = 1024;
+constexpr int kHistThreads = 256;
+constexpr int kHistUnroll = 4;
+constexpr int kMargThreads = 256;
+constexpr int kHistLdsWords = 16384;  // 64 KiB of counters per block when possible
+
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
+
+// rank_ptr[R+1], rank_exp[E]: experts of rank r are rank_exp[rank_ptr[r] ..
+// rank_ptr[r+1]) in ascending id order.  bad_home = 1 if some home is outside
+// [0, R).
+__global__ void __launch_bounds__(kCsrThreads)
+home_csr_kernel(const int32_t* __restrict__ home, int32_t R, int32_t E, int32_t* __restrict__ rank_ptr,
+                int32_t* __restrict__ rank_exp, int32_t* __restrict__ bad_home) {
+  __shared__ int32_t cnt[TAOT_MAX_RANKS + 1];
+  __shared__ int32_t bad;
+  if (threadIdx.x == 0) bad = 0;
+  for (int32_t r = threadIdx.x; r < R; r += kCsrThreads) {
+    int32_t c = 0;
+    for (int32_t e = 0; e < E; ++e) c += (home[e] == r);
+    cnt[r] = c;
+  }
+  __syncthreads();
+  for (int32_t e = threadIdx.x; e < E; e += kCsrThreads) {
+    int32_t h = home[e];
+    if (h < 0 || h >= R) atomicOr(&bad, 1);
+  }
+  if (threadIdx.x == 0) {
+    int32_t s = 0;
+    for (int32_t r = 0; r < R; ++r) {
+      int32_t c = cnt[r];
+      rank_ptr[r] = s;
+      cnt[r] = s;
+      s += c;
+    }
+    rank_ptr[R] = s;
+  }
+  __syncthreads();
+  for (int32_t r = threadIdx.x; r < R; r += kCsrThreads) {
+    int32_t pos = cnt[r];
+    for (int32_t e = 0; e < E; ++e)
+      if (home[e] == r) rank_exp[pos++] = e;
+  }
+  if (threadIdx.x == 0) bad_home[0] = bad;
+}
+
+// One block per (problem, source rank) row of N ids.  LDS holds `copies`
+// private histograms of E+1 words (the +1 rotates banks between copies); lane
+// group (tid & (copies-1)) owns one copy, which spreads the heavy Zipf bins
+// over distinct LDS addresses.  Ids outside [0, E) are counted per row.
+__global__ void __launch_bounds__(kHistThreads)
+histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t E, int32_t copies,
+                 int32_t* __restrict__ n, int32_t* __restrict__ bad_rows) {
+  extern __shared__ int32_t bins[];
+  const int64_t row = blockIdx.x;
+  const int32_t stride = E + 1;
+  const int32_t words = copies * stride;
+  for (int32_t i = threadIdx.x; i < words; i += kHistThreads) bins[i] = 0;
+  __syncthreads();
+  int32_t* my = bins + (int32_t)(threadIdx.x & (copies - 1)) * stride;
+  const int32_t* src = ids + row * N;
+  const uint32_t uE = (uint32_t)E;
+  int32_t bad = 0;
+  const bool vec = (N % 4 == 0) && ((reinterpret_cast<uintptr_t>(src) & 15u) == 0);
+  if (vec) {
+    const v4i* s4 = reinterpret_cast<const v4i*>(src);
+    const int64_t n4 = N / 4;
+    for (int64_t base = threadIdx.x; base < n4; base += (int64_t)kHistThreads * kHistUnroll) {
+      v4i v[kHistUnroll];
+#pragma unroll
+      for (int u = 0; u < kHistUnroll; ++u) {
+        const int64_t i = base + (int64_t)u * kHistThreads;
+        // ids are read exactly once: stream them past the caches
+        v[u] = i < n4 ? __builtin_nontemporal_load(&s4[i]) : v4i{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int u = 0; u < kHistUnroll; ++u) {
+        const int64_t i = base + (int64_t)u * kHistThreads;
+        if (i >= n4) break;
+        const int32_t q[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          if ((uint32_t)q[c] < uE) atomicAdd(&my[q[c]], 1);
+          else ++bad;
+        }
+      }
+    }
+  } else {
+    for (int64_t i = threadIdx.x; i < N; i += kHistThreads) {
+      const int32_t q = src[i];
+      if ((uint32_t)q < uE) atomicAdd(&my[q], 1);
+      else ++bad;
+    }
+  }
+  __syncthreads();
+  int32_t* dst = n + row * E;
+  for (int32_t e = threadIdx.x; e < E; e += kHistThreads) {
+    int32_t s = 0;
+    for (int32_t c = 0; c < copies; ++c) s += bins[c * stride + e];
+    dst[e] = s;
+  }
+  // per-row count of skipped ids (fixed-order block reduction)
+  __shared__ int32_t red[kHistThreads / kWave];
+  int32_t w = bad;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) w += __shfl_xor(w, o, kWave);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = w;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t s = 0;
+    for (int i = 0; i < kHistThreads / kWave; ++i) s += red[i];
+    bad_rows[row] = s;
+  }
+}
+
+// One block per problem.
+__global__ void __launch_bounds__(kMargThreads)
+marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int32_t* __restrict__ home,
+                 const int32_t* __restrict__ rank_ptr, const int32_t* __restrict__ rank_exp,
+                 const int32_t* __restrict__ bad_home, const int32_t* __restrict__ bad_rows,
+                 int64_t* __restrict__ load_e, int64_t* __restrict__ load_r, int64_t* __restrict__ excess,
+                 int64_t* __restrict__ spare, int64_t* __restrict__ spill, float* __restrict__ supply,
+                 float* __restrict__ demand, double* __restrict__ rho, double* __restrict__ alpha,
+                 int64_t* __restrict__ bad_ids, uint32_t* __restrict__ status) {
+  const int64_t b = blockIdx.x;
+  const int tid = threadIdx.x;
+  __shared__ int64_t red_s[kMargThreads / kWave], red_m[kMargThreads / kWave];
+  __shared__ int64_t sh_L, sh_max, sh_bad;
+  const bool home_bad = bad_home[0] != 0;
+
+  // skipped ids of this problem
+  int64_t nb = 0;
+  for (int32_t r = tid; r < R; r += kMargThreads) nb += bad_rows[b * R + r];
+  nb = wave_sum_i64(nb);
+  if ((tid & (kWave - 1)) == 0) red_s[tid / kWave] = nb;
+  __syncthreads();
+  if (tid == 0) {
+    int64_t s = 0;
+    for (int i = 0; i < kMargThreads / kWave; ++i) s += red_s[i];
+    sh_bad = s;
+  }
+  __syncthreads();
+
+  int64_t* xe = load_e + b * E;
+  if (home_bad) {
+    for (int32_t e = tid; e < E; e += kMargThreads) { xe[e] = 0; spill[b * E + e] = 0; }
+    for (int32_t r = tid; r < R; r += kMargThreads) {
+      load_r[b * R + r] = 0; excess[b * R + r] = 0; spare[b * R + r] = 0;
+      if (supply) supply[b * R + r] = 0.f;
+      if (demand) demand[b * R + r] = 0.f;
+    }
+    if (tid == 0) {
+      if (rho) rho[b] = 0.0;
+      alpha[b] = 0.0;
+      if (bad_ids) bad_ids[b] = sh_bad;
+      if (status) status[b] = TAOT_ST_BAD_INPUT | (sh_bad ? TAOT_ST_BAD_ID : 0u);
+    }
+    return;
+  }
+
+  // expert loads x_e = sum_r n_re (coalesced over e, 8 rows in flight)
+  const int32_t* nb_ = n + b * (int64_t)R * E;
+  for (int32_t e = tid; e < E; e += kMargThreads) {
+    int64_t s = 0;
+    int32_t r = 0;
+    for (; r + 8 <= R; r += 8) {
+      int32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = nb_[(int64_t)(r + u) * E + e];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; r < R; ++r) s += nb_[(int64_t)r * E + e];
+    xe[e] = s;
+  }
+  __syncthreads();
+
+  // rank loads, total and maximum
+  int64_t ls = 0, lm = 0;
+  for (int32_t r = tid; r < R; r += kMargThreads) {
+    int64_t s = 0;
+    for (int32_t q = rank_ptr[r]; q < rank_ptr[r + 1]; ++q) s += xe[rank_exp[q]];
+    load_r[b * R + r] = s;
+    ls += s;
+    lm = s > lm ? s : lm;
+  }
+  ls = wave_sum_i64(ls);
+  lm = wave_max_i64(lm);
+  if ((tid & (kWave - 1)) == 0) { red_s[tid / kWave] = ls; red_m[tid / kWave] = lm; }
+  __syncthreads();
+  if (tid == 0) {
+    int64_t s = 0, m = 0;
+    for (int i = 0; i < kMargThreads / kWave; ++i) { s += red_s[i]; m = red_m[i] > m ? red_m[i] : m; }
+    sh_L = s;
+    sh_max = m;
+  }
+  __syncthreads();
+  const int64_t L = sh_L;
+  const int64_t mean = L / R;  // integer mean floor(L / R)
+  for (int32_t r = tid; r < R; r += kMargThreads) {
+    const int64_t l = load_r[b * R + r];
+    const int64_t ex = l > mean ? l - mean : 0;
+    const int64_t sp = mean > l ? mean - l : 0;
+    excess[b * R + r] = ex;
+    spare[b * R + r] = sp;
+    if (supply) supply[b * R + r] = (float)ex;
+    if (demand) demand[b * R + r] = (float)sp;
+  }
+  if (tid == 0) {
+    if (rho) rho[b] = L > 0 ? (double)((int64_t)R * sh_max - L) / (double)L : 0.0;
+    alpha[b] = (double)L / (double)E;
+    if (bad_ids) bad_ids[b] = sh_bad;
+    if (status) status[b] = sh_bad ? TAOT_ST_BAD_ID : 0u;
+  }
+  // spill: prefix of the expert's rank in ascending (x, id) order, then
+  // sigma_k - sigma_{k-1} with sigma = max(prefix - mean, 0)
+  for (int32_t e = tid; e < E; e += kMargThreads) {
+    const int32_t h = home[e];
+    const int64_t x = xe[e];
+    int64_t P = 0;
+    for (int32_t q = rank_ptr[h]; q < rank_ptr[h + 1]; ++q) {
+      const int32_t e2 = rank_exp[q];
+      const int64_t x2 = xe[e2];
+      if (x2 < x || (x2 == x && e2 <= e)) P += x2;
+    }
+    const int64_t hi = P > mean ? P - mean : 0;
+    const int64_t lo = P - x > mean ? P - x - mean : 0;
+    spill[b * E + e] = hi - lo;
+  }
+}
+
+struct LoadsWs {
+  int32_t* rank_ptr;
+  int32_t* rank_exp;
+  int32_t* bad_home;
+  int32_t* bad_rows;
+  size_t bytes;
+};
+
+LoadsWs carve(void* ws, int32_t B, int32_t R, int32_t E) {
+  Carver c{static_cast<char*>(ws)};
+  LoadsWs w;
+  w.rank_ptr = c.take<int32_t>((size_t)R + 1);
+  w.rank_exp = c.take<int32_t>((size_t)E);
+  w.bad_home = c.take<int32_t>(1);
+  w.bad_rows = c.take<int32_t>((size_t)B * R);
+  w.bytes = c.off;
+  return w;
+}
+
+}  // namespace
+
+size_t plan_loads_ws(int32_t B, int32_t R, int32_t E) { return carve(nullptr, B, R, E).bytes; }
+
+taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N, int32_t E,
+                              const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
+                              int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
+                              float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                              uint32_t* status, void* ws, hipStream_t stream) {
+  if (B == 0) return TAOT_OK;
+  LoadsWs w = carve(ws, B, R, E);
+  hipLaunchKernelGGL(home_csr_kernel, dim3(1), dim3(kCsrThreads), 0, stream, home, R, E, w.rank_ptr,
+                     w.rank_exp, w.bad_home);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  int32_t copies = 16;
+  while (copies > 1 && (int64_t)copies * (E + 1) > kHistLdsWords) copies >>= 1;
+  const size_t lds = (size_t)copies * (E + 1) * sizeof(int32_t);
+  if (lds > 65536 && hipFuncSetAttribute((const void*)histogram_kernel,
+                                          hipFuncAttributeMaxDynamicSharedMemorySize,
+                                          (int)lds) != hipSuccess)
+    return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
+                     ids, N, E, copies, n, w.bad_rows);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(marginals_kernel, dim3((unsigned)B), dim3(kMargThreads), 0, stream, n, R, E, home,
+                     w.rank_ptr, w.rank_exp, w.bad_home, w.bad_rows, load_e, load_r, excess, spare,
+                     spill, supply, demand, rho, alpha, bad_ids, status);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  return TAOT_OK;
+}
+
+}  // namespace taot

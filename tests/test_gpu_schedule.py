@@ -1,0 +1,84 @@
+"""GPU parity of taot_round_schedule (Phase 2 + Phase 3) with the oracle:
+bit-exact when both sides consume the same fp32 plan (the oracle's plan cast
+to fp32)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2608_03676_amd as taot
+import workloads as W
+from helpers import oracle_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _to(x, dt=None):
+    return torch.from_numpy(np.ascontiguousarray(x if dt is None else x.astype(dt))).to("cuda:0")
+
+
+def _compare(L, home, T32, Bp, Ba, K, t_max=0, eta=2.0 ** -6, label=""):
+    se, sa, used = O.phase2(L.spill, L.spare, L.excess, L.alpha, home, T32, Bp, K)
+    X, unfilled, rounds, status = O.phase3(L.n, se, sa, Ba, K, eta, t_max)
+    s = taot.round_schedule(_to(L.n), _to(L.spill), _to(L.spare), _to(L.excess), _to(L.alpha),
+                            _to(home, np.int32), _to(T32), _to(Bp), _to(Ba), K, eta, t_max)
+    torch.cuda.synchronize()
+    assert np.array_equal(s.slot_expert.cpu().numpy(), se), f"{label} slot experts"
+    assert np.array_equal(s.slot_amount.cpu().numpy(), sa), f"{label} slot amounts"
+    assert np.array_equal(s.X.cpu().numpy(), X), f"{label} token split"
+    assert np.array_equal(s.unfilled.cpu().numpy(), unfilled), f"{label} unfilled"
+    ru = s.rounds_used.cpu().numpy()
+    assert np.array_equal(ru[:, 0], used), f"{label} phase-2 iterations"
+    assert np.array_equal(ru[:, 1], rounds), f"{label} phase-3 rounds"
+    assert np.array_equal(s.status.cpu().numpy().view(np.uint32), status), f"{label} status"
+    return se, sa, X, unfilled
+
+
+@pytest.mark.parametrize("cfg,problems", [(0, [0]), (1, list(range(0, 58, 4))), (2, [0, 100, 383]),
+                                          (3, [0, 1951])])
+@pytest.mark.parametrize("K", [2, 4])
+def test_workloads(cfg, problems, K, gpu):
+    w = W.WORKLOADS[cfg]
+    print(f"[schedule parity] workload {cfg} problems {problems} K={K}", flush=True)
+    _, L = oracle_inputs(w, problems)
+    C = W.cost_matrix(w)
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), w.eps, w.iters)
+    Bp, Ba = O.topology_pref(C)
+    se, sa, X, unfilled = _compare(L, W.home_map(w), P.T.astype(np.float32), Bp, Ba, K, label=f"cfg{cfg}")
+    assert np.all(unfilled == 0)
+
+
+def _random_instance(seed):
+    rng = np.random.default_rng(seed)
+    R = int(rng.integers(2, 40))
+    E = int(rng.integers(1, 4 * R + 1))
+    N = int(rng.integers(10, 300))
+    B = 3
+    p = rng.dirichlet(np.full(E, 0.4))
+    ids = rng.choice(E, size=(B, R, N), p=p).astype(np.int32)
+    home = rng.integers(0, R, size=E).astype(np.int32)
+    L = O.plan_loads(ids, home, E)
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 16))
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), 0.3, 40)
+    Bp, Ba = O.topology_pref(C)
+    return L, home, P.T.astype(np.float32), Bp, Ba
+
+
+@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("K", [0, 1, 3])
+def test_random(seed, K, gpu):
+    L, home, T32, Bp, Ba = _random_instance(seed)
+    _compare(L, home, T32, Bp, Ba, K, label=f"seed{seed}")
+
+
+def test_starved_auction_reports_unfilled(gpu):
+    L, home, T32, Bp, Ba = _random_instance(99)
+    se, sa, X, unfilled = _compare(L, home, T32, Bp, Ba, 2, t_max=2)
+    assert np.any(unfilled > 0)
+
+
+def test_uninformative_hint_and_negative_scores(gpu):
+    """A zero plan leaves the OT term at 0; a large price step drives auction
+    scores negative, exercising the ordered keys of the arbitration."""
+    L, home, T32, Bp, Ba = _random_instance(7)
+    _compare(L, home, np.zeros_like(T32), Bp, Ba, 2, eta=0.75)

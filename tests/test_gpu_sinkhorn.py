@@ -1,0 +1,147 @@
+"""GPU parity of taot_sinkhorn_batched with the fp64 oracle at the same
+iteration count: relative L1 <= 1e-4, column error <= 1e-5 * mass, row error
+within 1e-5 * mass of the oracle's own fixed-N residual."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2608_03676_amd as taot
+import workloads as W
+from helpers import oracle_inputs, sinkhorn_check
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_sinkhorn(a, b, C, eps, iters, flags=0):
+    dev = torch.device("cuda:0")
+    out = taot.sinkhorn_batched(torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev),
+                                torch.from_numpy(np.ascontiguousarray(b, np.float32)).to(dev),
+                                torch.from_numpy(np.ascontiguousarray(C, np.float32)).to(dev),
+                                eps, iters, flags)
+    torch.cuda.synchronize()
+    return (out.T.cpu().numpy(), out.f.cpu().numpy(), out.g.cpu().numpy(),
+            out.status.cpu().numpy().view(np.uint32))
+
+
+def _check_against_oracle(a32, b32, C32, eps, iters, flags=0):
+    a = a32.astype(np.float64)
+    b = b32.astype(np.float64)
+    T, f, g, st = _gpu_sinkhorn(a32, b32, C32, eps, iters, flags)
+    ref = O.sinkhorn(a, b, C32.astype(np.float64), eps, iters, colcap=not (flags & taot.SK_NO_COLCAP))
+    rels = sinkhorn_check(T, ref.T, a, b)
+    # potentials agree where finite (the plan pins them up to a shared constant:
+    # compare f_i + g_j on the support instead of f and g separately)
+    for p in range(a.shape[0]):
+        hot, cold = ref.f[p] > -np.inf, ref.g[p] > -np.inf
+        assert np.array_equal(hot, f[p] > -np.inf) and np.array_equal(cold, g[p] > -np.inf)
+    return T, st, rels
+
+
+@pytest.mark.parametrize("cfg,problems", [(0, [0]), (1, list(range(58))), (2, list(range(0, 384, 24))),
+                                          (3, [0, 1, 2, 977, 1951])])
+def test_workloads(cfg, problems, gpu):
+    w = W.WORKLOADS[cfg]
+    print(f"[sinkhorn parity] workload {cfg} problems {problems}", flush=True)
+    _, L = oracle_inputs(w, problems)
+    C = W.cost_matrix(w)
+    _, st, rels = _check_against_oracle(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, w.iters)
+    assert np.all(st == 0)
+    print(f"max relL1 {max(rels):.2e}")
+
+
+def test_workload4_streamed(gpu):
+    """R = 1024: the block never fits on chip and is streamed through device memory."""
+    w = W.WORKLOADS[4]
+    print("[sinkhorn parity] workload 4 problem 0 (streamed)", flush=True)
+    _, L = oracle_inputs(w, [0])
+    C = W.cost_matrix(w)
+    _, st, rels = _check_against_oracle(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, w.iters)
+    assert np.all(st == taot.ST_STREAMED)
+
+
+def test_forced_stream_matches_lds_path(gpu):
+    w = W.WORKLOADS[2]
+    _, L = oracle_inputs(w, [7, 8, 9])
+    C = W.cost_matrix(w)
+    a, b = L.excess.astype(np.float32), L.spare.astype(np.float32)
+    T1, st1, _ = _check_against_oracle(a, b, C, w.eps, w.iters)
+    T2, st2, _ = _check_against_oracle(a, b, C, w.eps, w.iters, taot.SK_FORCE_STREAM)
+    assert np.all(st1 == 0) and np.all(st2 == taot.ST_STREAMED)
+    np.testing.assert_allclose(T1, T2, rtol=1e-5, atol=1e-3)
+
+
+def _random_case(rng, R, overlap=False, integer=True):
+    a = np.zeros(R, np.float32)
+    b = np.zeros(R, np.float32)
+    hot = rng.choice(R, size=max(1, R // 4), replace=False)
+    cold = rng.choice(R, size=max(1, R // 2), replace=False) if overlap else np.setdiff1d(np.arange(R), hot)
+    if cold.size == 0:
+        cold = hot
+    if integer:
+        a[hot] = rng.integers(1, 5000, size=hot.size)
+        b[cold] = rng.multinomial(int(a.sum()), np.full(cold.size, 1.0 / cold.size))
+    else:
+        a[hot] = rng.uniform(0.5, 20.0, size=hot.size)
+        b[cold] = rng.uniform(0.5, 20.0, size=cold.size)
+    return a, b
+
+
+@pytest.mark.parametrize("R", [1, 2, 5, 16, 33, 100, 256, 300])
+@pytest.mark.parametrize("overlap", [False, True])
+def test_random(R, overlap, gpu):
+    rng = np.random.default_rng(R + 1000 * overlap)
+    B = 3
+    cases = [_random_case(rng, R, overlap, integer=(p != 2)) for p in range(B)]
+    a = np.stack([c[0] for c in cases])
+    b = np.stack([c[1] for c in cases])
+    C = rng.uniform(0.0, 3.0, (R, R)).astype(np.float32)
+    for eps, iters in ((0.5, 1), (0.2, 7), (0.08, 150)):
+        _check_against_oracle(a, b, C, eps, iters)
+
+
+def test_per_problem_cost_and_no_colcap(gpu):
+    rng = np.random.default_rng(11)
+    R, B = 48, 4
+    cases = [_random_case(rng, R) for _ in range(B)]
+    a = np.stack([c[0] for c in cases])
+    b = np.stack([c[1] for c in cases])
+    C = rng.uniform(0.0, 4.0, (B, R, R)).astype(np.float32)
+    dev = torch.device("cuda:0")
+    for flags in (0, taot.SK_NO_COLCAP):
+        out = taot.sinkhorn_batched(torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev),
+                                    torch.from_numpy(C).to(dev), 0.1, 80, flags)
+        torch.cuda.synchronize()
+        ref = O.sinkhorn(a.astype(float), b.astype(float), C.astype(float), 0.1, 80,
+                         colcap=not flags)
+        sinkhorn_check(out.T.cpu().numpy(), ref.T, a.astype(float), b.astype(float))
+
+
+def test_degenerate(gpu):
+    R = 8
+    C = np.ones((R, R), np.float32)
+    a = np.zeros((4, R), np.float32)
+    b = np.zeros((4, R), np.float32)
+    b[0, 1] = 3.0                    # zero supply
+    a[1, 2] = 3.0                    # zero demand
+    a[2, 0], b[2, 3] = np.nan, 1.0   # bad supply
+    a[3, 0], b[3, 3] = 2.0, 2.0      # fine problem next to the bad ones
+    T, f, g, st = _gpu_sinkhorn(a, b, C, 0.5, 10)
+    assert st[0] == taot.ST_ZERO_MASS and st[1] == taot.ST_ZERO_MASS and st[2] == taot.ST_BAD_INPUT
+    assert st[3] == 0
+    assert not T[:3].any() and np.all(np.isneginf(f[:3])) and np.all(np.isneginf(g[:3]))
+    np.testing.assert_allclose(T[3, 0, 3], 2.0, rtol=1e-6)
+    Cb = C.copy()
+    Cb[0, 5] = np.inf
+    _, _, _, st = _gpu_sinkhorn(a[3:], b[3:], Cb, 0.5, 10)
+    assert st[0] == taot.ST_BAD_INPUT
+
+
+def test_deterministic(gpu):
+    w = W.WORKLOADS[3]
+    _, L = oracle_inputs(w, [3, 4])
+    C = W.cost_matrix(w)
+    a, b = L.excess.astype(np.float32), L.spare.astype(np.float32)
+    T1 = _gpu_sinkhorn(a, b, C, w.eps, w.iters)[0]
+    T2 = _gpu_sinkhorn(a, b, C, w.eps, w.iters)[0]
+    assert T1.tobytes() == T2.tobytes()
