@@ -43,6 +43,18 @@ __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(
 __device__ __forceinline__ float flog2(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ float frcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
+// Register-resident one-wave path: the |H| x |C| block lives on one wave, CPL
+// columns per lane (|C| <= 64*CPL) and 8*C8 rows (|H| <= 8*C8).  Class 0 is
+// every other problem (degenerate, larger, or the path switched off).
+__host__ __device__ constexpr int cpl_index(int cpl) { return cpl == 1 ? 0 : cpl == 2 ? 1 : 2; }
+__host__ __device__ constexpr int wave_class(int cpl, int c8) { return 1 + cpl_index(cpl) * 8 + (c8 - 1); }
+__device__ __forceinline__ int classify(int32_t nh, int32_t nc, uint32_t flags) {
+  if (nh <= 0 || nc <= 0 || nh > 64 || nc > 256) return 0;
+  if (flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER)) return 0;
+  const int cpl = nc <= 64 ? 1 : nc <= 128 ? 2 : 4;
+  return wave_class(cpl, (nh + 7) / 8);
+}
+
 struct SkParams {
   const float* a;
   const float* b;
@@ -149,6 +161,10 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   // ---- where the Kt block lives ----------------------------------------------
   const int64_t need = (int64_t)nh * nc;
   const bool degenerate = sh_bad || nh == 0 || nc == 0;
+  if (!degenerate && classify(nh, nc, p.flags) != 0) {  // the register path owns it
+    if (!STREAM && tid == 0) p.stream_flag[pb] = 0;
+    return;
+  }
   if (!STREAM) {
     const bool to_stream = !degenerate && (need > p.lds_kt_cap || (p.flags & TAOT_SK_FORCE_STREAM));
     if (tid == 0) p.stream_flag[pb] = to_stream ? 1 : 0;
@@ -287,6 +303,392 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   if (tid == 0 && p.status) p.status[pb] = STREAM ? TAOT_ST_STREAMED : 0u;
 }
 
+// ---------------------------------------------------------------------------
+// Register-resident path: one 64-lane wave per problem, no barriers between
+// half-steps.  Lane l owns compact columns l, l+64, ... (CPL of them) and holds
+// Kt[i][c] for all 8*C8 rows: in VGPRs for the first 8*RC rows, in a per-wave
+// LDS tile for the rest (only when CPL = 4 and |H| > 48, which keeps the
+// kernel at <= 256 registers and two waves per SIMD).
+//   column half-step: x_c = sum_i u_i Kt_ic  (u_i broadcast with v_readlane)
+//   row half-step:    p_i = sum_c Kt_ic v_c per lane, then a transposed
+//                     butterfly reduce-scatter over the 64 lanes (8 rows at a
+//                     time: permlane32/16 swaps, then DPP) leaves the total of
+//                     row 8q + (l >> 3) in lane l.
+// An out-of-range scaling triggers the exact log-domain update of all rows
+// (or all columns) with Kt rebuilt from the new potentials.
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ void swap32(float& lo, float& hi) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(lo), __float_as_uint(hi), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void swap16(float& lo, float& hi) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(lo), __float_as_uint(hi), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float bcast(float x, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+}
+__device__ __forceinline__ float first_lane(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+
+// Sums 8 per-lane values over the wave; lane l ends with the total of value
+// (l >> 3).  Halving steps pair lanes l ^ 32 (permlane32 swap), l ^ 16
+// (permlane16 swap) and l <-> 15 - l (row_mirror); the last three steps add
+// over l <-> l ^ 7 (row_half_mirror), l ^ 2 and l ^ 1 (quad_perm).
+__device__ __forceinline__ float reduce8(float (&p)[8], int lane) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) { swap32(p[k], p[k + 4]); p[k] = p[k] + p[k + 4]; }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) { swap16(p[k], p[k + 2]); p[k] = p[k] + p[k + 2]; }
+  const bool b3 = lane & 8;
+  const float keep = b3 ? p[1] : p[0];
+  const float send = b3 ? p[0] : p[1];
+  float y = keep + dpp<0x140>(send);  // row_mirror
+  y = y + dpp<0x141>(y);              // row_half_mirror
+  y = y + dpp<0x4E>(y);               // quad_perm [2,3,0,1]
+  y = y + dpp<0xB1>(y);               // quad_perm [1,0,3,2]
+  return y;
+}
+
+// Rows kept in registers for a column count: 48 for CPL = 4, all 64 otherwise.
+__host__ __device__ constexpr int reg_chunks(int cpl) { return cpl == 4 ? 6 : 8; }
+
+// Iterations and outputs for one problem of class (CPL, C8); the caller has
+// filled the LDS vectors and the first-update potentials Fl.
+template <int CPL, int C8>
+__device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
+                                           const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
+                                           const int32_t* hidx, const float* sAl, float* Fl, float* ul,
+                                           float* kx, float kappa) {
+  constexpr int MAXH = 8 * C8;
+  constexpr int RC = C8 < reg_chunks(CPL) ? C8 : reg_chunks(CPL);
+  constexpr int MREG = 8 * RC;  // rows in registers; rows MREG.. live in kx
+  const int lane = threadIdx.x;
+  const int32_t R = p.R;
+  const float* bd = p.b + pb * R;
+  const float* Cb = p.C + pb * p.C_stride;
+
+  float K[MREG][CPL];
+  // access to row i (static after unrolling) of the lane's columns
+  auto kget = [&](int i, int c) -> float {
+    return i < MREG ? K[i < MREG ? i : 0][c] : kx[((i - MREG) * kWave + lane) * CPL + c];
+  };
+  auto kset = [&](int i, int c, float val) {
+    if (i < MREG) K[i < MREG ? i : 0][c] = val;
+    else kx[((i - MREG) * kWave + lane) * CPL + c] = val;
+  };
+
+  // per-lane column state; the column ids and validity are recomputed from
+  // LDS / the lane index where needed to keep the kernel within 256 VGPRs
+#define CV(c) (lane + kWave * (c) < nc)
+#define CJ(c) (CV(c) ? cidx[lane + kWave * (c)] : 0)
+  float sB[CPL], G[CPL], v[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    sB[c] = CV(c) ? bd[CJ(c)] : 0.f;
+    G[c] = 0.f;
+    v[c] = CV(c) ? 1.f : 0.f;
+  }
+  // row-owned values: lane l carries row 8q + (l >> 3) of chunk q
+#define RV(q) (8 * (q) + (lane >> 3) < nh)
+  float uq[C8];
+#pragma unroll
+  for (int q = 0; q < C8; ++q) uq[q] = RV(q) ? 1.f : 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXH; ++i) {
+    if (i < nh) {
+      const float Fi = Fl[i];
+      const float* crow = Cb + (int64_t)hidx[i] * R;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) kset(i, c, CV(c) ? fexp2(Fi - crow[CJ(c)] * kappa) : 0.f);
+    } else {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) kset(i, c, 0.f);
+    }
+  }
+
+  for (int32_t it = 1; it <= p.iters; ++it) {
+    if (it > 1) {
+      // ---- row half-step: u_i = s~_i / sum_c Kt_ic v_c ------------------------------
+      bool fail = false;
+#pragma unroll
+      for (int q = 0; q < C8; ++q) {
+        float pp[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          float acc = kget(8 * q + r, 0) * v[0];
+#pragma unroll
+          for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(kget(8 * q + r, c), v[c], acc);
+          pp[r] = acc;
+        }
+        const float y = reduce8(pp, lane);
+        const bool rv = RV(q);
+        const float un = (rv ? sAl[8 * q + (lane >> 3)] : 0.f) * frcp(y);
+        fail |= rv && !(un >= kLo && un <= kHi);
+        uq[q] = rv ? un : 0.f;
+      }
+      if (__ballot(fail) != 0) {
+        // exact log-domain update of every row, absorbed into F
+#pragma unroll
+        for (int i = 0; i < MAXH; ++i) {
+          if (i < nh) {
+            const float* crow = Cb + (int64_t)hidx[i] * R;
+            float t[CPL];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+              t[c] = CV(c) ? (G[c] + flog2(v[c])) - crow[CJ(c)] * kappa : -INFINITY;
+              mx = fmaxf(mx, t[c]);
+            }
+            mx = wave_max(mx);
+            float sum = 0.f;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
+            sum = first_lane(wave_sum(sum));
+            const float fi = flog2(sAl[i]) - (mx + flog2(sum));
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) kset(i, c, CV(c) ? fexp2((fi + G[c]) - crow[CJ(c)] * kappa) : 0.f);
+            if (lane == 0) Fl[i] = fi;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < C8; ++q) uq[q] = RV(q) ? 1.f : 0.f;
+        __syncthreads();
+      }
+    }
+    // ---- column half-step: v_c = d_c / sum_i u_i Kt_ic -------------------------------
+    float x[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) x[c] = 0.f;
+#pragma unroll
+    for (int q = 0; q < C8; ++q) {
+      // broadcast the chunk's row scalings first so that each FMA sits far
+      // enough behind the v_readlane that produced its operand
+      float us[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) us[r] = bcast(uq[q], 8 * r);
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], kget(8 * q + r, c), x[c]);
+    }
+    bool failc = false;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const float vn = sB[c] * frcp(x[c]);
+      failc |= CV(c) && !(vn >= kLo && vn <= kHi);
+      v[c] = CV(c) ? vn : 0.f;
+    }
+    if (__ballot(failc) != 0) {
+      // exact log-domain update of every column, absorbed into G (online LSE)
+      float mx[CPL], sum[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) { mx[c] = -INFINITY; sum[c] = 0.f; }
+#pragma unroll
+      for (int i = 0; i < MAXH; ++i) {
+        if (i < nh) {
+          const float fi = Fl[i] + flog2(bcast(uq[i / 8], 8 * (i % 8)));
+          const float* crow = Cb + (int64_t)hidx[i] * R;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            if (CV(c)) {
+              const float t = fi - crow[CJ(c)] * kappa;
+              const float m2 = fmaxf(mx[c], t);
+              sum[c] = sum[c] * fexp2(mx[c] - m2) + fexp2(t - m2);
+              mx[c] = m2;
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        G[c] = CV(c) ? flog2(sB[c]) - (mx[c] + flog2(sum[c])) : 0.f;
+        v[c] = CV(c) ? 1.f : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < MAXH; ++i) {
+        if (i < nh) {
+          const float Fi = Fl[i];
+          const float* crow = Cb + (int64_t)hidx[i] * R;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) kset(i, c, CV(c) ? fexp2((Fi + G[c]) - crow[CJ(c)] * kappa) : 0.f);
+        }
+      }
+    }
+  }
+
+  // ---- plan, column cap, outputs -------------------------------------------------
+  const bool colcap = !(p.flags & TAOT_SK_NO_COLCAP);
+  float fac[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) fac[c] = 1.f;
+  if (colcap) {
+    float cs[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) cs[c] = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXH; ++i) {
+      const float ui = bcast(uq[i / 8], 8 * (i % 8));
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) cs[c] += ui * kget(i, c) * v[c];
+    }
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) fac[c] = CV(c) ? fminf(1.f, sB[c] / (cs[c] + 1e-12f)) : 1.f;
+  }
+#pragma unroll
+  for (int q = 0; q < C8; ++q)
+    if ((lane & 7) == 0 && RV(q)) ul[8 * q + (lane >> 3)] = uq[q];
+  __syncthreads();
+  if (p.T) {
+    float* Tb = p.T + pb * R * R;
+    for (int32_t i = 0; i < R; ++i) {
+      const bool hot = hpos[i] >= 0;
+      for (int32_t j = lane; j < R; j += kWave)
+        if (!hot || cpos[j] < 0) Tb[(int64_t)i * R + j] = 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < MAXH; ++i) {
+      if (i < nh) {
+        const float ui = bcast(uq[i / 8], 8 * (i % 8));
+        float* trow = Tb + (int64_t)hidx[i] * R;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+          if (CV(c)) trow[CJ(c)] = ui * kget(i, c) * (v[c] * fac[c]);
+      }
+    }
+  }
+  const float to_nat = p.eps * kLn2;
+  for (int32_t i = lane; i < R; i += kWave) {
+    const int32_t ih = hpos[i];
+    if (p.f) p.f[pb * R + i] = ih >= 0 ? (Fl[ih] + flog2(ul[ih])) * to_nat : -INFINITY;
+    if (p.g && cpos[i] < 0) p.g[pb * R + i] = -INFINITY;
+  }
+  if (p.g) {
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+      if (CV(c)) p.g[pb * R + CJ(c)] = (G[c] + flog2(v[c])) * to_nat;
+  }
+  if (lane == 0 && p.status) p.status[pb] = 0u;
+#undef RV
+#undef CJ
+#undef CV
+}
+
+// LDS of the wave kernel: cpos, hpos [R] + cidx [256] + hidx [64] ints,
+// sA, F, u [64] floats, and the spill tile for rows 48..63 at CPL = 4.
+constexpr int kWaveXRows = 16;
+__host__ __device__ constexpr size_t wave_lds_bytes(int32_t R) {
+  return (size_t)(2 * R + 256 + 64) * 4 + 3 * 64 * 4 + (size_t)kWaveXRows * kWave * 4 * 4;
+}
+
+__global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
+  extern __shared__ int32_t wl[];
+  const int lane = threadIdx.x;
+  const int64_t pb = blockIdx.x;
+  const int32_t R = p.R;
+  int32_t* cpos = wl;              // [R] compact column of rank j, -1 if not cold
+  int32_t* hpos = cpos + R;        // [R] compact row of rank i, -1 if not hot
+  int32_t* cidx = hpos + R;        // [256]
+  int32_t* hidx = cidx + 256;      // [64]
+  float* sAl = reinterpret_cast<float*>(hidx + 64);  // [64] scaled supply
+  float* Fl = sAl + 64;            // [64] absorbed row potentials (log2 units)
+  float* ul = Fl + 64;             // [64] final row scalings
+  float* kx = ul + 64;             // [16][64][4] rows 48..63 when CPL = 4
+  const float* a = p.a + pb * R;
+  const float* bd = p.b + pb * R;
+  const float* Cb = p.C + pb * p.C_stride;
+
+  // ---- supports, validation, mass -------------------------------------------
+  double sa = 0.0, sd = 0.0;
+  bool bad = false;
+  int32_t nh = 0, nc = 0;
+  for (int32_t base = 0; base < R; base += kWave) {
+    const int32_t i = base + lane;
+    const bool in = i < R;
+    const float ai = in ? a[i] : 0.f, bi = in ? bd[i] : 0.f;
+    bad |= !(ai >= 0.f && ai <= 3.402823466e38f) || !(bi >= 0.f && bi <= 3.402823466e38f);
+    sa += (double)ai;
+    sd += (double)bi;
+    const uint64_t hm = __ballot(in && ai > 0.f), cm = __ballot(in && bi > 0.f);
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int32_t ph = nh + __popcll(hm & below), pc = nc + __popcll(cm & below);
+    if (in) {
+      hpos[i] = ai > 0.f ? ph : -1;
+      cpos[i] = bi > 0.f ? pc : -1;
+    }
+    if (in && ai > 0.f && ph < 64) hidx[ph] = i;
+    if (in && bi > 0.f && pc < 256) cidx[pc] = i;
+    nh += __popcll(hm);
+    nc += __popcll(cm);
+  }
+  const int cls = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
+  if (cls == 0) return;  // uniform: another path owns this problem
+  sa = wave_sum_d(sa);
+  sd = wave_sum_d(sd);
+  double gamma = __shfl(sd, 0, kWave) / fmax(__shfl(sa, 0, kWave), kEps0);
+  gamma = gamma < 1.0 ? gamma : 1.0;
+  if (lane < nh) sAl[lane] = (float)(gamma * (double)a[hidx[lane]]);
+  __syncthreads();
+  const float kappa = kLog2e / p.eps;
+
+  // ---- first row update over all R columns (v = 1): F_i = log2 s~_i - LSE2_j(-C'_ij)
+  bool badc = false;
+  for (int32_t i = 0; i < nh; ++i) {
+    const float* crow = Cb + (int64_t)hidx[i] * R;
+    float mx = -INFINITY;
+    for (int32_t j = lane; j < R; j += kWave) {
+      const float c = crow[j];
+      badc |= !(c == c) || c == INFINITY || c == -INFINITY;
+      mx = fmaxf(mx, -c * kappa);
+    }
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int32_t j = lane; j < R; j += kWave) sum += fexp2(-crow[j] * kappa - mx);
+    sum = first_lane(wave_sum(sum));
+    if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
+  }
+  if (__ballot(badc) != 0) {
+    if (p.T)
+      for (int64_t q = lane; q < (int64_t)R * R; q += kWave) p.T[pb * R * R + q] = 0.f;
+    for (int32_t i = lane; i < R; i += kWave) {
+      if (p.f) p.f[pb * R + i] = -INFINITY;
+      if (p.g) p.g[pb * R + i] = -INFINITY;
+    }
+    if (lane == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
+    return;
+  }
+  __syncthreads();
+  switch (cls) {
+#define TAOT_WAVE_CASE(CPL_, C8_)                                                                      \
+  case wave_class(CPL_, C8_):                                                                          \
+    wave_solve<CPL_, C8_>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, kx, kappa);               \
+    break;
+#define TAOT_WAVE_CPL(CPL_)                                                                            \
+  TAOT_WAVE_CASE(CPL_, 1) TAOT_WAVE_CASE(CPL_, 2) TAOT_WAVE_CASE(CPL_, 3) TAOT_WAVE_CASE(CPL_, 4)      \
+  TAOT_WAVE_CASE(CPL_, 5) TAOT_WAVE_CASE(CPL_, 6) TAOT_WAVE_CASE(CPL_, 7) TAOT_WAVE_CASE(CPL_, 8)
+    TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2) TAOT_WAVE_CPL(4)
+#undef TAOT_WAVE_CPL
+#undef TAOT_WAVE_CASE
+    default: break;
+  }
+}
+
+taot_status launch_wave(const SkParams& p, hipStream_t stream) {
+  const size_t lds = wave_lds_bytes(p.R);
+  if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_wave_kernel,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(sinkhorn_wave_kernel, dim3((unsigned)p.B), dim3(kWave), lds, stream, p);
+  return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
+}
+
 // Largest nh * nc over disjoint supports of R ranks (nh + nc <= R).
 int64_t max_block(int32_t R) { return (int64_t)(R / 2) * (R - R / 2); }
 
@@ -319,6 +721,10 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
   SkParams p{a, b, B, R, C, C_stride, eps, iters, flags, T, f, g, status, w.flag, w.kt, w.kt_stride, 0, 0};
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
+  if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {
+    const taot_status st = launch_wave(p, stream);
+    if (st != TAOT_OK) return st;
+  }
   if (lds_path) {
     p.lds_kt_cap = (int32_t)max_block(R);
     const size_t lds = vec_bytes + (size_t)p.lds_kt_cap * sizeof(float);

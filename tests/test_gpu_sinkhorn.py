@@ -40,14 +40,36 @@ def _check_against_oracle(a32, b32, C32, eps, iters, flags=0):
 
 @pytest.mark.parametrize("cfg,problems", [(0, [0]), (1, list(range(58))), (2, list(range(0, 384, 24))),
                                           (3, [0, 1, 2, 977, 1951])])
-def test_workloads(cfg, problems, gpu):
+@pytest.mark.parametrize("flags", [0, taot.SK_NO_REGISTER])
+def test_workloads(cfg, problems, flags, gpu):
+    """Default flags take the register-resident path at these sizes;
+    SK_NO_REGISTER takes the LDS-resident one."""
     w = W.WORKLOADS[cfg]
-    print(f"[sinkhorn parity] workload {cfg} problems {problems}", flush=True)
+    print(f"[sinkhorn parity] workload {cfg} problems {problems} flags {flags}", flush=True)
     _, L = oracle_inputs(w, problems)
     C = W.cost_matrix(w)
-    _, st, rels = _check_against_oracle(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, w.iters)
+    _, st, rels = _check_against_oracle(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps,
+                                        w.iters, flags)
     assert np.all(st == 0)
     print(f"max relL1 {max(rels):.2e}")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_mixed_size_classes_in_one_batch(seed, gpu):
+    """One batch whose problems fall into different kernel classes: hot-set
+    sizes 1..70 and cold-set sizes 1..250 (register classes and the fallback)."""
+    rng = np.random.default_rng(50 + seed)
+    R, B = 256, 24
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p in range(B):
+        nh = int(rng.integers(1, 71))
+        nc = int(rng.integers(1, min(250, R - nh) + 1))
+        perm = rng.permutation(R)
+        a[p, perm[:nh]] = rng.integers(1, 3000, size=nh)
+        b[p, perm[nh:nh + nc]] = rng.multinomial(int(a[p].sum()), np.full(nc, 1.0 / nc))
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32))
+    _check_against_oracle(a, b, C, 0.08, 300)
 
 
 def test_workload4_streamed(gpu):
@@ -61,14 +83,16 @@ def test_workload4_streamed(gpu):
 
 
 def test_forced_stream_matches_lds_path(gpu):
+    """The streamed and the LDS-resident kernels run the same arithmetic in the
+    same order, only the plan block lives elsewhere: their plans are identical."""
     w = W.WORKLOADS[2]
     _, L = oracle_inputs(w, [7, 8, 9])
     C = W.cost_matrix(w)
     a, b = L.excess.astype(np.float32), L.spare.astype(np.float32)
-    T1, st1, _ = _check_against_oracle(a, b, C, w.eps, w.iters)
+    T1, st1, _ = _check_against_oracle(a, b, C, w.eps, w.iters, taot.SK_NO_REGISTER)
     T2, st2, _ = _check_against_oracle(a, b, C, w.eps, w.iters, taot.SK_FORCE_STREAM)
     assert np.all(st1 == 0) and np.all(st2 == taot.ST_STREAMED)
-    np.testing.assert_allclose(T1, T2, rtol=1e-5, atol=1e-3)
+    assert T1.tobytes() == T2.tobytes()
 
 
 def _random_case(rng, R, overlap=False, integer=True):
