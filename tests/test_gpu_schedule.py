@@ -82,3 +82,61 @@ def test_uninformative_hint_and_negative_scores(gpu):
     scores negative, exercising the ordered keys of the arbitration."""
     L, home, T32, Bp, Ba = _random_instance(7)
     _compare(L, home, np.zeros_like(T32), Bp, Ba, 2, eta=0.75)
+
+
+def _instance(seed, R, E=None, N=None, B=2):
+    rng = np.random.default_rng(seed)
+    E = E or int(rng.integers(R, 2 * R + 1))
+    N = N or int(rng.integers(50, 400))
+    p = rng.dirichlet(np.full(E, 0.4))
+    ids = rng.choice(E, size=(B, R, N), p=p).astype(np.int32)
+    home = rng.integers(0, R, size=E).astype(np.int32)
+    L = O.plan_loads(ids, home, E)
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32))
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), 0.3, 40)
+    Bp, Ba = O.topology_pref(C)
+    return rng, L, home, P.T.astype(np.float32), Bp, Ba
+
+
+@pytest.mark.parametrize("R", [63, 64, 65, 130, 200, 256, 300])
+def test_rank_counts(R, gpu):
+    """Rank sets span one to four 64-bit words (ragged last word); R = 300
+    exceeds the one-wave layout and runs on the general kernel."""
+    print(f"[schedule parity] R={R}", flush=True)
+    _, L, home, T32, Bp, Ba = _instance(300 + R, R)
+    _compare(L, home, T32, Bp, Ba, 2, label=f"R{R}")
+
+
+@pytest.mark.parametrize("eta", [0.0, 2.0 ** -6, 0.5, 1e-300, -0.25])
+def test_price_steps(eta, gpu):
+    """Step 0 keeps every price at 0 (lowest rank of the best tier); a step
+    below the spacing of doubles makes prices stall, so service counts no
+    longer order the scores and the general kernel takes over, as it does
+    for a negative step."""
+    _, L, home, T32, Bp, Ba = _instance(77, 96)
+    _compare(L, home, T32, Bp, Ba, 2, eta=eta, label=f"eta{eta}")
+
+
+@pytest.mark.parametrize("kind", ["few", "few_neg_inf", "many", "pos_inf", "five"])
+def test_bonus_structures(kind, gpu):
+    """Auction bonuses other than topology tiers: few distinct values per
+    column (random, with -inf and NaN entries that can never win), more values than
+    the tier search keeps, and +inf bonuses (both sent to the general kernel)."""
+    rng, L, home, T32, Bp, _ = _instance(11, 80)
+    R = 80
+    if kind.startswith("few") or kind == "five":
+        pool = np.array([1.5, 0.75, 0.0, -0.25, -2.0, 3.0])
+        nv = 5 if kind == "five" else 4
+        Ba = np.empty((R, R))
+        for h in range(R):
+            vals = rng.choice(pool, size=nv, replace=False)
+            Ba[:, h] = vals[rng.integers(0, nv, size=R)]
+        if kind == "few_neg_inf":
+            Ba[rng.random((R, R)) < 0.1] = -np.inf
+            Ba[rng.random((R, R)) < 0.05] = np.nan
+    elif kind == "many":
+        Ba = rng.uniform(-1.0, 1.0, (R, R))
+    else:
+        Ba = O.topology_pref(W.cost_matrix_for(R, ("two_tier", 1.0, 4.0)))[1]
+        Ba[3, :] = np.inf
+    _compare(L, home, T32, Bp, Ba, 2, label=kind)
