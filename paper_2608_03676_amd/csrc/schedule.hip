@@ -55,7 +55,7 @@ struct SchParams {
   uint32_t* status;
   char* slab;
   int64_t slab_bytes;
-  const int32_t* fallback;  // [B] 1 = the one-wave kernel left this problem to us (nullable)
+  const int32_t* fallback;  // [B] 1 = the LDS-resident kernel left this problem to us (nullable)
 };
 
 struct Slab {
@@ -416,10 +416,10 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 
 
 // ===========================================================================
-// One-wave path.  Same arithmetic and order as schedule_kernel, with all
-// per-problem state in LDS, one 64-lane wave per problem and no block
-// barriers.  It serves R <= 256 and needs every column of Bauct to take few
-// distinct values (as topology costs do):
+// LDS-resident path.  Same arithmetic and order as schedule_kernel, with one
+// 256-thread workgroup per problem and all of its state in LDS and registers.
+// It serves R <= 256, R*K <= 1024 and bonuses (Bauct columns) that take few
+// distinct values, as topology costs do.
 //
 // Phase-3 bids by tiers.  The ranks of host column h split into tiers of equal
 // bonus (descending).  With prices that start at 0 and rise by a fixed step on
@@ -431,15 +431,26 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 // bid is the best tier result under (max score, lowest rank), and tiers whose
 // bonus is below the best score so far are skipped (price >= 0).  A price step
 // of 0 keeps every price at 0, and the argmax is the lowest rank of the first
-// non-empty tier.  A prepass checks the conditions on the device and sends
-// problems to schedule_kernel when they fail, as it does problems whose
-// candidate or slot-expert counts exceed the LDS layout.
+// non-empty tier.
+//
+// Phase-3 arbitration by bonus.  Every live bid on rank r was placed at r's
+// current price (a slot re-bids when its rank serves), so among r's bidders
+// the score order is the order of their bonuses when distinct bonuses stay
+// distinct after subtracting any reachable price.  A rank's winner is then the
+// maximum of the 32-bit key (bonus rank, -slot), taken with one atomicMax.
+//
+// A prepass checks these conditions on the device and sends problems to
+// schedule_kernel when they fail, as it does problems whose candidate or
+// slot-expert counts exceed the LDS layout.
 
-constexpr int kDistinctCap = 64;   // distinct slot experts per problem in LDS
-constexpr int kTierMax = 4;        // distinct bonus values per host column
-constexpr int kTierWords = 4;      // 64-rank words of a rank set (R <= 256)
-constexpr int kStructCap = 32;     // distinct host tier structures kept in LDS
-constexpr int kPlanes = 17;        // count bit-planes: counts <= R*K <= 65536
+constexpr int kDistinctCap = 64;            // distinct slot experts per problem in LDS
+constexpr int kTierMax = 4;                 // distinct bonus values per host column
+constexpr int kTierWords = 4;               // 64-rank words of a rank set (R <= 256)
+constexpr int kStructCap = 32;              // distinct host tier structures kept in LDS
+constexpr int kValueCap = kStructCap * kTierMax;  // distinct bonuses of the table
+constexpr int kMaxSlots = 1024;             // S = R*K of the LDS-resident path
+constexpr int kPlanes = 11;                 // count bit-planes: counts <= S <= 1024
+static_assert(kTierWords == kSchWaves, "one wave per 64-rank word");
 
 // Tier structure of column h of Bauct: its distinct bonuses in descending
 // order and the rank set of each; ntier[h] = -1 if there are more than
@@ -486,18 +497,21 @@ auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __res
 }
 
 // Deduplicates the host tier structures into a table of at most kStructCap
-// (one block, one thread per host): sidx[h] is host h's entry, hdr[0] the
-// table size, hdr[1] = 1 when the tier search is exact for this Bauct and
-// price step: every column has at most kTierMax values, none is +inf, the
-// table fits, and the step is 0 or exceeds twice the spacing of doubles at
+// (one block, one thread per host) and ranks the table's distinct bonuses
+// (ascending): sidx[h] is host h's entry, cvr the bonus rank of each tier,
+// hdr[0] the table size and hdr[1] = 1 when the LDS-resident auction is exact for
+// this Bauct and price step: every column has at most kTierMax values, none
+// is +inf, the table fits, and both the step (if not 0) and every gap between
+// distinct bonuses exceed twice the spacing of doubles at
 // max|bonus| + S * step (prices stay below S * step: a rank serves each slot
 // at most once).
 __global__ void __launch_bounds__(256)
 auction_struct_kernel(const int32_t* __restrict__ ntier, const double* __restrict__ tv,
                       const uint64_t* __restrict__ tmask, int32_t R, int64_t S, double step,
                       int32_t* __restrict__ sidx, int32_t* __restrict__ cn, double* __restrict__ cv,
-                      uint64_t* __restrict__ cm, int32_t* __restrict__ hdr) {
+                      int32_t* __restrict__ cvr, uint64_t* __restrict__ cm, int32_t* __restrict__ hdr) {
   __shared__ int32_t first[256];
+  __shared__ double dv[kValueCap];
   const int32_t h = threadIdx.x;
   constexpr int kRow = kTierMax * kTierWords;
   if (h < R) {
@@ -512,61 +526,79 @@ auction_struct_kernel(const int32_t* __restrict__ ntier, const double* __restric
     first[h] = f;
   }
   __syncthreads();
-  if (h == 0) {
-    int32_t ns = 0;
-    double vm = 0.0;
-    bool ok = true;
-    for (int32_t g = 0; g < R; ++g) {
-      ok &= ntier[g] >= 0;
-      if (first[g] != g) {
-        sidx[g] = sidx[first[g]];
-        continue;
-      }
-      for (int32_t t = 0; t < kTierMax; ++t) {
-        const double v = tv[g * kTierMax + t];
-        if (t < ntier[g]) {
-          ok &= v != INFINITY;
-          vm = fmax(vm, fabs(v));
-        }
-      }
-      if (ns < kStructCap) {
-        cn[ns] = ntier[g] > 0 ? ntier[g] : 0;
-        for (int32_t t = 0; t < kTierMax; ++t) cv[ns * kTierMax + t] = tv[g * kTierMax + t];
-        for (int32_t q = 0; q < kRow; ++q) cm[ns * kRow + q] = tmask[g * kRow + q];
-      }
-      sidx[g] = ns;
-      ++ns;
+  if (h != 0) return;
+  int32_t ns = 0, nd = 0;
+  double vm = 0.0;
+  bool ok = true;
+  for (int32_t g = 0; g < R; ++g) {
+    ok &= ntier[g] >= 0;
+    if (first[g] != g) {
+      sidx[g] = sidx[first[g]];
+      continue;
     }
-    ok &= ns <= kStructCap;
-    const double top = vm + (double)S * step * 1.01 + 1.0;
-    ok &= step == 0.0 || (step > 0.0 && step > 2.0 * (nextafter(top, INFINITY) - top));
-    hdr[0] = ns < kStructCap ? ns : kStructCap;
-    hdr[1] = ok ? 1 : 0;
+    const int32_t nt = ntier[g] > 0 ? ntier[g] : 0;
+    for (int32_t t = 0; t < nt; ++t) {
+      const double v = tv[g * kTierMax + t];
+      ok &= v != INFINITY;
+      vm = fmax(vm, fabs(v));
+    }
+    if (ns < kStructCap) {
+      cn[ns] = nt;
+      for (int32_t t = 0; t < kTierMax; ++t) cv[ns * kTierMax + t] = tv[g * kTierMax + t];
+      for (int32_t q = 0; q < kRow; ++q) cm[ns * kRow + q] = tmask[g * kRow + q];
+      // distinct bonuses of the table, ascending
+      for (int32_t t = 0; t < nt; ++t) {
+        const double v = tv[g * kTierMax + t];
+        int32_t pos = 0;
+        bool dup = false;
+        for (int32_t i = 0; i < nd; ++i) {
+          dup |= dv[i] == v;
+          pos += dv[i] < v;
+        }
+        if (dup) continue;
+        for (int32_t i = nd; i > pos; --i) dv[i] = dv[i - 1];
+        dv[pos] = v;
+        ++nd;
+      }
+    }
+    sidx[g] = ns;
+    ++ns;
   }
+  ok &= ns <= kStructCap;
+  const int32_t nsc = ns < kStructCap ? ns : kStructCap;
+  for (int32_t i = 0; i < nsc; ++i)
+    for (int32_t t = 0; t < kTierMax; ++t) {
+      int32_t rank = 0;
+      if (t < cn[i])
+        while (dv[rank] != cv[i * kTierMax + t]) ++rank;
+      cvr[i * kTierMax + t] = rank;
+    }
+  const double top = vm + (double)S * step * 1.01 + 1.0;
+  const double spacing2 = 2.0 * (nextafter(top, INFINITY) - top);
+  ok &= step == 0.0 || (step > 0.0 && step > spacing2);
+  for (int32_t i = 0; i + 1 < nd; ++i) ok &= dv[i + 1] - dv[i] > spacing2;
+  hdr[0] = nsc;
+  hdr[1] = ok ? 1 : 0;
 }
 
-struct WaveLds {
+struct LdsState {
   // both phases
   int32_t* slot_ec;   // [S] candidate index of the slot's expert or -1
-  int32_t* amt;       // [S] phase 2: slot amount; phase 3: tokens still planned
+  int32_t* amt;       // [S] slot amounts (Phase 2)
   int32_t* ce;        // [NEC] candidate experts (spill > 0), ascending
-  // phase 2
-  int32_t* cr; int64_t* spare_p; int32_t* matched; int32_t* prop_e; double* prop_s; int32_t* assigned;
-  int64_t* spill_p; uint64_t* ekey; int32_t* ewin;
-  // phase 3 (aliases the phase-2 region)
-  double* price; uint64_t* rkey; int32_t* rwin; uint64_t* served;
-  int32_t* bid; double* bid_s; int32_t* dsl; int32_t* work;
-  uint64_t* vmask; int32_t* dexp; int32_t* dmap;
-  int32_t* cnt; uint64_t* planes;
-  int32_t* sidx; int32_t* cn; double* cv; uint64_t* cm;
+  // Phase 2
+  int32_t* hce; double* den; int32_t* cr; int32_t* spare_p; int32_t* matched; int32_t* prop_e;
+  double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
+  // Phase 3 (aliases the Phase-2 region)
+  double* price; uint32_t* rkey; uint64_t* served; int32_t* work; uint32_t* wres;
+  uint64_t* vmask; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
+  int32_t* sidx; int32_t* cn; double* cv; int32_t* cvr; uint64_t* cm;
   size_t bytes;
 };
 
-__host__ __device__ inline WaveLds carve_wave(char* base, int32_t R, int32_t K, int32_t NEC) {
-  WaveLds w;
-  const int64_t S = (int64_t)R * K;
-  const size_t S1 = S > 0 ? (size_t)S : 1;
-  const int32_t W64 = (R + 63) / 64;
+__host__ __device__ inline LdsState carve_lds(char* base, int32_t R, int32_t K, int32_t NEC) {
+  LdsState w;
+  const size_t S1 = R * K > 0 ? (size_t)R * K : 1, R_ = (size_t)R, N_ = (size_t)NEC;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     char* q = base + off;
@@ -575,45 +607,61 @@ __host__ __device__ inline WaveLds carve_wave(char* base, int32_t R, int32_t K, 
   };
   w.slot_ec = (int32_t*)take(4 * S1);
   w.amt = (int32_t*)take(4 * S1);
-  w.ce = (int32_t*)take(4 * (size_t)NEC);
+  w.ce = (int32_t*)take(4 * N_);
   const size_t split = off;
-  w.cr = (int32_t*)take(4 * (size_t)R); w.spare_p = (int64_t*)take(8 * (size_t)R);
-  w.matched = (int32_t*)take(4 * (size_t)R); w.prop_e = (int32_t*)take(4 * (size_t)R);
-  w.prop_s = (double*)take(8 * (size_t)R); w.assigned = (int32_t*)take(4 * (size_t)R * (K > 0 ? K : 1));
-  w.spill_p = (int64_t*)take(8 * (size_t)NEC); w.ekey = (uint64_t*)take(8 * (size_t)NEC);
-  w.ewin = (int32_t*)take(4 * (size_t)NEC);
+  w.hce = (int32_t*)take(4 * N_); w.den = (double*)take(8 * R_); w.cr = (int32_t*)take(4 * R_);
+  w.spare_p = (int32_t*)take(4 * R_); w.matched = (int32_t*)take(4 * R_); w.prop_e = (int32_t*)take(4 * R_);
+  w.prop_s = (double*)take(8 * R_); w.assigned = (int32_t*)take(4 * S1);
+  w.spill_p = (int32_t*)take(4 * N_); w.ekey = (uint64_t*)take(8 * N_); w.ewin = (int32_t*)take(4 * N_);
   const size_t end2 = off;
   off = split;
-  w.price = (double*)take(8 * (size_t)R); w.rkey = (uint64_t*)take(8 * (size_t)R);
-  w.rwin = (int32_t*)take(4 * (size_t)R); w.served = (uint64_t*)take(8 * (size_t)W64);
-  w.bid = (int32_t*)take(4 * S1); w.bid_s = (double*)take(8 * S1);
-  w.dsl = (int32_t*)take(4 * S1); w.work = (int32_t*)take(4 * S1);
+  w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(4 * R_);
+  w.served = (uint64_t*)take(8 * kTierWords); w.work = (int32_t*)take(4 * S1); w.wres = (uint32_t*)take(4 * S1);
   w.vmask = (uint64_t*)take(8 * (size_t)kDistinctCap * kTierWords);
-  w.dexp = (int32_t*)take(4 * kDistinctCap); w.dmap = (int32_t*)take(4 * (size_t)NEC);
-  w.cnt = (int32_t*)take(4 * (size_t)R); w.planes = (uint64_t*)take(8 * kPlanes * kTierWords);
-  w.sidx = (int32_t*)take(4 * (size_t)R); w.cn = (int32_t*)take(4 * kStructCap);
-  w.cv = (double*)take(8 * kStructCap * kTierMax);
+  w.dexp = (int32_t*)take(4 * kDistinctCap); w.dmap = (int32_t*)take(4 * N_);
+  w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * kPlanes * kTierWords);
+  w.sidx = (int32_t*)take(4 * R_); w.cn = (int32_t*)take(4 * kStructCap);
+  w.cv = (double*)take(8 * kStructCap * kTierMax); w.cvr = (int32_t*)take(4 * kStructCap * kTierMax);
   w.cm = (uint64_t*)take(8 * kStructCap * kTierMax * kTierWords);
   w.bytes = end2 > off ? end2 : off;
   return w;
 }
 
-struct WaveParams {
+struct LdsParams {
   SchParams s;
   const int32_t* sidx;   // [R] host -> tier structure
   const int32_t* cn;     // [kStructCap] tiers per structure
   const double* cv;      // [kStructCap][kTierMax] tier bonuses, descending
+  const int32_t* cvr;    // [kStructCap][kTierMax] rank of each tier bonus among the table's
   const uint64_t* cm;    // [kStructCap][kTierMax][kTierWords] tier rank sets
-  const int32_t* hdr;    // [0] structures, [1] tier search exact
+  const int32_t* hdr;    // [0] structures, [1] LDS-resident auction exact
   int32_t* fallback;     // [B] 1 = left to schedule_kernel
   int32_t* nprime;       // [B][kDistinctCap][R]
   int32_t NEC;           // candidate-expert capacity of the LDS layout
 };
 
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+// Block-wide OR with one barrier; flags alternate between two halves of buf
+// ([2][kSchWaves]) so that a call never overwrites flags still being read.
+__device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
+  const uint64_t m = __ballot(flag);
+  if ((threadIdx.x & (kWave - 1)) == 0) buf[parity * kSchWaves + threadIdx.x / kWave] = m != 0;
+  __syncthreads();
+  bool any = false;
+#pragma unroll
+  for (int w = 0; w < kSchWaves; ++w) any |= buf[parity * kSchWaves + w] != 0;
+  parity ^= 1;
+  return any;
+}
+
+// Appends the flagged items of a wave to a list whose length lives in LDS
+// (*count); the order of the list is unspecified.
+__device__ __forceinline__ void list_append(bool flag, int32_t item, int32_t* list, int32_t* count) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t m = __ballot(flag);
+  int32_t base = 0;
+  if (lane == 0 && m) base = atomicAdd(count, __popcll(m));
+  base = __shfl(base, 0, kWave);
+  if (flag) list[base + __popcll(m & ((1ull << lane) - 1ull))] = item;
 }
 
 __device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
@@ -622,22 +670,28 @@ __device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
     const int32_t u = __shfl_xor(v, o, kWave);
     v = u > v ? u : v;
   }
-  return __builtin_amdgcn_readfirstlane(v);
+  return v;
 }
 
-__global__ void __launch_bounds__(kWave) schedule_wave_kernel(WaveParams wp) {
-  extern __shared__ __attribute__((aligned(16))) char wlds[];
+// One problem per 256-thread workgroup; thread i owns Phase-3 slots
+// i, i + 256, ... (SPL of them).
+template <int SPL>
+__global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp) {
+  extern __shared__ __attribute__((aligned(16))) char lds_dyn[];
+  __shared__ int32_t wave_cnt[kSchWaves];
+  __shared__ int32_t flagbuf[2 * kSchWaves];
+  __shared__ int32_t sh_nwork, sh_maxc;
+  __shared__ unsigned long long sh_sum, sh_big;
   const SchParams& p = wp.s;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
   const int64_t b = blockIdx.x;
   const int32_t R = p.R, E = p.E, K = p.K;
-  const int64_t S = (int64_t)R * K;
-  const int32_t W64 = (R + 63) / 64;
-  const uint64_t below = (1ull << lane) - 1ull;
-  WaveLds L = carve_wave(wlds, R, K, wp.NEC);
+  const int32_t S = R * K;
+  int parity = 0;
+  LdsState L = carve_lds(lds_dyn, R, K, wp.NEC);
 
-  if (wp.hdr[1] == 0) {  // the tier search would not be exact for this Bauct and step
-    if (lane == 0) wp.fallback[b] = 1;
+  if (wp.hdr[1] == 0) {  // the LDS-resident auction would not be exact for this Bauct and step
+    if (tid == 0) wp.fallback[b] = 1;
     return;
   }
   const int64_t* spill = p.spill + b * E;
@@ -652,14 +706,15 @@ __global__ void __launch_bounds__(kWave) schedule_wave_kernel(WaveParams wp) {
 
   // ---- validation, candidates, cold ranks ------------------------------------------
   bool badh = false;
-  for (int32_t e = lane; e < E; e += kWave) {
+  for (int32_t e = tid; e < E; e += kSchThreads) {
     const int32_t h = p.home[e];
     badh |= h < 0 || h >= R;
   }
-  if (__ballot(badh) != 0) {
-    for (int64_t s = lane; s < S; s += kWave) { se[s] = -1; sa[s] = 0; }
-    for (int64_t q = lane; q < (int64_t)R * S; q += kWave) Xb[q] = 0;
-    if (lane == 0) {
+  if (tid == 0) { sh_sum = 0; sh_big = 0; sh_maxc = 0; sh_nwork = 0; }
+  if (block_or(badh, flagbuf, parity)) {
+    for (int32_t s = tid; s < S; s += kSchThreads) { se[s] = -1; sa[s] = 0; }
+    for (int64_t q = tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
+    if (tid == 0) {
       p.unfilled[b] = 0;
       if (p.rounds_used) { p.rounds_used[2 * b] = 0; p.rounds_used[2 * b + 1] = 0; }
       if (p.status) p.status[b] = TAOT_ST_BAD_INPUT;
@@ -668,166 +723,204 @@ __global__ void __launch_bounds__(kWave) schedule_wave_kernel(WaveParams wp) {
     return;
   }
   int32_t ne = 0, nc = 0;
-  int64_t mass = 0;  // bounds every slot amount and transfer
-  for (int32_t base = 0; base < E; base += kWave) {
-    const int32_t e = base + lane;
+  int64_t mass = 0, big = 0;  // amounts must fit the 32-bit LDS state
+  for (int32_t base = 0; base < E; base += kSchThreads) {
+    const int32_t e = base + tid;
     const int64_t v = e < E ? spill[e] : 0;
     const bool f = v > 0;
-    const uint64_t m = __ballot(f);
-    const int32_t pos = ne + __popcll(m & below);
-    if (f && pos < wp.NEC) { L.ce[pos] = e; L.spill_p[pos] = v; }
-    ne += __popcll(m);
+    int32_t tot;
+    const int32_t pos = ne + compact_pos(f, wave_cnt, tot);
+    if (f && pos < wp.NEC) {
+      L.ce[pos] = e;
+      L.spill_p[pos] = (int32_t)(v < INT_MAX ? v : INT_MAX);
+      L.hce[pos] = p.home[e];
+    }
+    ne += tot;
     mass += f ? v : 0;
   }
+  for (int32_t base = 0; base < R; base += kSchThreads) {
+    const int32_t r = base + tid;
+    const int64_t v = r < R ? spare[r] : 0;
+    const bool f = v > 0;
+    int32_t tot;
+    const int32_t pos = nc + compact_pos(f, wave_cnt, tot);
+    if (f) { L.cr[pos] = r; L.spare_p[pos] = (int32_t)(v < INT_MAX ? v : INT_MAX); }
+    nc += tot;
+    big = v > big ? v : big;
+    if (r < R) {
+      const double ex = (double)excess[r];
+      L.den[r] = ex > kEps0 ? ex : kEps0;
+    }
+  }
   mass = wave_sum_i64(mass);
-  if (ne > wp.NEC || mass > INT_MAX) {  // beyond the LDS layout or its 32-bit amounts
-    if (lane == 0) wp.fallback[b] = 1;
+  big = wave_max_i64(big);
+  if (lane == 0) {
+    atomicAdd(&sh_sum, (unsigned long long)mass);
+    atomicMax(&sh_big, (unsigned long long)big);
+  }
+  __syncthreads();
+  if (ne > wp.NEC || sh_sum > (unsigned long long)INT_MAX || sh_big > (unsigned long long)INT_MAX) {
+    if (tid == 0) wp.fallback[b] = 1;
     return;
   }
-  for (int32_t base = 0; base < R; base += kWave) {
-    const int32_t r = base + lane;
-    const bool f = r < R && spare[r] > 0;
-    const uint64_t m = __ballot(f);
-    const int32_t pos = nc + __popcll(m & below);
-    if (f) { L.cr[pos] = r; L.spare_p[pos] = spare[r]; }
-    nc += __popcll(m);
-  }
-  for (int64_t q = lane; q < (int64_t)nc * K; q += kWave) L.assigned[q] = -1;
-  for (int32_t ec = lane; ec < ne; ec += kWave) { L.ekey[ec] = 0; L.ewin[ec] = INT_MAX; }
-  for (int64_t s = lane; s < S; s += kWave) { L.slot_ec[s] = -1; L.amt[s] = 0; se[s] = -1; }
-  wave_sync();
+  for (int32_t q = tid; q < nc * K; q += kSchThreads) L.assigned[q] = -1;
+  for (int32_t ec = tid; ec < ne; ec += kSchThreads) { L.ekey[ec] = 0; L.ewin[ec] = INT_MAX; }
+  for (int32_t s = tid; s < S; s += kSchThreads) { L.slot_ec[s] = -1; L.amt[s] = 0; se[s] = -1; }
+  __syncthreads();
 
   // ---- Phase 2: column-priority iterative matching ---------------------------------
   int32_t used2 = 0;
   for (int32_t k = 0; k < K; ++k) {
-    for (int32_t rc = lane; rc < nc; rc += kWave) L.matched[rc] = 0;
-    wave_sync();
+    for (int32_t rc = tid; rc < nc; rc += kSchThreads) { L.matched[rc] = 0; L.prop_e[rc] = -1; }
+    __syncthreads();
     for (int32_t inner = 0; inner < nc; ++inner) {
+      // Step 1: every unmatched cold rank proposes its best candidate expert
       bool proposed = false;
-      for (int32_t rc = lane; rc < nc; rc += kWave) {
+      for (int32_t rc = tid; rc < nc; rc += kSchThreads) {
+        if (L.matched[rc]) continue;
         int32_t best = -1;
         double bs = -INFINITY;
-        const int64_t sp = L.spare_p[rc];
-        if (!L.matched[rc] && sp > 0) {
+        const int32_t sp = L.spare_p[rc];
+        if (sp > 0) {
           const int32_t r = L.cr[rc];
-          for (int32_t ec = 0; ec < ne; ++ec) {
-            const int64_t spl = L.spill_p[ec];
-            if (spl <= 0) continue;
-            const int32_t h = p.home[L.ce[ec]];
-            if (h == r) continue;
-            bool taken = false;
-            for (int32_t kk = 0; kk < k; ++kk) taken |= L.assigned[(int64_t)rc * K + kk] == ec;
-            if (taken) continue;
-            const double q = (double)(spl < sp ? spl : sp);
-            const double t1 = alpha * p.Bpref[(int64_t)h * R + r];
-            const double ex = (double)excess[h];
-            const double tn = (double)Tb[(int64_t)h * R + r] / (ex > kEps0 ? ex : kEps0);
-            const double t2 = a2 * tn;
-            const double score = (q + t1) + t2;
-            if (score > bs) { bs = score; best = ec; }
+          const int32_t* asg = L.assigned + rc * K;
+          const int32_t a0 = k > 0 ? asg[0] : -1, a1 = k > 1 ? asg[1] : -1;
+          const int32_t a2_ = k > 2 ? asg[2] : -1, a3 = k > 3 ? asg[3] : -1;
+          for (int32_t ec0 = 0; ec0 < ne; ec0 += 8) {
+            int32_t sl[8], hh[8];
+            double bp[8];
+            float tt[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const bool in = ec0 + u < ne;
+              sl[u] = in ? L.spill_p[ec0 + u] : 0;
+              hh[u] = in ? L.hce[ec0 + u] : r;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const bool ok = sl[u] > 0 && hh[u] != r;
+              const int64_t o = (int64_t)hh[u] * R + r;
+              bp[u] = ok ? p.Bpref[o] : 0.0;
+              tt[u] = ok ? Tb[o] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const int32_t ec = ec0 + u;
+              if (sl[u] <= 0 || hh[u] == r) continue;
+              bool taken = ec == a0 || ec == a1 || ec == a2_ || ec == a3;
+              for (int32_t kk = 4; kk < k; ++kk) taken |= asg[kk] == ec;
+              if (taken) continue;
+              const double q = (double)(sl[u] < sp ? sl[u] : sp);
+              const double t1 = alpha * bp[u];
+              const double tn = (double)tt[u] / L.den[hh[u]];
+              const double t2 = a2 * tn;
+              const double score = (q + t1) + t2;
+              if (score > bs) { bs = score; best = ec; }
+            }
           }
         }
         L.prop_e[rc] = best;
         L.prop_s[rc] = bs;
         proposed |= best >= 0;
       }
-      if (__ballot(proposed) == 0) break;  // nothing can change any more
-      wave_sync();
-      // each proposed expert keeps its best proposer: max score, then lowest rank
-      for (int32_t rc = lane; rc < nc; rc += kWave)
+      if (!block_or(proposed, flagbuf, parity)) break;  // nothing can change any more
+      // Steps 2-3: each proposed expert keeps its best proposer: max score, then lowest rank
+      for (int32_t rc = tid; rc < nc; rc += kSchThreads)
         if (L.prop_e[rc] >= 0)
           atomicMax(reinterpret_cast<unsigned long long*>(&L.ekey[L.prop_e[rc]]),
                     (unsigned long long)ordered_key(L.prop_s[rc]));
-      wave_sync();
-      for (int32_t rc = lane; rc < nc; rc += kWave)
+      __syncthreads();
+      for (int32_t rc = tid; rc < nc; rc += kSchThreads)
         if (L.prop_e[rc] >= 0 && ordered_key(L.prop_s[rc]) == L.ekey[L.prop_e[rc]])
           atomicMin(&L.ewin[L.prop_e[rc]], rc);
-      wave_sync();
-      // winners take g = min(spill, spare) into slot k of their rank
-      for (int32_t ec = lane; ec < ne; ec += kWave) {
+      __syncthreads();
+      // Step 4: winners take g = min(spill, spare) into slot k of their rank
+      for (int32_t ec = tid; ec < ne; ec += kSchThreads) {
         const int32_t w = L.ewin[ec];
         if (w != INT_MAX) {
-          const int64_t g = L.spill_p[ec] < L.spare_p[w] ? L.spill_p[ec] : L.spare_p[w];
+          const int32_t g = L.spill_p[ec] < L.spare_p[w] ? L.spill_p[ec] : L.spare_p[w];
           L.spill_p[ec] -= g;
           L.spare_p[w] -= g;
           L.matched[w] = 1;
-          L.assigned[(int64_t)w * K + k] = ec;
-          const int64_t s = (int64_t)L.cr[w] * K + k;
+          L.prop_e[w] = -1;  // matched ranks stop proposing
+          L.assigned[w * K + k] = ec;
+          const int32_t s = L.cr[w] * K + k;
           L.slot_ec[s] = ec;
-          L.amt[s] += (int32_t)g;
+          L.amt[s] += g;
           se[s] = L.ce[ec];
         }
         L.ekey[ec] = 0;
         L.ewin[ec] = INT_MAX;
       }
-      wave_sync();
+      __syncthreads();
       ++used2;
     }
   }
-  for (int64_t s = lane; s < S; s += kWave) sa[s] = L.amt[s];
+  for (int32_t s = tid; s < S; s += kSchThreads) sa[s] = L.amt[s];
 
   // ---- Phase 3: Lagrangian auction ---------------------------------------------------
   // distinct slot experts, in ascending candidate (= expert) order
-  for (int32_t ec = lane; ec < ne; ec += kWave) L.dmap[ec] = 0;
-  wave_sync();
-  for (int64_t s = lane; s < S; s += kWave)
+  __syncthreads();
+  for (int32_t ec = tid; ec < ne; ec += kSchThreads) L.dmap[ec] = 0;
+  __syncthreads();
+  for (int32_t s = tid; s < S; s += kSchThreads)
     if (L.slot_ec[s] >= 0) L.dmap[L.slot_ec[s]] = 1;
-  wave_sync();
+  __syncthreads();
   int32_t D = 0;
-  for (int32_t base = 0; base < ne; base += kWave) {
-    const int32_t ec = base + lane;
+  for (int32_t base = 0; base < ne; base += kSchThreads) {
+    const int32_t ec = base + tid;
     const bool f = ec < ne && L.dmap[ec] == 1;
-    const uint64_t m = __ballot(f);
-    const int32_t pos = D + __popcll(m & below);
+    int32_t tot;
+    const int32_t pos = D + compact_pos(f, wave_cnt, tot);
     if (ec < ne) L.dmap[ec] = f ? pos : -1;
     if (f && pos < kDistinctCap) L.dexp[pos] = L.ce[ec];
-    D += __popcll(m);
+    D += tot;
   }
   if (D > kDistinctCap) {
-    if (lane == 0) wp.fallback[b] = 1;
+    if (tid == 0) wp.fallback[b] = 1;
     return;
   }
-  wave_sync();
-  // tokens of each slot expert per rank (device memory) and the valid-rank sets
+  __syncthreads();
+  // tokens of each slot expert per rank (device memory) and the valid-rank
+  // sets; wave w covers ranks 64w .. 64w+63
   int32_t* np = wp.nprime + b * (int64_t)kDistinctCap * R;
   const int32_t* nb = p.n + b * (int64_t)R * E;
   for (int32_t d = 0; d < D; ++d) {
     const int32_t e = L.dexp[d];
-    for (int32_t w = 0; w < kTierWords; ++w) {
-      const int32_t r = w * kWave + lane;
-      const int32_t v = r < R ? nb[(int64_t)r * E + e] : 0;
-      if (r < R) np[(int64_t)d * R + r] = v;
-      const uint64_t m = __ballot(v > 0);
-      if (lane == 0) L.vmask[d * kTierWords + w] = m;
-    }
+    const int32_t r = wid * kWave + lane;
+    const int32_t v = r < R ? nb[(int64_t)r * E + e] : 0;
+    if (r < R) np[(int64_t)d * R + r] = v;
+    const uint64_t m = __ballot(v > 0);
+    if (lane == 0) L.vmask[d * kTierWords + wid] = m;
   }
-  // slots that bid in the first round
-  int32_t nwork = 0;
-  for (int64_t base = 0; base < S; base += kWave) {
-    const int64_t s = base + lane;
+  // slot state in registers; every open slot bids in the first round
+  int32_t amt[SPL], bid[SPL], dsl[SPL];
+  uint32_t key[SPL];
+  uint32_t need = 0;
+#pragma unroll
+  for (int j = 0; j < SPL; ++j) {
+    const int32_t s = j * kSchThreads + tid;
     const int32_t ec = s < S ? L.slot_ec[s] : -1;
-    if (s < S) {
-      L.dsl[s] = ec >= 0 ? L.dmap[ec] : -1;
-      L.bid[s] = -1;
-      if (ec < 0) L.amt[s] = 0;
-    }
-    const bool f = ec >= 0 && L.amt[s] > 0;
-    const uint64_t m = __ballot(f);
-    if (f) L.work[nwork + __popcll(m & below)] = (int32_t)s;
-    nwork += __popcll(m);
+    dsl[j] = ec >= 0 ? L.dmap[ec] : -1;
+    amt[j] = ec >= 0 ? L.amt[s] : 0;
+    bid[j] = -1;
+    key[j] = 0;
+    const bool f = amt[j] > 0;
+    list_append(f, (dsl[j] << 16) | s, L.work, &sh_nwork);
+    need |= f ? 1u << j : 0u;
   }
-  for (int32_t r = lane; r < R; r += kWave) {
+  for (int32_t r = tid; r < R; r += kSchThreads) {
     L.price[r] = 0.0;
     L.rkey[r] = 0;
-    L.rwin[r] = INT_MAX;
     L.cnt[r] = 0;
     L.sidx[r] = wp.sidx[r];
   }
-  for (int32_t q = lane; q < kPlanes * kTierWords; q += kWave) L.planes[q] = 0ull;
+  if (tid < kTierWords) L.served[tid] = 0ull;
+  for (int32_t q = tid; q < kPlanes * kTierWords; q += kSchThreads) L.planes[q] = 0ull;
   const int32_t ns = wp.hdr[0];
-  for (int32_t q = lane; q < ns; q += kWave) L.cn[q] = wp.cn[q];
-  for (int32_t q = lane; q < ns * kTierMax; q += kWave) L.cv[q] = wp.cv[q];
-  for (int32_t q = lane; q < ns * kTierMax * kTierWords; q += kWave) L.cm[q] = wp.cm[q];
+  for (int32_t q = tid; q < ns; q += kSchThreads) L.cn[q] = wp.cn[q];
+  for (int32_t q = tid; q < ns * kTierMax; q += kSchThreads) { L.cv[q] = wp.cv[q]; L.cvr[q] = wp.cvr[q]; }
+  for (int32_t q = tid; q < ns * kTierMax * kTierWords; q += kSchThreads) L.cm[q] = wp.cm[q];
   // X starts at zero; every (rank, slot) pair is served at most once (after a
   // transfer either the rank holds no more tokens of the slot's expert or the
   // slot is full), so transfers below are plain stores
@@ -835,35 +928,35 @@ __global__ void __launch_bounds__(kWave) schedule_wave_kernel(WaveParams wp) {
     int4* x4 = reinterpret_cast<int4*>(Xb);
     const int64_t n4 = ((int64_t)R * S) / 4;
     if ((reinterpret_cast<uintptr_t>(Xb) & 15u) == 0) {
-      for (int64_t q = lane; q < n4; q += kWave) x4[q] = make_int4(0, 0, 0, 0);
-      for (int64_t q = n4 * 4 + lane; q < (int64_t)R * S; q += kWave) Xb[q] = 0;
+      for (int64_t q = tid; q < n4; q += kSchThreads) x4[q] = make_int4(0, 0, 0, 0);
+      for (int64_t q = n4 * 4 + tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
     } else {
-      for (int64_t q = lane; q < (int64_t)R * S; q += kWave) Xb[q] = 0;
+      for (int64_t q = tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
     }
   }
-  wave_sync();
+  __syncthreads();
 
   const double step = p.price_step;
   const bool track = step > 0.0;  // counts order the prices; with step 0 all prices stay 0
+  int32_t nwork = sh_nwork;
   int32_t maxc = 0;               // largest service count so far
-  const int64_t tmax = p.t_max > 0 ? p.t_max : S * (R + 1);
+  const int64_t tmax = p.t_max > 0 ? p.t_max : (int64_t)S * (R + 1);
   int64_t rounds = 0;
   for (int64_t t = 1; t <= tmax; ++t) {
     // (a) bids of the listed slots: argmax over ranks holding tokens of the
     //     slot's expert of Bauct[r][host] - price[r], lowest rank on ties
     const int32_t nplanes = maxc > 0 ? 32 - __builtin_clz((uint32_t)maxc) : 0;
-    for (int32_t w0 = 0; w0 < nwork; w0 += kWave) {
-      if (w0 + lane >= nwork) continue;
-      const int32_t s = L.work[w0 + lane];
-      const int32_t host = s / K;
-      const uint64_t* vm = L.vmask + L.dsl[s] * kTierWords;
-      const int32_t st = L.sidx[host];
+    for (int32_t q = tid; q < nwork; q += kSchThreads) {
+      const int32_t item = L.work[q];
+      const int32_t s = item & 0xFFFF, d = item >> 16;
+      const int32_t st = L.sidx[s / K];
       const int32_t nt = L.cn[st];
+      const uint64_t* vm = L.vmask + d * kTierWords;
       uint64_t valid[kTierWords];
 #pragma unroll
       for (int w = 0; w < kTierWords; ++w) valid[w] = vm[w];
       double bs = -INFINITY;
-      int32_t br = INT_MAX;
+      int32_t br = INT_MAX, bv = 0;
       for (int32_t ti = 0; ti < nt; ++ti) {
         const double v = L.cv[st * kTierMax + ti];
         if (v < bs) break;  // every score in this tier and the next is <= v
@@ -890,97 +983,108 @@ __global__ void __launch_bounds__(kWave) schedule_wave_kernel(WaveParams wp) {
         for (int w = kTierWords - 1; w >= 0; --w)
           if (c[w]) r = w * kWave + __builtin_ctzll(c[w]);
         const double sc = v - L.price[r];
-        if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; }
+        if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; bv = L.cvr[st * kTierMax + ti]; }
       }
-      L.bid[s] = br == INT_MAX ? -1 : br;
-      L.bid_s[s] = bs;
+      L.wres[s] = br == INT_MAX ? 0u : ((uint32_t)bv << 16) | (uint32_t)(br + 1);
     }
-    wave_sync();
-    // (b) each rank keeps its best bidder: max score, then lowest slot
+    __syncthreads();
+    // (b) owners take their new bids and post each to its rank: the key orders
+    //     by bonus, then by lowest slot
+    if (tid == 0) sh_nwork = 0;
+    if (tid < kTierWords) L.served[tid] = 0ull;
     bool any = false;
-    for (int64_t s = lane; s < S; s += kWave) {
-      const int32_t r = L.bid[s];
-      if (L.amt[s] > 0 && r >= 0) {
-        atomicMax(reinterpret_cast<unsigned long long*>(&L.rkey[r]),
-                  (unsigned long long)auction_key(L.bid_s[s]));
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) {
+      const int32_t s = j * kSchThreads + tid;
+      if ((need >> j) & 1u) {
+        const uint32_t w = L.wres[s];
+        bid[j] = w ? (int32_t)(w & 0xFFFFu) - 1 : -1;
+        key[j] = (w & 0xFFFF0000u) | (uint32_t)(0xFFFF - s);
+      }
+      if (amt[j] > 0 && bid[j] >= 0) {
+        atomicMax(&L.rkey[bid[j]], key[j]);
         any = true;
       }
     }
-    if (__ballot(any) == 0) break;  // no bid: the state is final
-    wave_sync();
-    for (int64_t s = lane; s < S; s += kWave) {
-      const int32_t r = L.bid[s];
-      if (L.amt[s] > 0 && r >= 0 && auction_key(L.bid_s[s]) == L.rkey[r]) atomicMin(&L.rwin[r], (int32_t)s);
-    }
-    wave_sync();
-    // (c) transfers; a rank that moved tokens raises its price
+    if (!block_or(any, flagbuf, parity)) break;  // no bid: the state is final
+    // (c) each rank's winner moves min(tokens held, tokens planned); a rank
+    //     that moved tokens raises its price
+    int32_t held[SPL];
+#pragma unroll
+    for (int j = 0; j < SPL; ++j)  // issued before the winners are known
+      held[j] = amt[j] > 0 && bid[j] >= 0 ? np[(int64_t)dsl[j] * R + bid[j]] : 0;
+    uint32_t won = 0;
     int32_t newmax = 0;
-    for (int32_t w = 0; w < W64; ++w) {
-      const int32_t r = w * kWave + lane;
-      bool did = false;
-      if (r < R) {
-        const int32_t s = L.rwin[r];
-        if (s != INT_MAX) {
-          const int32_t d = L.dsl[s];
-          int32_t* cell = np + (int64_t)d * R + r;
-          const int32_t have = *cell;
-          const int32_t x = have < L.amt[s] ? have : L.amt[s];
-          Xb[(int64_t)r * S + s] = x;
-          *cell = have - x;
-          L.amt[s] -= x;
-          if (x > 0) {
-            L.price[r] = L.price[r] + step;
-            if (track) {
-              const int32_t c0 = L.cnt[r], c1 = c0 + 1;
-              L.cnt[r] = c1;
-              newmax = c1 > newmax ? c1 : newmax;
-              for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
-                atomicXor(reinterpret_cast<unsigned long long*>(
-                              &L.planes[__builtin_ctz(flip) * kTierWords + w]),
-                          1ull << lane);
-            }
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) {
+      const int32_t r = bid[j];
+      if (amt[j] > 0 && r >= 0 && L.rkey[r] == key[j]) {
+        const int32_t s = j * kSchThreads + tid;
+        const int32_t d = dsl[j];
+        const int32_t have = held[j];
+        const int32_t x = have < amt[j] ? have : amt[j];
+        Xb[(int64_t)r * S + s] = x;
+        np[(int64_t)d * R + r] = have - x;
+        amt[j] -= x;
+        const uint64_t bit = 1ull << (r & 63);
+        if (x > 0) {
+          L.price[r] = L.price[r] + step;
+          if (track) {
+            const int32_t c0 = L.cnt[r], c1 = c0 + 1;
+            L.cnt[r] = c1;
+            newmax = c1 > newmax ? c1 : newmax;
+            for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
+              atomicXor(reinterpret_cast<unsigned long long*>(
+                            &L.planes[__builtin_ctz(flip) * kTierWords + (r >> 6)]),
+                        bit);
           }
-          if (have - x <= 0)
-            atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * kTierWords + w]), ~(1ull << lane));
-          did = true;
         }
-        L.rkey[r] = 0;
-        L.rwin[r] = INT_MAX;
+        if (have - x <= 0)
+          atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * kTierWords + (r >> 6)]), ~bit);
+        atomicOr(reinterpret_cast<unsigned long long*>(&L.served[r >> 6]), bit);
+        won |= 1u << j;
       }
-      const uint64_t m = __ballot(did);
-      if (lane == 0) L.served[w] = m;
     }
-    const int32_t m2 = wave_max_i32(newmax);
-    maxc = m2 > maxc ? m2 : maxc;
-    wave_sync();
-    // (d) a slot re-bids if its rank served or ran out of the slot's expert
-    nwork = 0;
-    for (int64_t base = 0; base < S; base += kWave) {
-      const int64_t s = base + lane;
+    newmax = wave_max_i32(newmax);
+    if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
+    __syncthreads();
+    maxc = sh_maxc;
+    // (d) winners clear their rank's key; a slot re-bids if its rank served
+    //     or ran out of the slot's expert
+    need = 0;
+#pragma unroll
+    for (int j = 0; j < SPL; ++j) {
+      const int32_t s = j * kSchThreads + tid;
+      const int32_t r = bid[j];
+      if ((won >> j) & 1u) L.rkey[r] = 0;
       bool f = false;
-      if (s < S) {
-        const int32_t r = L.bid[s];
-        if (L.amt[s] > 0 && r >= 0) {
-          const bool served = (L.served[r >> 6] >> (r & 63)) & 1ull;
-          const bool valid = (L.vmask[L.dsl[s] * kTierWords + (r >> 6)] >> (r & 63)) & 1ull;
-          f = served || !valid;
-        }
+      if (amt[j] > 0 && r >= 0) {
+        const bool served = (L.served[r >> 6] >> (r & 63)) & 1ull;
+        const bool valid = (L.vmask[dsl[j] * kTierWords + (r >> 6)] >> (r & 63)) & 1ull;
+        f = served || !valid;
       }
-      const uint64_t m = __ballot(f);
-      if (f) L.work[nwork + __popcll(m & below)] = (int32_t)s;
-      nwork += __popcll(m);
+      list_append(f, (dsl[j] << 16) | s, L.work, &sh_nwork);
+      need |= f ? 1u << j : 0u;
     }
-    wave_sync();
+    __syncthreads();
+    nwork = sh_nwork;
     rounds = t;
   }
 
   int64_t left = 0;
-  for (int64_t s = lane; s < S; s += kWave) left += L.amt[s];
+#pragma unroll
+  for (int j = 0; j < SPL; ++j) left += amt[j];
   left = wave_sum_i64(left);
-  if (lane == 0) {
-    p.unfilled[b] = left;
+  __syncthreads();
+  if (tid == 0) sh_sum = 0;
+  __syncthreads();
+  if (lane == 0) atomicAdd(&sh_sum, (unsigned long long)left);
+  __syncthreads();
+  if (tid == 0) {
+    const int64_t tot = (int64_t)sh_sum;
+    p.unfilled[b] = tot;
     if (p.rounds_used) { p.rounds_used[2 * b] = used2; p.rounds_used[2 * b + 1] = (int32_t)rounds; }
-    if (p.status) p.status[b] = left > 0 ? TAOT_ST_UNFILLED : 0u;
+    if (p.status) p.status[b] = tot > 0 ? TAOT_ST_UNFILLED : 0u;
     wp.fallback[b] = 0;
   }
 }
@@ -999,6 +1103,7 @@ struct SchWs {
   int32_t* sidx;       // [R]
   int32_t* cn;         // [kStructCap]
   double* cv;          // [kStructCap][kTierMax]
+  int32_t* cvr;        // [kStructCap][kTierMax]
   uint64_t* cm;        // [kStructCap][kTierMax][kTierWords]
   int32_t* hdr;        // [2]
   int32_t* nprime;     // [B][kDistinctCap][R]
@@ -1018,6 +1123,7 @@ SchWs carve_sched(void* ws, int32_t B, int32_t R, int32_t E, int32_t K) {
   w.sidx = c.take<int32_t>((size_t)R);
   w.cn = c.take<int32_t>(kStructCap);
   w.cv = c.take<double>(kStructCap * kTierMax);
+  w.cvr = c.take<int32_t>(kStructCap * kTierMax);
   w.cm = c.take<uint64_t>(kStructCap * kTierMax * kTierWords);
   w.hdr = c.take<int32_t>(2);
   w.nprime = c.take<int32_t>((size_t)B * kDistinctCap * R);
@@ -1025,7 +1131,13 @@ SchWs carve_sched(void* ws, int32_t B, int32_t R, int32_t E, int32_t K) {
   return w;
 }
 
-constexpr size_t kWaveLdsMax = 64 * 1024;  // keep several problems resident per CU
+constexpr size_t kLdsMax = 64 * 1024;
+
+template <int SPL>
+taot_status launch_lds(const LdsParams& wp, int32_t B, size_t lds, hipStream_t stream) {
+  hipLaunchKernelGGL(schedule_lds_kernel<SPL>, dim3((unsigned)B), dim3(kSchThreads), lds, stream, wp);
+  return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
+}
 
 }  // namespace
 
@@ -1042,21 +1154,24 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
   SchWs w = carve_sched(ws, B, R, E, K);
   SchParams p{n, spill, spare, excess, alpha, home, T, Bpref, Bauct, B, R, E, K, price_step, t_max,
               slot_expert, slot_amount, X, unfilled, rounds_used, status, w.slab, w.slab_bytes, w.fallback};
-  // one-wave path when its LDS layout fits
+  // LDS-resident path when its layout fits
   const int32_t NEC = E < 512 ? E : 512;
   const int64_t S = (int64_t)R * K;
-  const size_t wlds = carve_wave(nullptr, R, K, NEC).bytes;
-  const bool wave_ok = R <= kTierWords * kWave && S > 0 && S <= 65536 && wlds <= kWaveLdsMax;
-  if (wave_ok) {
+  const size_t slds = carve_lds(nullptr, R, K, NEC).bytes;
+  const bool lds_ok = R <= kTierWords * kWave && S > 0 && S <= kMaxSlots && slds <= kLdsMax;
+  if (lds_ok) {
     hipLaunchKernelGGL(auction_tiers_kernel, dim3((unsigned)R), dim3(256), 0, stream, Bauct, R, w.ntier, w.tv,
                        w.tmask);
     if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
     hipLaunchKernelGGL(auction_struct_kernel, dim3(1), dim3(256), 0, stream, w.ntier, w.tv, w.tmask, R, S,
-                       price_step, w.sidx, w.cn, w.cv, w.cm, w.hdr);
+                       price_step, w.sidx, w.cn, w.cv, w.cvr, w.cm, w.hdr);
     if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-    WaveParams wp{p, w.sidx, w.cn, w.cv, w.cm, w.hdr, w.fallback, w.nprime, NEC};
-    hipLaunchKernelGGL(schedule_wave_kernel, dim3((unsigned)B), dim3(kWave), wlds, stream, wp);
-    if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+    const LdsParams wp{p, w.sidx, w.cn, w.cv, w.cvr, w.cm, w.hdr, w.fallback, w.nprime, NEC};
+    taot_status st;
+    if (S <= 256) st = launch_lds<1>(wp, B, slds, stream);
+    else if (S <= 512) st = launch_lds<2>(wp, B, slds, stream);
+    else st = launch_lds<4>(wp, B, slds, stream);
+    if (st != TAOT_OK) return st;
   } else {
     p.fallback = nullptr;  // the general kernel takes every problem
   }
