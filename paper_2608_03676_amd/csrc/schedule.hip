@@ -590,9 +590,9 @@ struct LdsState {
   int32_t* hce; double* den; int32_t* cr; int32_t* spare_p; int32_t* matched; int32_t* prop_e;
   double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
   // Phase 3 (aliases the Phase-2 region)
-  double* price; uint32_t* rkey; uint64_t* served; int32_t* work; uint32_t* wres;
+  double* price; uint32_t* rkey; int32_t* work;
   uint64_t* vmask; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
-  int32_t* sidx; int32_t* cn; double* cv; int32_t* cvr; uint64_t* cm;
+  int32_t* cn; double* cv; int32_t* cvr; uint64_t* cm;
   size_t bytes;
 };
 
@@ -615,12 +615,12 @@ __host__ __device__ inline LdsState carve_lds(char* base, int32_t R, int32_t K, 
   w.spill_p = (int32_t*)take(4 * N_); w.ekey = (uint64_t*)take(8 * N_); w.ewin = (int32_t*)take(4 * N_);
   const size_t end2 = off;
   off = split;
-  w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(4 * R_);
-  w.served = (uint64_t*)take(8 * kTierWords); w.work = (int32_t*)take(4 * S1); w.wres = (uint32_t*)take(4 * S1);
+  w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
+  w.work = (int32_t*)take(2 * 4 * S1);
   w.vmask = (uint64_t*)take(8 * (size_t)kDistinctCap * kTierWords);
   w.dexp = (int32_t*)take(4 * kDistinctCap); w.dmap = (int32_t*)take(4 * N_);
   w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * kPlanes * kTierWords);
-  w.sidx = (int32_t*)take(4 * R_); w.cn = (int32_t*)take(4 * kStructCap);
+  w.cn = (int32_t*)take(4 * kStructCap);
   w.cv = (double*)take(8 * kStructCap * kTierMax); w.cvr = (int32_t*)take(4 * kStructCap * kTierMax);
   w.cm = (uint64_t*)take(8 * kStructCap * kTierMax * kTierWords);
   w.bytes = end2 > off ? end2 : off;
@@ -654,7 +654,7 @@ __device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
 }
 
 // Appends the flagged items of a wave to a list whose length lives in LDS
-// (*count); the order of the list is unspecified.
+// (*count); the order of the list is unspecified.  All lanes must call it.
 __device__ __forceinline__ void list_append(bool flag, int32_t item, int32_t* list, int32_t* count) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t m = __ballot(flag);
@@ -680,7 +680,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
   extern __shared__ __attribute__((aligned(16))) char lds_dyn[];
   __shared__ int32_t wave_cnt[kSchWaves];
   __shared__ int32_t flagbuf[2 * kSchWaves];
-  __shared__ int32_t sh_nwork, sh_maxc;
+  __shared__ int32_t sh_maxc, sh_nw[2];
   __shared__ unsigned long long sh_sum, sh_big;
   const SchParams& p = wp.s;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
@@ -710,7 +710,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
     const int32_t h = p.home[e];
     badh |= h < 0 || h >= R;
   }
-  if (tid == 0) { sh_sum = 0; sh_big = 0; sh_maxc = 0; sh_nwork = 0; }
+  if (tid == 0) { sh_sum = 0; sh_big = 0; sh_maxc = 0; }
   if (block_or(badh, flagbuf, parity)) {
     for (int32_t s = tid; s < S; s += kSchThreads) { se[s] = -1; sa[s] = 0; }
     for (int64_t q = tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
@@ -786,25 +786,25 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
           const int32_t* asg = L.assigned + rc * K;
           const int32_t a0 = k > 0 ? asg[0] : -1, a1 = k > 1 ? asg[1] : -1;
           const int32_t a2_ = k > 2 ? asg[2] : -1, a3 = k > 3 ? asg[3] : -1;
-          for (int32_t ec0 = 0; ec0 < ne; ec0 += 8) {
-            int32_t sl[8], hh[8];
-            double bp[8];
-            float tt[8];
+          for (int32_t ec0 = 0; ec0 < ne; ec0 += 4) {
+            int32_t sl[4], hh[4];
+            double bp[4];
+            float tt[4];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < 4; ++u) {
               const bool in = ec0 + u < ne;
               sl[u] = in ? L.spill_p[ec0 + u] : 0;
               hh[u] = in ? L.hce[ec0 + u] : r;
             }
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < 4; ++u) {
               const bool ok = sl[u] > 0 && hh[u] != r;
               const int64_t o = (int64_t)hh[u] * R + r;
               bp[u] = ok ? p.Bpref[o] : 0.0;
               tt[u] = ok ? Tb[o] : 0.f;
             }
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < 4; ++u) {
               const int32_t ec = ec0 + u;
               if (sl[u] <= 0 || hh[u] == r) continue;
               bool taken = ec == a0 || ec == a1 || ec == a2_ || ec == a3;
@@ -893,29 +893,23 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
     const uint64_t m = __ballot(v > 0);
     if (lane == 0) L.vmask[d * kTierWords + wid] = m;
   }
-  // slot state in registers; every open slot bids in the first round
-  int32_t amt[SPL], bid[SPL], dsl[SPL];
-  uint32_t key[SPL];
-  uint32_t need = 0;
-#pragma unroll
-  for (int j = 0; j < SPL; ++j) {
-    const int32_t s = j * kSchThreads + tid;
+  // the active-slot list of the first round: every slot with tokens planned;
+  // an entry packs (slot, slot-expert index, host tier structure)
+  if (tid < 2) sh_nw[tid] = 0;
+  __syncthreads();
+  for (int32_t base = 0; base < S; base += kSchThreads) {
+    const int32_t s = base + tid;
     const int32_t ec = s < S ? L.slot_ec[s] : -1;
-    dsl[j] = ec >= 0 ? L.dmap[ec] : -1;
-    amt[j] = ec >= 0 ? L.amt[s] : 0;
-    bid[j] = -1;
-    key[j] = 0;
-    const bool f = amt[j] > 0;
-    list_append(f, (dsl[j] << 16) | s, L.work, &sh_nwork);
-    need |= f ? 1u << j : 0u;
+    const bool f = ec >= 0 && L.amt[s] > 0;
+    const int32_t item = f ? s | (L.dmap[ec] << 10) | (wp.sidx[s / K] << 16) : 0;
+    list_append(f, item, L.work + S, &sh_nw[1]);  // the list of round 1 (odd)
   }
   for (int32_t r = tid; r < R; r += kSchThreads) {
     L.price[r] = 0.0;
     L.rkey[r] = 0;
+    L.rkey[R + r] = 0;
     L.cnt[r] = 0;
-    L.sidx[r] = wp.sidx[r];
   }
-  if (tid < kTierWords) L.served[tid] = 0ull;
   for (int32_t q = tid; q < kPlanes * kTierWords; q += kSchThreads) L.planes[q] = 0ull;
   const int32_t ns = wp.hdr[0];
   for (int32_t q = tid; q < ns; q += kSchThreads) L.cn[q] = wp.cn[q];
@@ -936,144 +930,160 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
   }
   __syncthreads();
 
+  // Every bid names a rank, which then serves its best bidder with a positive
+  // amount; so every open slot with a valid rank bids again in every round,
+  // and the auction keeps a list of them.  A round is two steps, one barrier
+  // each, with the list and the rank keys in two buffers by round parity:
+  //   X: each listed slot bids and posts its key to the rank it bid for;
+  //   Y: the same thread moves tokens if its slot won, and keeps the slot on
+  //      next round's list while it still plans tokens.
   const double step = p.price_step;
   const bool track = step > 0.0;  // counts order the prices; with step 0 all prices stay 0
-  int32_t nwork = sh_nwork;
-  int32_t maxc = 0;               // largest service count so far
   const int64_t tmax = p.t_max > 0 ? p.t_max : (int64_t)S * (R + 1);
   int64_t rounds = 0;
   for (int64_t t = 1; t <= tmax; ++t) {
-    // (a) bids of the listed slots: argmax over ranks holding tokens of the
-    //     slot's expert of Bauct[r][host] - price[r], lowest rank on ties
+    const int cur = (int)(t & 1), prv = cur ^ 1;
+    uint32_t* rk = L.rkey + cur * R;
+    const int32_t* list = L.work + cur * S;
+    const int32_t nw = sh_nw[cur];
+    const int32_t maxc = sh_maxc;
     const int32_t nplanes = maxc > 0 ? 32 - __builtin_clz((uint32_t)maxc) : 0;
-    for (int32_t q = tid; q < nwork; q += kSchThreads) {
-      const int32_t item = L.work[q];
-      const int32_t s = item & 0xFFFF, d = item >> 16;
-      const int32_t st = L.sidx[s / K];
-      const int32_t nt = L.cn[st];
-      const uint64_t* vm = L.vmask + d * kTierWords;
-      uint64_t valid[kTierWords];
-#pragma unroll
-      for (int w = 0; w < kTierWords; ++w) valid[w] = vm[w];
-      double bs = -INFINITY;
-      int32_t br = INT_MAX, bv = 0;
-      for (int32_t ti = 0; ti < nt; ++ti) {
-        const double v = L.cv[st * kTierMax + ti];
-        if (v < bs) break;  // every score in this tier and the next is <= v
-        const uint64_t* tm = L.cm + (st * kTierMax + ti) * kTierWords;
-        uint64_t c[kTierWords];
-        uint64_t any = 0;
-#pragma unroll
-        for (int w = 0; w < kTierWords; ++w) { c[w] = tm[w] & valid[w]; any |= c[w]; }
-        if (!any) continue;
-        // fewest services: keep the ranks with a 0 in each bit-plane, top down,
-        // whenever any remain
-        for (int32_t j = nplanes - 1; j >= 0; --j) {
-          uint64_t m[kTierWords];
-          uint64_t mm = 0;
-#pragma unroll
-          for (int w = 0; w < kTierWords; ++w) { m[w] = c[w] & ~L.planes[j * kTierWords + w]; mm |= m[w]; }
-          if (mm) {
-#pragma unroll
-            for (int w = 0; w < kTierWords; ++w) c[w] = m[w];
-          }
-        }
-        int32_t r = INT_MAX;
-#pragma unroll
-        for (int w = kTierWords - 1; w >= 0; --w)
-          if (c[w]) r = w * kWave + __builtin_ctzll(c[w]);
-        const double sc = v - L.price[r];
-        if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; bv = L.cvr[st * kTierMax + ti]; }
-      }
-      L.wres[s] = br == INT_MAX ? 0u : ((uint32_t)bv << 16) | (uint32_t)(br + 1);
-    }
-    __syncthreads();
-    // (b) owners take their new bids and post each to its rank: the key orders
-    //     by bonus, then by lowest slot
-    if (tid == 0) sh_nwork = 0;
-    if (tid < kTierWords) L.served[tid] = 0ull;
+    if (tid == 0) sh_nw[prv] = 0;
+    for (int32_t r = tid; r < R; r += kSchThreads) L.rkey[prv * R + r] = 0;
+    // ---- X: bids --------------------------------------------------------------------------
+    int32_t item[SPL], bid[SPL], held[SPL];
+    uint32_t key[SPL];
     bool any = false;
 #pragma unroll
-    for (int j = 0; j < SPL; ++j) {
-      const int32_t s = j * kSchThreads + tid;
-      if ((need >> j) & 1u) {
-        const uint32_t w = L.wres[s];
-        bid[j] = w ? (int32_t)(w & 0xFFFFu) - 1 : -1;
-        key[j] = (w & 0xFFFF0000u) | (uint32_t)(0xFFFF - s);
+    for (int i = 0; i < SPL; ++i) {
+      const int32_t q = i * kSchThreads + tid;
+      item[i] = -1;
+      bid[i] = -1;
+      key[i] = 0;
+      held[i] = 0;
+      if (q >= nw) continue;
+      const int32_t it = list[q];
+      item[i] = it;
+      const int32_t s = it & 1023, d = (it >> 10) & 63, st = it >> 16;
+      // argmax over ranks holding tokens of the slot's expert of
+      // Bauct[r][host] - price[r], lowest rank on ties, by tiers
+      const int32_t nt = L.cn[st];
+      uint64_t valid[kTierWords];
+      double tvv[kTierMax];
+#pragma unroll
+      for (int w = 0; w < kTierWords; ++w) valid[w] = L.vmask[d * kTierWords + w];
+#pragma unroll
+      for (int ti = 0; ti < kTierMax; ++ti) tvv[ti] = L.cv[st * kTierMax + ti];
+      double bs = -INFINITY;
+      int32_t br = INT_MAX, bv = 0;
+#pragma unroll
+      for (int ti = 0; ti < kTierMax; ++ti) {
+        if (ti >= nt || tvv[ti] < bs) break;  // every score in this tier and the next is <= its bonus
+        const uint64_t* tm = L.cm + (st * kTierMax + ti) * kTierWords;
+        uint64_t c[kTierWords];
+        uint32_t wm = 0;  // words holding candidates
+#pragma unroll
+        for (int w = 0; w < kTierWords; ++w) {
+          c[w] = tm[w] & valid[w];
+          wm |= (c[w] != 0ull ? 1u : 0u) << w;
+        }
+        if (!wm) continue;
+        int32_t r;
+        if ((wm & (wm - 1)) == 0) {
+          // candidates within one 64-rank word (always so for tiers that are
+          // aligned groups of at most 64 ranks)
+          const int w = __builtin_ctz(wm);
+          uint64_t x = w == 0 ? c[0] : w == 1 ? c[1] : w == 2 ? c[2] : c[3];
+          if (track && (x & (x - 1))) {
+            // fewest services: keep the ranks with a 0 in each bit-plane, top
+            // down, whenever any remain (four planes per load batch)
+            for (int32_t j0 = nplanes - 1; j0 >= 0; j0 -= 4) {
+              uint64_t pl[4];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) pl[u] = j0 - u >= 0 ? L.planes[(j0 - u) * kTierWords + w] : 0ull;
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                const uint64_t m = x & ~pl[u];
+                x = m ? m : x;
+              }
+            }
+          }
+          r = w * kWave + __builtin_ctzll(x);
+        } else {
+          if (track) {
+            // the same over all words
+            for (int32_t j = nplanes - 1; j >= 0; --j) {
+              uint64_t m[kTierWords];
+              uint64_t mm = 0;
+#pragma unroll
+              for (int w = 0; w < kTierWords; ++w) { m[w] = c[w] & ~L.planes[j * kTierWords + w]; mm |= m[w]; }
+              if (mm) {
+#pragma unroll
+                for (int w = 0; w < kTierWords; ++w) c[w] = m[w];
+              }
+            }
+          }
+          r = INT_MAX;
+#pragma unroll
+          for (int w = kTierWords - 1; w >= 0; --w)
+            if (c[w]) r = w * kWave + __builtin_ctzll(c[w]);
+        }
+        const double sc = tvv[ti] - L.price[r];
+        if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; bv = L.cvr[st * kTierMax + ti]; }
       }
-      if (amt[j] > 0 && bid[j] >= 0) {
-        atomicMax(&L.rkey[bid[j]], key[j]);
+      if (br != INT_MAX) {
+        bid[i] = br;
+        key[i] = ((uint32_t)bv << 16) | (uint32_t)(0xFFFF - s);  // bonus, then lowest slot
+        held[i] = np[(int64_t)d * R + br];
+        atomicMax(&rk[br], key[i]);
         any = true;
       }
     }
     if (!block_or(any, flagbuf, parity)) break;  // no bid: the state is final
-    // (c) each rank's winner moves min(tokens held, tokens planned); a rank
-    //     that moved tokens raises its price
-    int32_t held[SPL];
-#pragma unroll
-    for (int j = 0; j < SPL; ++j)  // issued before the winners are known
-      held[j] = amt[j] > 0 && bid[j] >= 0 ? np[(int64_t)dsl[j] * R + bid[j]] : 0;
-    uint32_t won = 0;
+    // ---- Y: transfers -----------------------------------------------------------------------
     int32_t newmax = 0;
 #pragma unroll
-    for (int j = 0; j < SPL; ++j) {
-      const int32_t r = bid[j];
-      if (amt[j] > 0 && r >= 0 && L.rkey[r] == key[j]) {
-        const int32_t s = j * kSchThreads + tid;
-        const int32_t d = dsl[j];
-        const int32_t have = held[j];
-        const int32_t x = have < amt[j] ? have : amt[j];
-        Xb[(int64_t)r * S + s] = x;
-        np[(int64_t)d * R + r] = have - x;
-        amt[j] -= x;
-        const uint64_t bit = 1ull << (r & 63);
-        if (x > 0) {
-          L.price[r] = L.price[r] + step;
-          if (track) {
-            const int32_t c0 = L.cnt[r], c1 = c0 + 1;
-            L.cnt[r] = c1;
-            newmax = c1 > newmax ? c1 : newmax;
-            for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
-              atomicXor(reinterpret_cast<unsigned long long*>(
-                            &L.planes[__builtin_ctz(flip) * kTierWords + (r >> 6)]),
-                        bit);
+    for (int i = 0; i < SPL; ++i) {
+      const int32_t r = bid[i];
+      bool keep = false;
+      if (r >= 0) {
+        const int32_t s = item[i] & 1023, d = (item[i] >> 10) & 63;
+        int32_t a = L.amt[s];
+        if (rk[r] == key[i]) {
+          const int32_t have = held[i];
+          const int32_t x = have < a ? have : a;
+          Xb[(int64_t)r * S + s] = x;
+          np[(int64_t)d * R + r] = have - x;
+          a -= x;
+          L.amt[s] = a;
+          const uint64_t bit = 1ull << (r & 63);
+          if (x > 0) {
+            L.price[r] = L.price[r] + step;
+            if (track) {
+              const int32_t c0 = L.cnt[r], c1 = c0 + 1;
+              L.cnt[r] = c1;
+              newmax = c1 > newmax ? c1 : newmax;
+              for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
+                atomicXor(reinterpret_cast<unsigned long long*>(
+                              &L.planes[__builtin_ctz(flip) * kTierWords + (r >> 6)]),
+                          bit);
+            }
           }
+          if (have - x <= 0)
+            atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * kTierWords + (r >> 6)]), ~bit);
         }
-        if (have - x <= 0)
-          atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * kTierWords + (r >> 6)]), ~bit);
-        atomicOr(reinterpret_cast<unsigned long long*>(&L.served[r >> 6]), bit);
-        won |= 1u << j;
+        keep = a > 0;
       }
+      list_append(keep, item[i], L.work + prv * S, &sh_nw[prv]);
     }
     newmax = wave_max_i32(newmax);
     if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
     __syncthreads();
-    maxc = sh_maxc;
-    // (d) winners clear their rank's key; a slot re-bids if its rank served
-    //     or ran out of the slot's expert
-    need = 0;
-#pragma unroll
-    for (int j = 0; j < SPL; ++j) {
-      const int32_t s = j * kSchThreads + tid;
-      const int32_t r = bid[j];
-      if ((won >> j) & 1u) L.rkey[r] = 0;
-      bool f = false;
-      if (amt[j] > 0 && r >= 0) {
-        const bool served = (L.served[r >> 6] >> (r & 63)) & 1ull;
-        const bool valid = (L.vmask[dsl[j] * kTierWords + (r >> 6)] >> (r & 63)) & 1ull;
-        f = served || !valid;
-      }
-      list_append(f, (dsl[j] << 16) | s, L.work, &sh_nwork);
-      need |= f ? 1u << j : 0u;
-    }
-    __syncthreads();
-    nwork = sh_nwork;
     rounds = t;
   }
 
   int64_t left = 0;
-#pragma unroll
-  for (int j = 0; j < SPL; ++j) left += amt[j];
+  for (int32_t s = tid; s < S; s += kSchThreads) left += L.slot_ec[s] >= 0 ? L.amt[s] : 0;
   left = wave_sum_i64(left);
   __syncthreads();
   if (tid == 0) sh_sum = 0;
@@ -1155,7 +1165,7 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
   SchParams p{n, spill, spare, excess, alpha, home, T, Bpref, Bauct, B, R, E, K, price_step, t_max,
               slot_expert, slot_amount, X, unfilled, rounds_used, status, w.slab, w.slab_bytes, w.fallback};
   // LDS-resident path when its layout fits
-  const int32_t NEC = E < 512 ? E : 512;
+  const int32_t NEC = E < 256 ? E : 256;  // candidate experts (spill > 0) held in LDS
   const int64_t S = (int64_t)R * K;
   const size_t slds = carve_lds(nullptr, R, K, NEC).bytes;
   const bool lds_ok = R <= kTierWords * kWave && S > 0 && S <= kMaxSlots && slds <= kLdsMax;
