@@ -33,7 +33,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--K", type=int, default=None, help="guest slots per rank (default: the workload's)")
-    ap.add_argument("--cpu-sample", type=int, default=24, help="problems in the oracle CPU baseline (0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=32, help="problems in the oracle CPU baseline (0: skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="oracle Sinkhorn passes over the sample repeat until this much time has passed")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (HBM counter calibration)")
     ap.add_argument("--json-out", default=None)
     return ap.parse_args()
 
@@ -42,8 +46,55 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+PLAN_LOADS_SOURCES = ["paper_2608_03676_amd/csrc/loads.hip", "paper_2608_03676_amd/csrc/common.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "plan_loads_workload3_traffic.txt")
+
+
+def sources_digest(paths):
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per plan_loads step from the committed counter summary, or
+    None when it is for another workload or the kernels changed since."""
+    if workload != 3 or not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("source_sha256") != sources_digest(PLAN_LOADS_SOURCES):
+        return None
+    try:
+        return float(fields["traffic_bytes_per_step"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib):
+    import torch
+    n = mib * 2**20 // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4,
+                      "launches": 5}), flush=True)
+
+
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: the planner's problems are independent and "
               f"this build has no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
@@ -151,14 +202,15 @@ def main():
     for s in stage.values():
         if "peak" in s:
             s["frac"] = s["achieved"] / s["peak"]
-    dom_name = max(stage, key=lambda k: stage[k]["ms"])
+    # roofline of the longest stage that has one (the schedule is a chain of
+    # dependent rounds: latency, not bandwidth or ALU, bounds it)
+    dom_name = max(("plan_loads", "sinkhorn"), key=lambda k: stage[k]["ms"])
     dom = stage[dom_name]
-    if dom["bound"] == "latency":
-        # no roofline for a dependent-round kernel: report the largest bandwidth/ALU stage
-        dom_name = max(("plan_loads", "sinkhorn"), key=lambda k: stage[k]["ms"])
-        dom = stage[dom_name]
-    roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
-                "unit": dom["unit"], "frac": dom["frac"], "traffic": None}
+    kernels = {"plan_loads": "histogram_kernel + marginals_kernel (taot_plan_loads)",
+               "sinkhorn": "sinkhorn_wave_kernel (taot_sinkhorn_batched)"}
+    traffic = measured_traffic(w.index) if dom_name == "plan_loads" else None
+    roofline = {"kernel": kernels[dom_name], "bound": dom["bound"], "achieved": dom["achieved"],
+                "peak": dom["peak"], "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
 
     value = B * w.iters / (mean(sk_ms) * 1e-3)
     rec = {
@@ -177,36 +229,56 @@ def main():
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----------
     if args.cpu_sample > 0:
-        import oracle as O
-        sample = list(range(0, B, max(1, B // args.cpu_sample)))[: args.cpu_sample]
-        host_ids = np.stack([W.problem_ids_host(w, b) for b in sample])
-        cores = int(os.environ.get("OMP_NUM_THREADS", 0) or os.cpu_count())
-        t = time.time()
-        Lo = O.plan_loads(host_ids, home_np, E)
-        t_loads = time.time() - t
-        t = time.time()
-        Po = O.sinkhorn(Lo.excess.astype(float), Lo.spare.astype(float), C_np.astype(float), w.eps, w.iters)
-        t_sk = time.time() - t
-        t = time.time()
-        se, sa, _ = O.phase2(Lo.spill, Lo.spare, Lo.excess, Lo.alpha, home_np, Po.T.astype(np.float32), Bp_np, K)
-        O.phase3(Lo.n, se, sa, Ba_np, K, w.price_step)
-        t_sch = time.time() - t
-        del host_ids
-        per_problem_s = (t_loads + t_sk + t_sch) / len(sample)
-        rec["cpu_baseline"] = {
-            "value": len(sample) * w.iters / t_sk, "unit": "problem-iters/s", "cores": cores, "kind": "oracle",
-            "sample": f"{len(sample)} of {B} problems (every {max(1, B // args.cpu_sample)}th), full iteration count; "
-                      f"fp64 C oracle, OpenMP over problems",
-            "planner_ms_per_step_extrapolated": per_problem_s * B * 1e3,
-            "stage_s": {"plan_loads": t_loads, "sinkhorn": t_sk, "schedule": t_sch},
-        }
-        log(f"[bench] oracle sample {len(sample)} problems on {cores} cores: loads {t_loads:.1f}s "
-            f"sinkhorn {t_sk:.1f}s schedule {t_sch:.1f}s")
+        rec["cpu_baseline"] = cpu_baseline(w, K, args, home_np, C_np, Bp_np, Ba_np)
     line = json.dumps(rec)
     print(line, flush=True)
     if args.json_out:
         with open(args.json_out, "w") as fh:
             fh.write(line + "\n")
+
+
+def cpu_baseline(w, K, args, home_np, C_np, Bp_np, Ba_np):
+    """The oracle, as it is, on a sample of the workload's problems: ids made
+    on the host, plan_loads, then Sinkhorn passes over the sample until
+    --cpu-seconds have passed, then Phases 2-3 once."""
+    import numpy as np
+
+    import oracle as O
+    import workloads as W
+    B = w.B
+    stride = max(1, B // args.cpu_sample)
+    sample = list(range(0, B, stride))[: args.cpu_sample]
+    threads = O.max_threads()
+    t = time.time()
+    parts = []
+    for b in sample:  # one problem of ids at a time (OpenMP over ranks; the buffer is reused)
+        ids = W.problem_ids_host(w, b)[None]
+        parts.append(O.plan_loads(ids, home_np, w.E))
+        del ids
+    t_gen_loads = time.time() - t
+    cat = lambda f: np.concatenate([getattr(x, f) for x in parts])
+    excess, spare, spill, alpha, n = cat("excess"), cat("spare"), cat("spill"), cat("alpha"), cat("n")
+    a, b, Cd = excess.astype(float), spare.astype(float), C_np.astype(float)
+    passes, t_sk = 0, 0.0
+    while t_sk < args.cpu_seconds or passes == 0:
+        t = time.time()
+        Po = O.sinkhorn(a, b, Cd, w.eps, w.iters)
+        t_sk += time.time() - t
+        passes += 1
+    t = time.time()
+    se, sa, _ = O.phase2(spill, spare, excess, alpha, home_np, Po.T.astype(np.float32), Bp_np, K)
+    O.phase3(n, se, sa, Ba_np, K, w.price_step)
+    t_sch = time.time() - t
+    used = min(threads, len(sample))
+    log(f"[bench] oracle on {len(sample)} problems, {used} threads: ids + plan_loads {t_gen_loads:.1f}s, "
+        f"sinkhorn {passes} passes {t_sk:.1f}s, schedule {t_sch:.1f}s")
+    return {
+        "value": passes * len(sample) * w.iters / t_sk, "unit": "problem-iters/s", "cores": used, "kind": "oracle",
+        "sample": f"{len(sample)} of {B} problems (every {stride}th), ids generated on the host; fp64 C oracle "
+                  f"Sinkhorn at the full iteration count, {passes} passes over the sample ({t_sk:.1f} s), "
+                  f"OpenMP over problems",
+        "schedule_s_per_problem": t_sch / len(sample),
+    }
 
 
 if __name__ == "__main__":

@@ -33,11 +33,12 @@ def lib():
         L.oracle_sinkhorn.argtypes = [_P, _P, _I32, _I32, _P, _I64, _F64, _I32, _I32, _F64, _I32,
                                       _P, _P, _P, _P, _P]
         L.oracle_topology_pref.argtypes = [_P, _I32, _P, _P]
+        L.oracle_max_threads.argtypes = []
         L.oracle_phase2.argtypes = [_P] * 7 + [_I32] * 4 + [_P] * 3
         L.oracle_phase3.argtypes = [_P] * 4 + [_I32] * 4 + [_F64, _I64] + [_P] * 4
         L.oracle_metrics.argtypes = [_P] * 4 + [_I32] * 5 + [_F64] + [_P] * 5
         for f in (L.oracle_plan_loads, L.oracle_sinkhorn, L.oracle_topology_pref, L.oracle_phase2,
-                  L.oracle_phase3, L.oracle_metrics):
+                  L.oracle_phase3, L.oracle_metrics, L.oracle_max_threads):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -110,6 +111,11 @@ def sinkhorn(a, b, C, eps: float, iters: int, domain: str = "log", tol: float = 
                                out.status.ctypes.data)
     _check(rc, "oracle_sinkhorn")
     return out
+
+
+def max_threads() -> int:
+    """OpenMP threads the oracle's loops over problems may use."""
+    return int(lib().oracle_max_threads())
 
 
 def topology_pref(C):

@@ -24,6 +24,7 @@
  * in the paper, so their exact output is pinned only by invariants, the
  * relaxed-LP upper bound on tiny cases and hand-traced micro-cases.
  */
+#include <omp.h>
 #include "taot_oracle.h"
 
 #include <math.h>
@@ -554,3 +555,5 @@ int oracle_metrics(const int64_t* load, const int32_t* home, const int32_t* slot
   }
   return 0;
 }
+
+int oracle_max_threads(void) { return omp_get_max_threads(); }

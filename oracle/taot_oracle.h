@@ -28,6 +28,9 @@
 extern "C" {
 #endif
 
+/* Threads the OpenMP loops over problems may use (omp_get_max_threads). */
+int oracle_max_threads(void);
+
 /* Sec. 3.1 / A.1: expert-load histogram, rank loads, excess/spare, rho,
  * alpha and the spill of Sec. A.3.
  *   ids   [B][R][N] int32 routing ids (expert chosen by a token of source rank r)

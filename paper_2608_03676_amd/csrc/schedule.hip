@@ -458,15 +458,18 @@ static_assert(kTierWords == kSchWaves, "one wave per 64-rank word");
 __global__ void __launch_bounds__(256)
 auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __restrict__ ntier,
                      double* __restrict__ tv, uint64_t* __restrict__ tmask) {
+  __shared__ double col[kTierWords * kWave];
   __shared__ double vals[kTierMax];
   __shared__ int32_t nv;
   __shared__ unsigned long long msk[kTierMax * kTierWords];
   const int32_t h = blockIdx.x, tid = threadIdx.x;
   if (tid < kTierMax * kTierWords) msk[tid] = 0ull;
+  for (int32_t r = tid; r < R; r += blockDim.x) col[r] = Bauct[(int64_t)r * R + h];
+  __syncthreads();
   if (tid == 0) {
     int32_t n = 0;
     for (int32_t r = 0; r < R && n >= 0; ++r) {
-      const double v = Bauct[(int64_t)r * R + h];
+      const double v = col[r];
       if (v != v || v == -INFINITY) continue;
       int32_t pos = 0;
       bool dup = false;
@@ -485,7 +488,7 @@ auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __res
   __syncthreads();
   const int32_t n = nv;
   for (int32_t r = tid; r < R && n > 0; r += blockDim.x) {
-    const double v = Bauct[(int64_t)r * R + h];
+    const double v = col[r];
     for (int32_t i = 0; i < n; ++i)
       if (vals[i] == v) atomicOr(&msk[i * kTierWords + (r >> 6)], 1ull << (r & 63));
   }
@@ -506,14 +509,22 @@ auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __res
 // max|bonus| + S * step (prices stay below S * step: a rank serves each slot
 // at most once).
 __global__ void __launch_bounds__(256)
-auction_struct_kernel(const int32_t* __restrict__ ntier, const double* __restrict__ tv,
-                      const uint64_t* __restrict__ tmask, int32_t R, int64_t S, double step,
+auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restrict__ tv_g,
+                      const uint64_t* __restrict__ tmask_g, int32_t R, int64_t S, double step,
                       int32_t* __restrict__ sidx, int32_t* __restrict__ cn, double* __restrict__ cv,
                       int32_t* __restrict__ cvr, uint64_t* __restrict__ cm, int32_t* __restrict__ hdr) {
-  __shared__ int32_t first[256];
-  __shared__ double dv[kValueCap];
-  const int32_t h = threadIdx.x;
   constexpr int kRow = kTierMax * kTierWords;
+  constexpr int kMaxR = kTierWords * kWave;
+  __shared__ int32_t ntier[kMaxR], first[kMaxR], sid[kMaxR], tab[kStructCap];
+  __shared__ double tv[kMaxR * kTierMax];
+  __shared__ uint64_t tmask[kMaxR * kRow];
+  __shared__ double dv[kValueCap];
+  __shared__ int32_t sh_ns, sh_ok;
+  const int32_t h = threadIdx.x;
+  for (int32_t q = h; q < R; q += blockDim.x) ntier[q] = ntier_g[q];
+  for (int32_t q = h; q < R * kTierMax; q += blockDim.x) tv[q] = tv_g[q];
+  for (int32_t q = h; q < R * kRow; q += blockDim.x) tmask[q] = tmask_g[q];
+  __syncthreads();
   if (h < R) {
     const int32_t nh = ntier[h];
     int32_t f = h;
@@ -526,59 +537,70 @@ auction_struct_kernel(const int32_t* __restrict__ ntier, const double* __restric
     first[h] = f;
   }
   __syncthreads();
-  if (h != 0) return;
-  int32_t ns = 0, nd = 0;
-  double vm = 0.0;
-  bool ok = true;
-  for (int32_t g = 0; g < R; ++g) {
-    ok &= ntier[g] >= 0;
-    if (first[g] != g) {
-      sidx[g] = sidx[first[g]];
-      continue;
-    }
-    const int32_t nt = ntier[g] > 0 ? ntier[g] : 0;
-    for (int32_t t = 0; t < nt; ++t) {
-      const double v = tv[g * kTierMax + t];
-      ok &= v != INFINITY;
-      vm = fmax(vm, fabs(v));
-    }
-    if (ns < kStructCap) {
-      cn[ns] = nt;
-      for (int32_t t = 0; t < kTierMax; ++t) cv[ns * kTierMax + t] = tv[g * kTierMax + t];
-      for (int32_t q = 0; q < kRow; ++q) cm[ns * kRow + q] = tmask[g * kRow + q];
-      // distinct bonuses of the table, ascending
+  if (h == 0) {
+    int32_t ns = 0, nd = 0;
+    double vm = 0.0;
+    bool ok = true;
+    for (int32_t g = 0; g < R; ++g) {
+      ok &= ntier[g] >= 0;
+      if (first[g] != g) {
+        sid[g] = sid[first[g]];
+        continue;
+      }
+      const int32_t nt = ntier[g] > 0 ? ntier[g] : 0;
       for (int32_t t = 0; t < nt; ++t) {
         const double v = tv[g * kTierMax + t];
-        int32_t pos = 0;
-        bool dup = false;
-        for (int32_t i = 0; i < nd; ++i) {
-          dup |= dv[i] == v;
-          pos += dv[i] < v;
+        ok &= v != INFINITY;
+        vm = fmax(vm, fabs(v));
+      }
+      if (ns < kStructCap) {
+        tab[ns] = g;
+        // distinct bonuses of the table, ascending
+        for (int32_t t = 0; t < nt; ++t) {
+          const double v = tv[g * kTierMax + t];
+          int32_t pos = 0;
+          bool dup = false;
+          for (int32_t i = 0; i < nd; ++i) {
+            dup |= dv[i] == v;
+            pos += dv[i] < v;
+          }
+          if (dup) continue;
+          for (int32_t i = nd; i > pos; --i) dv[i] = dv[i - 1];
+          dv[pos] = v;
+          ++nd;
         }
-        if (dup) continue;
-        for (int32_t i = nd; i > pos; --i) dv[i] = dv[i - 1];
-        dv[pos] = v;
-        ++nd;
+      }
+      sid[g] = ns;
+      ++ns;
+    }
+    ok &= ns <= kStructCap;
+    const double top = vm + (double)S * step * 1.01 + 1.0;
+    const double spacing2 = 2.0 * (nextafter(top, INFINITY) - top);
+    ok &= step == 0.0 || (step > 0.0 && step > spacing2);
+    for (int32_t i = 0; i + 1 < nd; ++i) ok &= dv[i + 1] - dv[i] > spacing2;
+    sh_ns = ns < kStructCap ? ns : kStructCap;
+    sh_ok = ok ? 1 : 0;
+    // bonus ranks of the table's tiers
+    for (int32_t i = 0; i < sh_ns; ++i) {
+      const int32_t g = tab[i];
+      for (int32_t t = 0; t < kTierMax; ++t) {
+        int32_t rank = 0;
+        if (t < ntier[g])
+          while (dv[rank] != tv[g * kTierMax + t]) ++rank;
+        cvr[i * kTierMax + t] = rank;
       }
     }
-    sidx[g] = ns;
-    ++ns;
   }
-  ok &= ns <= kStructCap;
-  const int32_t nsc = ns < kStructCap ? ns : kStructCap;
-  for (int32_t i = 0; i < nsc; ++i)
-    for (int32_t t = 0; t < kTierMax; ++t) {
-      int32_t rank = 0;
-      if (t < cn[i])
-        while (dv[rank] != cv[i * kTierMax + t]) ++rank;
-      cvr[i * kTierMax + t] = rank;
-    }
-  const double top = vm + (double)S * step * 1.01 + 1.0;
-  const double spacing2 = 2.0 * (nextafter(top, INFINITY) - top);
-  ok &= step == 0.0 || (step > 0.0 && step > spacing2);
-  for (int32_t i = 0; i + 1 < nd; ++i) ok &= dv[i + 1] - dv[i] > spacing2;
-  hdr[0] = nsc;
-  hdr[1] = ok ? 1 : 0;
+  __syncthreads();
+  const int32_t ns = sh_ns;
+  for (int32_t q = h; q < R; q += blockDim.x) sidx[q] = sid[q];
+  for (int32_t q = h; q < ns; q += blockDim.x) cn[q] = ntier[tab[q]] > 0 ? ntier[tab[q]] : 0;
+  for (int32_t q = h; q < ns * kTierMax; q += blockDim.x) cv[q] = tv[tab[q / kTierMax] * kTierMax + q % kTierMax];
+  for (int32_t q = h; q < ns * kRow; q += blockDim.x) cm[q] = tmask[tab[q / kRow] * kRow + q % kRow];
+  if (h == 0) {
+    hdr[0] = ns;
+    hdr[1] = sh_ok;
+  }
 }
 
 struct LdsState {
