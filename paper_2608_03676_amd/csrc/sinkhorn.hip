@@ -25,6 +25,8 @@
 // all iterations fused); problems whose block does not fit are flagged and
 // handled by sinkhorn_kernel<true>, which streams Kt through device memory
 // (L2-resident at the sizes used here).
+#include <mutex>
+
 #include "common.h"
 
 namespace taot {
@@ -319,7 +321,9 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+  // every lane has a source lane for the patterns used here, so bound_ctrl
+  // changes nothing but lets the move fold into the add
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, true));
 }
 __device__ __forceinline__ void swap32(float& lo, float& hi) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(lo), __float_as_uint(hi), false, false);
@@ -357,50 +361,47 @@ __device__ __forceinline__ float reduce8(float (&p)[8], int lane) {
   return y;
 }
 
-// Rows kept in registers for a column count: 48 for CPL = 4, all 64 otherwise.
-__host__ __device__ constexpr int reg_chunks(int cpl) { return cpl == 4 ? 6 : 8; }
-
 // Iterations and outputs for one problem of class (CPL, C8); the caller has
 // filled the LDS vectors and the first-update potentials Fl.
 template <int CPL, int C8>
 __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
                                            const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
                                            const int32_t* hidx, const float* sAl, float* Fl, float* ul,
-                                           float* kx, float kappa) {
+                                           float kappa) {
   constexpr int MAXH = 8 * C8;
-  constexpr int RC = C8 < reg_chunks(CPL) ? C8 : reg_chunks(CPL);
-  constexpr int MREG = 8 * RC;  // rows in registers; rows MREG.. live in kx
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
   const int32_t R = p.R;
   const float* bd = p.b + pb * R;
   const float* Cb = p.C + pb * p.C_stride;
 
-  float K[MREG][CPL];
-  // access to row i (static after unrolling) of the lane's columns
-  auto kget = [&](int i, int c) -> float {
-    return i < MREG ? K[i < MREG ? i : 0][c] : kx[((i - MREG) * kWave + lane) * CPL + c];
-  };
-  auto kset = [&](int i, int c, float val) {
-    if (i < MREG) K[i < MREG ? i : 0][c] = val;
-    else kx[((i - MREG) * kWave + lane) * CPL + c] = val;
-  };
+  float K[MAXH][CPL];
+  // row i (static after unrolling) of the lane's columns
+  auto kget = [&](int i, int c) -> float { return K[i][c]; };
+  auto kset = [&](int i, int c, float val) { K[i][c] = val; };
 
   // per-lane column state; the column ids and validity are recomputed from
   // LDS / the lane index where needed to keep the kernel within 256 VGPRs
 #define CV(c) (lane + kWave * (c) < nc)
 #define CJ(c) (CV(c) ? cidx[lane + kWave * (c)] : 0)
-  float sB[CPL], G[CPL], v[CPL];
+  // xb / yb are 1 for padding columns / rows and 0 otherwise: added to the
+  // sums of zero padding they keep the scalings finite (0) without selects,
+  // and added to the scalings they keep padding inside the range check
+  float sB[CPL], G[CPL], v[CPL], xb[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
     sB[c] = CV(c) ? bd[CJ(c)] : 0.f;
     G[c] = 0.f;
     v[c] = CV(c) ? 1.f : 0.f;
+    xb[c] = CV(c) ? 0.f : 1.f;
   }
   // row-owned values: lane l carries row 8q + (l >> 3) of chunk q
 #define RV(q) (8 * (q) + (lane >> 3) < nh)
-  float uq[C8];
+  float uq[C8], yb[C8];
 #pragma unroll
-  for (int q = 0; q < C8; ++q) uq[q] = RV(q) ? 1.f : 0.f;
+  for (int q = 0; q < C8; ++q) {
+    uq[q] = RV(q) ? 1.f : 0.f;
+    yb[q] = RV(q) ? 0.f : 1.f;
+  }
 #pragma unroll
   for (int i = 0; i < MAXH; ++i) {
     if (i < nh) {
@@ -417,7 +418,7 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
   for (int32_t it = 1; it <= p.iters; ++it) {
     if (it > 1) {
       // ---- row half-step: u_i = s~_i / sum_c Kt_ic v_c ------------------------------
-      bool fail = false;
+      uint32_t lo = 0xFFFFFFFFu, hi = 0u;  // range of the scalings' bit patterns
 #pragma unroll
       for (int q = 0; q < C8; ++q) {
         float pp[8];
@@ -429,11 +430,14 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
           pp[r] = acc;
         }
         const float y = reduce8(pp, lane);
-        const bool rv = RV(q);
-        const float un = (rv ? sAl[8 * q + (lane >> 3)] : 0.f) * frcp(y);
-        fail |= rv && !(un >= kLo && un <= kHi);
-        uq[q] = rv ? un : 0.f;
+        const float un = sAl[8 * q + (lane >> 3)] * frcp(y + yb[q]);
+        const uint32_t bits = __float_as_uint(un + yb[q]);
+        lo = bits < lo ? bits : lo;
+        hi = bits > hi ? bits : hi;
+        uq[q] = un;
       }
+      // outside [kLo, kHi], negative, infinite or NaN
+      const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
       if (__ballot(fail) != 0) {
         // exact log-domain update of every row, absorbed into F
 #pragma unroll
@@ -460,13 +464,13 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
         }
 #pragma unroll
         for (int q = 0; q < C8; ++q) uq[q] = RV(q) ? 1.f : 0.f;
-        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
       }
     }
     // ---- column half-step: v_c = d_c / sum_i u_i Kt_ic -------------------------------
     float x[CPL];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) x[c] = 0.f;
+    for (int c = 0; c < CPL; ++c) x[c] = xb[c];
 #pragma unroll
     for (int q = 0; q < C8; ++q) {
       // broadcast the chunk's row scalings first so that each FMA sits far
@@ -479,13 +483,16 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
 #pragma unroll
         for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], kget(8 * q + r, c), x[c]);
     }
-    bool failc = false;
+    uint32_t clo = 0xFFFFFFFFu, chi = 0u;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const float vn = sB[c] * frcp(x[c]);
-      failc |= CV(c) && !(vn >= kLo && vn <= kHi);
-      v[c] = CV(c) ? vn : 0.f;
+      const uint32_t bits = __float_as_uint(vn + xb[c]);
+      clo = bits < clo ? bits : clo;
+      chi = bits > chi ? bits : chi;
+      v[c] = vn;
     }
+    const bool failc = !(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi));
     if (__ballot(failc) != 0) {
       // exact log-domain update of every column, absorbed into G (online LSE)
       float mx[CPL], sum[CPL];
@@ -545,7 +552,7 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
 #pragma unroll
   for (int q = 0; q < C8; ++q)
     if ((lane & 7) == 0 && RV(q)) ul[8 * q + (lane >> 3)] = uq[q];
-  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
   if (p.T) {
     float* Tb = p.T + pb * R * R;
     for (int32_t i = 0; i < R; ++i) {
@@ -581,17 +588,264 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
 #undef CV
 }
 
-// LDS of the wave kernel: cpos, hpos [R] + cidx [256] + hidx [64] ints,
-// sA, F, u [64] floats, and the spill tile for rows 48..63 at CPL = 4.
-constexpr int kWaveXRows = 16;
-__host__ __device__ constexpr size_t wave_lds_bytes(int32_t R) {
-  return (size_t)(2 * R + 256 + 64) * 4 + 3 * 64 * 4 + (size_t)kWaveXRows * kWave * 4 * 4;
+// Two waves per problem where the row block does not fit one wave's
+// registers (|H| > 48 at CPL = 4): wave w holds rows 32w .. 32w+31 and all of
+// the lane's columns.  Row sums stay within a wave.  Each column half-step
+// adds the two waves' partial sums in a fixed order after an exchange through
+// LDS (one barrier per iteration, buffers alternating by parity), so both
+// waves derive the same v and take the same branches.
+template <int CPL, int C8W>
+__device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
+                                            const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
+                                            const int32_t* hidx, const float* sAl, float* Fl, float* ul,
+                                            float* xbuf, float kappa) {
+  constexpr int MW = 8 * C8W;  // rows per wave
+  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+  const int rb = MW * wv;      // first row of this wave
+  const int32_t R = p.R;
+  const float* bd = p.b + pb * R;
+  const float* Cb = p.C + pb * p.C_stride;
+  float K[MW][CPL];
+#define CV(c) (lane + kWave * (c) < nc)
+#define CJ(c) (CV(c) ? cidx[lane + kWave * (c)] : 0)
+#define RV(q) (rb + 8 * (q) + (lane >> 3) < nh)
+  float sB[CPL], G[CPL], v[CPL], xb[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    sB[c] = CV(c) ? bd[CJ(c)] : 0.f;
+    G[c] = 0.f;
+    v[c] = CV(c) ? 1.f : 0.f;
+    xb[c] = CV(c) ? 0.f : 1.f;
+  }
+  float uq[C8W], yb[C8W];
+#pragma unroll
+  for (int q = 0; q < C8W; ++q) {
+    uq[q] = RV(q) ? 1.f : 0.f;
+    yb[q] = RV(q) ? 0.f : 1.f;
+  }
+#pragma unroll
+  for (int i = 0; i < MW; ++i) {
+    const int gi = rb + i;
+    if (gi < nh) {
+      const float Fi = Fl[gi];
+      const float* crow = Cb + (int64_t)hidx[gi] * R;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2(Fi - crow[CJ(c)] * kappa) : 0.f;
+    } else {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) K[i][c] = 0.f;
+    }
+  }
+
+  for (int32_t it = 1; it <= p.iters; ++it) {
+    if (it > 1) {
+      // ---- row half-step on this wave's rows ----------------------------------------
+      uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+      for (int q = 0; q < C8W; ++q) {
+        float pp[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          float acc = K[8 * q + r][0] * v[0];
+#pragma unroll
+          for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[8 * q + r][c], v[c], acc);
+          pp[r] = acc;
+        }
+        const float y = reduce8(pp, lane);
+        const float un = sAl[rb + 8 * q + (lane >> 3)] * frcp(y + yb[q]);
+        const uint32_t bits = __float_as_uint(un + yb[q]);
+        lo = bits < lo ? bits : lo;
+        hi = bits > hi ? bits : hi;
+        uq[q] = un;
+      }
+      const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
+      if (__ballot(fail) != 0) {
+        // exact log-domain update of this wave's rows, absorbed into F
+#pragma unroll
+        for (int i = 0; i < MW; ++i) {
+          const int gi = rb + i;
+          if (gi < nh) {
+            const float* crow = Cb + (int64_t)hidx[gi] * R;
+            float t[CPL];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+              t[c] = CV(c) ? (G[c] + flog2(v[c])) - crow[CJ(c)] * kappa : -INFINITY;
+              mx = fmaxf(mx, t[c]);
+            }
+            mx = wave_max(mx);
+            float sum = 0.f;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
+            sum = first_lane(wave_sum(sum));
+            const float fi = flog2(sAl[gi]) - (mx + flog2(sum));
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2((fi + G[c]) - crow[CJ(c)] * kappa) : 0.f;
+            if (lane == 0) Fl[gi] = fi;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < C8W; ++q) uq[q] = RV(q) ? 1.f : 0.f;
+      }
+    }
+    // ---- column half-step: partial sums of both waves, added in wave order ------------
+    float x[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) x[c] = wv == 0 ? xb[c] : 0.f;
+#pragma unroll
+    for (int q = 0; q < C8W; ++q) {
+      float us[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) us[r] = bcast(uq[q], 8 * r);
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], K[8 * q + r][c], x[c]);
+    }
+    float* xs = xbuf + (size_t)((it & 1) * 2 + wv) * CPL * kWave;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) xs[c * kWave + lane] = x[c];
+    __syncthreads();
+    const float* x0 = xbuf + (size_t)((it & 1) * 2) * CPL * kWave;
+    const float* x1 = x0 + CPL * kWave;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) x[c] = x0[c * kWave + lane] + x1[c * kWave + lane];
+    uint32_t clo = 0xFFFFFFFFu, chi = 0u;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const float vn = sB[c] * frcp(x[c]);
+      const uint32_t bits = __float_as_uint(vn + xb[c]);
+      clo = bits < clo ? bits : clo;
+      chi = bits > chi ? bits : chi;
+      v[c] = vn;
+    }
+    const bool failc = !(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi));
+    if (__ballot(failc) != 0) {  // the same decision on both waves
+      // exact log-domain update of every column, absorbed into G (online LSE
+      // over all rows: each wave publishes its row scalings first)
+#pragma unroll
+      for (int q = 0; q < C8W; ++q)
+        if ((lane & 7) == 0 && RV(q)) ul[rb + 8 * q + (lane >> 3)] = uq[q];
+      __syncthreads();
+      float mx[CPL], sum[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) { mx[c] = -INFINITY; sum[c] = 0.f; }
+      for (int32_t i = 0; i < nh; ++i) {
+        const float fi = Fl[i] + flog2(ul[i]);
+        const float* crow = Cb + (int64_t)hidx[i] * R;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          if (CV(c)) {
+            const float t = fi - crow[CJ(c)] * kappa;
+            const float m2 = fmaxf(mx[c], t);
+            sum[c] = sum[c] * fexp2(mx[c] - m2) + fexp2(t - m2);
+            mx[c] = m2;
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        G[c] = CV(c) ? flog2(sB[c]) - (mx[c] + flog2(sum[c])) : 0.f;
+        v[c] = CV(c) ? 1.f : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < MW; ++i) {
+        const int gi = rb + i;
+        if (gi < nh) {
+          const float Fi = Fl[gi];
+          const float* crow = Cb + (int64_t)hidx[gi] * R;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2((Fi + G[c]) - crow[CJ(c)] * kappa) : 0.f;
+        }
+      }
+      __syncthreads();  // both waves have read ul
+    }
+  }
+
+  // ---- plan, column cap, outputs -------------------------------------------------
+  const bool colcap = !(p.flags & TAOT_SK_NO_COLCAP);
+  float fac[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) fac[c] = 1.f;
+  if (colcap) {
+    float cs[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) cs[c] = 0.f;
+#pragma unroll
+    for (int i = 0; i < MW; ++i) {
+      const float ui = bcast(uq[i / 8], 8 * (i % 8));
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) cs[c] += ui * K[i][c] * v[c];
+    }
+    // the iteration loop's last exchange used parity iters & 1
+    float* xs = xbuf + (size_t)(((p.iters + 1) & 1) * 2 + wv) * CPL * kWave;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) xs[c * kWave + lane] = cs[c];
+    __syncthreads();
+    const float* c0 = xbuf + (size_t)(((p.iters + 1) & 1) * 2) * CPL * kWave;
+    const float* c1 = c0 + CPL * kWave;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+      fac[c] = CV(c) ? fminf(1.f, sB[c] / ((c0[c * kWave + lane] + c1[c * kWave + lane]) + 1e-12f)) : 1.f;
+  }
+#pragma unroll
+  for (int q = 0; q < C8W; ++q)
+    if ((lane & 7) == 0 && RV(q)) ul[rb + 8 * q + (lane >> 3)] = uq[q];
+  __syncthreads();
+  if (p.T) {
+    float* Tb = p.T + pb * R * R;
+    for (int32_t i = wv; i < R; i += 2) {
+      const bool hot = hpos[i] >= 0;
+      for (int32_t j = lane; j < R; j += kWave)
+        if (!hot || cpos[j] < 0) Tb[(int64_t)i * R + j] = 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < MW; ++i) {
+      const int gi = rb + i;
+      if (gi < nh) {
+        const float ui = bcast(uq[i / 8], 8 * (i % 8));
+        float* trow = Tb + (int64_t)hidx[gi] * R;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+          if (CV(c)) trow[CJ(c)] = ui * K[i][c] * (v[c] * fac[c]);
+      }
+    }
+  }
+  if (wv == 0) {
+    const float to_nat = p.eps * kLn2;
+    for (int32_t i = lane; i < R; i += kWave) {
+      const int32_t ih = hpos[i];
+      if (p.f) p.f[pb * R + i] = ih >= 0 ? (Fl[ih] + flog2(ul[ih])) * to_nat : -INFINITY;
+      if (p.g && cpos[i] < 0) p.g[pb * R + i] = -INFINITY;
+    }
+    if (p.g) {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+        if (CV(c)) p.g[pb * R + CJ(c)] = (G[c] + flog2(v[c])) * to_nat;
+    }
+    if (lane == 0 && p.status) p.status[pb] = 0u;
+  }
+#undef RV
+#undef CJ
+#undef CV
 }
 
-__global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
-  extern __shared__ int32_t wl[];
-  const int lane = threadIdx.x;
-  const int64_t pb = blockIdx.x;
+// LDS of the wave kernels: cpos, hpos [R] + cidx [256] + hidx [64] ints,
+// sA, F, u [64] floats, and for the two-wave solver the column exchange
+// [2 parities][2 waves][4][64] floats.
+__host__ __device__ constexpr size_t wave_lds_bytes(int32_t R, bool two) {
+  return (size_t)(2 * R + 256 + 64) * 4 + 3 * 64 * 4 + (two ? (size_t)2 * 2 * 4 * kWave * 4 : 0);
+}
+__host__ __device__ constexpr bool two_wave_class(int cls) {
+  return cls == wave_class(4, 7) || cls == wave_class(4, 8);
+}
+
+// Problem pb on one wave (TWO = false: the row block fits one wave's
+// registers) or on a two-wave workgroup (TWO = true: the rest of the register
+// classes); returns at once for the other kind.  Uniform over the workgroup.
+template <bool TWO>
+__device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int32_t* wl) {
+  const int lane = threadIdx.x & (kWave - 1);
   const int32_t R = p.R;
   int32_t* cpos = wl;              // [R] compact column of rank j, -1 if not cold
   int32_t* hpos = cpos + R;        // [R] compact row of rank i, -1 if not hot
@@ -599,8 +853,8 @@ __global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
   int32_t* hidx = cidx + 256;      // [64]
   float* sAl = reinterpret_cast<float*>(hidx + 64);  // [64] scaled supply
   float* Fl = sAl + 64;            // [64] absorbed row potentials (log2 units)
-  float* ul = Fl + 64;             // [64] final row scalings
-  float* kx = ul + 64;             // [16][64][4] rows 48..63 when CPL = 4
+  float* ul = Fl + 64;             // [64] row scalings (final, and for exchanges)
+  float* xbuf = ul + 64;           // [2][2][4][64] column partial sums (TWO only)
   const float* a = p.a + pb * R;
   const float* bd = p.b + pb * R;
   const float* Cb = p.C + pb * p.C_stride;
@@ -629,12 +883,12 @@ __global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
     nc += __popcll(cm);
   }
   const int cls = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
-  if (cls == 0) return;  // uniform: another path owns this problem
+  if (cls == 0 || two_wave_class(cls) != TWO) return;  // uniform: another kernel owns this problem
   sa = wave_sum_d(sa);
   sd = wave_sum_d(sd);
   double gamma = __shfl(sd, 0, kWave) / fmax(__shfl(sa, 0, kWave), kEps0);
   gamma = gamma < 1.0 ? gamma : 1.0;
-  if (lane < nh) sAl[lane] = (float)(gamma * (double)a[hidx[lane]]);
+  sAl[lane] = lane < nh ? (float)(gamma * (double)a[hidx[lane]]) : 0.f;  // zero padding to 64 rows
   __syncthreads();
   const float kappa = kLog2e / p.eps;
 
@@ -665,28 +919,124 @@ __global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
     return;
   }
   __syncthreads();
+  if constexpr (TWO) {
+    wave2_solve<4, 4>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, xbuf, kappa);
+    return;
+  } else {
   switch (cls) {
 #define TAOT_WAVE_CASE(CPL_, C8_)                                                                      \
   case wave_class(CPL_, C8_):                                                                          \
-    wave_solve<CPL_, C8_>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, kx, kappa);               \
+    wave_solve<CPL_, C8_>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, kappa);                   \
     break;
 #define TAOT_WAVE_CPL(CPL_)                                                                            \
   TAOT_WAVE_CASE(CPL_, 1) TAOT_WAVE_CASE(CPL_, 2) TAOT_WAVE_CASE(CPL_, 3) TAOT_WAVE_CASE(CPL_, 4)      \
   TAOT_WAVE_CASE(CPL_, 5) TAOT_WAVE_CASE(CPL_, 6) TAOT_WAVE_CASE(CPL_, 7) TAOT_WAVE_CASE(CPL_, 8)
-    TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2) TAOT_WAVE_CPL(4)
+    TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2)
+    TAOT_WAVE_CASE(4, 1) TAOT_WAVE_CASE(4, 2) TAOT_WAVE_CASE(4, 3) TAOT_WAVE_CASE(4, 4)
+    TAOT_WAVE_CASE(4, 5) TAOT_WAVE_CASE(4, 6)
 #undef TAOT_WAVE_CPL
 #undef TAOT_WAVE_CASE
     default: break;
   }
+  }
 }
 
-taot_status launch_wave(const SkParams& p, hipStream_t stream) {
-  const size_t lds = wave_lds_bytes(p.R);
-  if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_wave_kernel,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-    return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(sinkhorn_wave_kernel, dim3((unsigned)p.B), dim3(kWave), lds, stream, p);
-  return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
+__global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
+  extern __shared__ int32_t wl[];
+  wave_problem<false>(p, blockIdx.x, wl);
+}
+
+// The listed two-wave problems, a small grid walking the list.
+__global__ void __launch_bounds__(2 * kWave, 2)
+sinkhorn_wave2_kernel(SkParams p, const int32_t* __restrict__ list, const int32_t* __restrict__ count) {
+  extern __shared__ int32_t wl[];
+  const int32_t n = *count;
+  for (int32_t k = blockIdx.x; k < n; k += gridDim.x) {
+    wave_problem<true>(p, list[k], wl);
+    __syncthreads();  // LDS is reused by the next problem
+  }
+}
+
+// Register class of every problem (0: not a register problem), with the same
+// support scan and tests as wave_problem.
+__global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* __restrict__ cls) {
+  const int lane = threadIdx.x;
+  const int64_t pb = blockIdx.x;
+  const int32_t R = p.R;
+  const float* a = p.a + pb * R;
+  const float* bd = p.b + pb * R;
+  bool bad = false;
+  int32_t nh = 0, nc = 0;
+  for (int32_t base = 0; base < R; base += kWave) {
+    const int32_t i = base + lane;
+    const bool in = i < R;
+    const float ai = in ? a[i] : 0.f, bi = in ? bd[i] : 0.f;
+    bad |= !(ai >= 0.f && ai <= 3.402823466e38f) || !(bi >= 0.f && bi <= 3.402823466e38f);
+    nh += __popcll(__ballot(in && ai > 0.f));
+    nc += __popcll(__ballot(in && bi > 0.f));
+  }
+  const int c = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
+  if (lane == 0) cls[pb] = c;
+}
+
+// Ascending list of the two-wave problems (one block).
+__global__ void __launch_bounds__(kSkThreads) two_wave_list_kernel(const int32_t* __restrict__ cls, int32_t B,
+                                                                   int32_t* __restrict__ list,
+                                                                   int32_t* __restrict__ count) {
+  __shared__ int32_t wave_cnt[kSkWaves];
+  int32_t n = 0;
+  for (int32_t base = 0; base < B; base += kSkThreads) {
+    const int32_t b = base + (int32_t)threadIdx.x;
+    const bool f = b < B && two_wave_class(cls[b]);
+    int32_t tot;
+    const int32_t pos = chunk_compact(f, wave_cnt, tot);
+    if (f) list[n + pos] = b;
+    n += tot;
+  }
+  if (threadIdx.x == 0) *count = n;
+}
+
+// A stream beside the caller's, so that the one- and two-wave kernels run
+// concurrently: created once per device and kept for the life of the
+// process, at the default priority.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxDevices = 64;
+constexpr int kTwoWaveGrid = 64;  // workgroups of the two-wave kernel
+std::mutex g_side_mutex;
+SideStream g_side[kMaxDevices];
+
+// The register path: classes and the two-wave list on the caller's stream;
+// then the two-wave kernel (a small grid, launched first so that its
+// workgroups find room) on the caller's stream, beside the one-wave kernel on
+// the side stream; the caller's stream waits for both.
+taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* list, int32_t* count, hipStream_t stream) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(wave_class_kernel, dim3((unsigned)p.B), dim3(kWave), 0, stream, p, cls);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(two_wave_list_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, list, count);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  std::lock_guard<std::mutex> lock(g_side_mutex);
+  SideStream& sd = g_side[dev];
+  if (sd.s == nullptr) {
+    if (hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&sd.join, hipEventDisableTiming) != hipSuccess)
+      return TAOT_ERR_LAUNCH;
+  }
+  if (hipEventRecord(sd.fork, stream) != hipSuccess) return TAOT_ERR_LAUNCH;
+  const unsigned grid2 = (unsigned)(p.B < kTwoWaveGrid ? p.B : kTwoWaveGrid);
+  hipLaunchKernelGGL(sinkhorn_wave2_kernel, dim3(grid2), dim3(2 * kWave), wave_lds_bytes(p.R, true), stream, p,
+                     list, count);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  if (hipStreamWaitEvent(sd.s, sd.fork, 0) != hipSuccess) return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(sinkhorn_wave_kernel, dim3((unsigned)p.B), dim3(kWave), wave_lds_bytes(p.R, false), sd.s, p);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  if (hipEventRecord(sd.join, sd.s) != hipSuccess) return TAOT_ERR_LAUNCH;
+  return hipStreamWaitEvent(stream, sd.join, 0) == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
 }
 
 // Largest nh * nc over disjoint supports of R ranks (nh + nc <= R).
@@ -694,6 +1044,9 @@ int64_t max_block(int32_t R) { return (int64_t)(R / 2) * (R - R / 2); }
 
 struct SkWs {
   int32_t* flag;
+  int32_t* cls;    // [B] register class
+  int32_t* list;   // [B] two-wave problems
+  int32_t* count;  // [1]
   float* kt;
   int64_t kt_stride;
   size_t bytes;
@@ -703,6 +1056,9 @@ SkWs carve(void* ws, int32_t B, int32_t R) {
   Carver c{static_cast<char*>(ws)};
   SkWs w;
   w.flag = c.take<int32_t>((size_t)B);
+  w.cls = c.take<int32_t>((size_t)B);
+  w.list = c.take<int32_t>((size_t)B);
+  w.count = c.take<int32_t>(1);
   w.kt_stride = round_up((int64_t)R * R, 64);
   w.kt = c.take<float>((size_t)B * w.kt_stride);
   w.bytes = c.off;
@@ -722,7 +1078,7 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
   if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {
-    const taot_status st = launch_wave(p, stream);
+    const taot_status st = launch_wave(p, w.cls, w.list, w.count, stream);
     if (st != TAOT_OK) return st;
   }
   if (lds_path) {

@@ -169,3 +169,23 @@ def test_deterministic(gpu):
     T1 = _gpu_sinkhorn(a, b, C, w.eps, w.iters)[0]
     T2 = _gpu_sinkhorn(a, b, C, w.eps, w.iters)[0]
     assert T1.tobytes() == T2.tobytes()
+
+
+@pytest.mark.parametrize("nh,nc", [(49, 129), (56, 200), (57, 256), (64, 193), (64, 256)])
+def test_two_wave_rows(nh, nc, gpu):
+    """Hot sets of 49..64 ranks with more than 128 cold ranks: the row block is
+    split over two waves that exchange column sums.  Small eps drives the
+    scalings out of range, so both log-domain absorptions run as well."""
+    rng = np.random.default_rng(nh * 1000 + nc)
+    R = nh + nc
+    B = 3
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p in range(B):
+        perm = rng.permutation(R)
+        a[p, perm[:nh]] = rng.integers(1, 4000, size=nh)
+        b[p, perm[nh:]] = rng.multinomial(int(a[p].sum()), np.full(nc, 1.0 / nc)) + 1
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32))
+    for eps, iters in ((0.5, 3), (0.08, 200), (0.02, 120)):
+        print(f"[sinkhorn parity] two-wave nh={nh} nc={nc} eps={eps}", flush=True)
+        _check_against_oracle(a, b, C, eps, iters)
