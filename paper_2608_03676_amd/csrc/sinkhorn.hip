@@ -468,16 +468,20 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
       }
     }
     // ---- column half-step: v_c = d_c / sum_i u_i Kt_ic -------------------------------
+    // the row scalings reach every lane through LDS (one store per row, two
+    // broadcast 16-byte loads per 8 rows; a wave's LDS accesses run in order)
+#pragma unroll
+    for (int q = 0; q < C8; ++q)
+      if ((lane & 7) == 0) ul[8 * q + (lane >> 3)] = uq[q];
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     float x[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) x[c] = xb[c];
 #pragma unroll
     for (int q = 0; q < C8; ++q) {
-      // broadcast the chunk's row scalings first so that each FMA sits far
-      // enough behind the v_readlane that produced its operand
-      float us[8];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) us[r] = bcast(uq[q], 8 * r);
+      const float4 ua = *reinterpret_cast<const float4*>(ul + 8 * q);
+      const float4 ub = *reinterpret_cast<const float4*>(ul + 8 * q + 4);
+      const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
 #pragma unroll
       for (int r = 0; r < 8; ++r)
 #pragma unroll
@@ -689,14 +693,19 @@ __device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32
       }
     }
     // ---- column half-step: partial sums of both waves, added in wave order ------------
+    // row scalings to every lane through this wave's part of ul (as in wave_solve)
+#pragma unroll
+    for (int q = 0; q < C8W; ++q)
+      if ((lane & 7) == 0) ul[rb + 8 * q + (lane >> 3)] = uq[q];
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     float x[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) x[c] = wv == 0 ? xb[c] : 0.f;
 #pragma unroll
     for (int q = 0; q < C8W; ++q) {
-      float us[8];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) us[r] = bcast(uq[q], 8 * r);
+      const float4 ua = *reinterpret_cast<const float4*>(ul + rb + 8 * q);
+      const float4 ub = *reinterpret_cast<const float4*>(ul + rb + 8 * q + 4);
+      const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
 #pragma unroll
       for (int r = 0; r < 8; ++r)
 #pragma unroll
@@ -830,9 +839,9 @@ __device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32
 #undef CV
 }
 
-// LDS of the wave kernels: cpos, hpos [R] + cidx [256] + hidx [64] ints,
-// sA, F, u [64] floats, and for the two-wave solver the column exchange
-// [2 parities][2 waves][4][64] floats.
+// LDS of the wave kernels: sA, F, u [64] floats, for the two-wave solver the
+// column exchange [2 parities][2 waves][4][64] floats, then cpos, hpos [R] +
+// cidx [256] + hidx [64] ints.
 __host__ __device__ constexpr size_t wave_lds_bytes(int32_t R, bool two) {
   return (size_t)(2 * R + 256 + 64) * 4 + 3 * 64 * 4 + (two ? (size_t)2 * 2 * 4 * kWave * 4 : 0);
 }
@@ -847,14 +856,15 @@ template <bool TWO>
 __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int32_t* wl) {
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t R = p.R;
-  int32_t* cpos = wl;              // [R] compact column of rank j, -1 if not cold
+  // float arrays first: ul is read 16 bytes at a time
+  float* sAl = reinterpret_cast<float*>(wl);  // [64] scaled supply
+  float* Fl = sAl + 64;            // [64] absorbed row potentials (log2 units)
+  float* ul = Fl + 64;             // [64] row scalings (broadcast, final, exchanges)
+  float* xbuf = ul + 64;           // [2][2][4][64] column partial sums (TWO only)
+  int32_t* cpos = reinterpret_cast<int32_t*>(TWO ? xbuf + 2 * 2 * 4 * kWave : xbuf);  // [R] compact column, -1 if not cold
   int32_t* hpos = cpos + R;        // [R] compact row of rank i, -1 if not hot
   int32_t* cidx = hpos + R;        // [256]
   int32_t* hidx = cidx + 256;      // [64]
-  float* sAl = reinterpret_cast<float*>(hidx + 64);  // [64] scaled supply
-  float* Fl = sAl + 64;            // [64] absorbed row potentials (log2 units)
-  float* ul = Fl + 64;             // [64] row scalings (final, and for exchanges)
-  float* xbuf = ul + 64;           // [2][2][4][64] column partial sums (TWO only)
   const float* a = p.a + pb * R;
   const float* bd = p.b + pb * R;
   const float* Cb = p.C + pb * p.C_stride;
@@ -941,15 +951,17 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
   }
 }
 
-__global__ void __launch_bounds__(kWave, 2) sinkhorn_wave_kernel(SkParams p) {
-  extern __shared__ int32_t wl[];
-  wave_problem<false>(p, blockIdx.x, wl);
+__global__ void __launch_bounds__(kWave, 2)
+sinkhorn_wave_kernel(SkParams p, const int32_t* __restrict__ ord, const int32_t* __restrict__ count) {
+  extern __shared__ __attribute__((aligned(16))) int32_t wl[];
+  if ((int32_t)blockIdx.x >= *count) return;
+  wave_problem<false>(p, ord[blockIdx.x], wl);
 }
 
 // The listed two-wave problems, a small grid walking the list.
 __global__ void __launch_bounds__(2 * kWave, 2)
 sinkhorn_wave2_kernel(SkParams p, const int32_t* __restrict__ list, const int32_t* __restrict__ count) {
-  extern __shared__ int32_t wl[];
+  extern __shared__ __attribute__((aligned(16))) int32_t wl[];
   const int32_t n = *count;
   for (int32_t k = blockIdx.x; k < n; k += gridDim.x) {
     wave_problem<true>(p, list[k], wl);
@@ -979,21 +991,55 @@ __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* 
   if (lane == 0) cls[pb] = c;
 }
 
-// Ascending list of the two-wave problems (one block).
-__global__ void __launch_bounds__(kSkThreads) two_wave_list_kernel(const int32_t* __restrict__ cls, int32_t B,
-                                                                   int32_t* __restrict__ list,
-                                                                   int32_t* __restrict__ count) {
+// Per-iteration work of a register class: rows (8 C8) x columns per lane.
+__device__ __forceinline__ int32_t class_work(int32_t cls) {
+  const int32_t c8 = (cls - 1) % 8 + 1, ci = (cls - 1) / 8;
+  return c8 * (ci == 0 ? 1 : ci == 1 ? 2 : 4);
+}
+
+// Launch orders (one block): the two-wave problems ascending, and the
+// one-wave problems by descending work (ascending index within equal work),
+// so that workgroups dealt out in order mix heavy and light problems on every
+// compute unit.
+__global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* __restrict__ cls, int32_t B,
+                                                                int32_t* __restrict__ list2,
+                                                                int32_t* __restrict__ count2,
+                                                                int32_t* __restrict__ ord1,
+                                                                int32_t* __restrict__ count1) {
   __shared__ int32_t wave_cnt[kSkWaves];
+  __shared__ unsigned long long present;  // bit w: some one-wave problem has work w
+  if (threadIdx.x == 0) present = 0ull;
+  __syncthreads();
+  for (int32_t b = threadIdx.x; b < B; b += kSkThreads) {
+    const int32_t c = cls[b];
+    if (c != 0 && !two_wave_class(c)) atomicOr(&present, 1ull << class_work(c));
+  }
+  __syncthreads();
+  const unsigned long long works = present;
   int32_t n = 0;
   for (int32_t base = 0; base < B; base += kSkThreads) {
     const int32_t b = base + (int32_t)threadIdx.x;
     const bool f = b < B && two_wave_class(cls[b]);
     int32_t tot;
     const int32_t pos = chunk_compact(f, wave_cnt, tot);
-    if (f) list[n + pos] = b;
+    if (f) list2[n + pos] = b;
     n += tot;
   }
-  if (threadIdx.x == 0) *count = n;
+  if (threadIdx.x == 0) *count2 = n;
+  n = 0;
+  for (int32_t wk = 63; wk > 0; --wk) {
+    if (!((works >> wk) & 1ull)) continue;
+    for (int32_t base = 0; base < B; base += kSkThreads) {
+      const int32_t b = base + (int32_t)threadIdx.x;
+      const int32_t c = b < B ? cls[b] : 0;
+      const bool f = c != 0 && !two_wave_class(c) && class_work(c) == wk;
+      int32_t tot;
+      const int32_t pos = chunk_compact(f, wave_cnt, tot);
+      if (f) ord1[n + pos] = b;
+      n += tot;
+    }
+  }
+  if (threadIdx.x == 0) *count1 = n;
 }
 
 // A stream beside the caller's, so that the one- and two-wave kernels run
@@ -1012,12 +1058,13 @@ SideStream g_side[kMaxDevices];
 // then the two-wave kernel (a small grid, launched first so that its
 // workgroups find room) on the caller's stream, beside the one-wave kernel on
 // the side stream; the caller's stream waits for both.
-taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* list, int32_t* count, hipStream_t stream) {
+taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* list, int32_t* count, int32_t* ord,
+                        int32_t* count1, hipStream_t stream) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TAOT_ERR_LAUNCH;
   hipLaunchKernelGGL(wave_class_kernel, dim3((unsigned)p.B), dim3(kWave), 0, stream, p, cls);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(two_wave_list_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, list, count);
+  hipLaunchKernelGGL(wave_order_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, list, count, ord, count1);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   std::lock_guard<std::mutex> lock(g_side_mutex);
   SideStream& sd = g_side[dev];
@@ -1033,7 +1080,8 @@ taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* list, int32_t*
                      list, count);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   if (hipStreamWaitEvent(sd.s, sd.fork, 0) != hipSuccess) return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(sinkhorn_wave_kernel, dim3((unsigned)p.B), dim3(kWave), wave_lds_bytes(p.R, false), sd.s, p);
+  hipLaunchKernelGGL(sinkhorn_wave_kernel, dim3((unsigned)p.B), dim3(kWave), wave_lds_bytes(p.R, false), sd.s, p,
+                     ord, count1);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   if (hipEventRecord(sd.join, sd.s) != hipSuccess) return TAOT_ERR_LAUNCH;
   return hipStreamWaitEvent(stream, sd.join, 0) == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
@@ -1047,6 +1095,8 @@ struct SkWs {
   int32_t* cls;    // [B] register class
   int32_t* list;   // [B] two-wave problems
   int32_t* count;  // [1]
+  int32_t* ord;    // [B] one-wave problems by descending work
+  int32_t* count1; // [1]
   float* kt;
   int64_t kt_stride;
   size_t bytes;
@@ -1059,6 +1109,8 @@ SkWs carve(void* ws, int32_t B, int32_t R) {
   w.cls = c.take<int32_t>((size_t)B);
   w.list = c.take<int32_t>((size_t)B);
   w.count = c.take<int32_t>(1);
+  w.ord = c.take<int32_t>((size_t)B);
+  w.count1 = c.take<int32_t>(1);
   w.kt_stride = round_up((int64_t)R * R, 64);
   w.kt = c.take<float>((size_t)B * w.kt_stride);
   w.bytes = c.off;
@@ -1078,7 +1130,7 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
   if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {
-    const taot_status st = launch_wave(p, w.cls, w.list, w.count, stream);
+    const taot_status st = launch_wave(p, w.cls, w.list, w.count, w.ord, w.count1, stream);
     if (st != TAOT_OK) return st;
   }
   if (lds_path) {
