@@ -417,9 +417,11 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 
 // ===========================================================================
 // LDS-resident path.  Same arithmetic and order as schedule_kernel, with one
-// 256-thread workgroup per problem and all of its state in LDS and registers.
-// It serves R <= 256, R*K <= 1024 and bonuses (Bauct columns) that take few
-// distinct values, as topology costs do.
+// workgroup per problem and all of its state in LDS and registers.  Two size
+// configurations: 256 threads for R <= 256 and R*K <= 1024 (several problems
+// per compute unit), 1024 threads for R <= 1024 and R*K <= 4096 (up to
+// ~155 KB of LDS, one problem per compute unit).  Both need bonuses (Bauct
+// columns) that take few distinct values, as topology costs do.
 //
 // Phase-3 bids by tiers.  The ranks of host column h split into tiers of equal
 // bonus (descending).  With prices that start at 0 and rise by a fixed step on
@@ -427,11 +429,11 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 // the step is large against the spacing of doubles at the magnitudes reached,
 // bonus - price falls strictly with every service.  Within a tier the argmax
 // of the score is then the lowest-index rank among those with the fewest
-// services, found with a bit-sliced minimum over the count bit-planes; the
-// bid is the best tier result under (max score, lowest rank), and tiers whose
-// bonus is below the best score so far are skipped (price >= 0).  A price step
-// of 0 keeps every price at 0, and the argmax is the lowest rank of the first
-// non-empty tier.
+// services, found word by word (64 ranks) with a bit-sliced minimum over the
+// count bit-planes; the bid is the best tier result under (max score, lowest
+// rank), and tiers whose bonus is below the best score so far are skipped
+// (price >= 0).  A price step of 0 keeps every price at 0, and the argmax is
+// the lowest rank of the first non-empty tier.
 //
 // Phase-3 arbitration by bonus.  Every live bid on rank r was placed at r's
 // current price (a slot re-bids when its rank serves), so among r's bidders
@@ -443,27 +445,43 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 // schedule_kernel when they fail, as it does problems whose candidate or
 // slot-expert counts exceed the LDS layout.
 
-constexpr int kDistinctCap = 64;            // distinct slot experts per problem in LDS
-constexpr int kTierMax = 4;                 // distinct bonus values per host column
-constexpr int kTierWords = 4;               // 64-rank words of a rank set (R <= 256)
-constexpr int kStructCap = 32;              // distinct host tier structures kept in LDS
-constexpr int kValueCap = kStructCap * kTierMax;  // distinct bonuses of the table
-constexpr int kMaxSlots = 1024;             // S = R*K of the LDS-resident path
-constexpr int kPlanes = 11;                 // count bit-planes: counts <= S <= 1024
-static_assert(kTierWords == kSchWaves, "one wave per 64-rank word");
+constexpr int kTierMax = 4;  // distinct bonus values per host column
+
+struct LdsSmall {
+  static constexpr int kT = 256;     // threads per problem
+  static constexpr int kTW = 4;      // 64-rank words of a rank set (R <= 256)
+  static constexpr int kSC = 32;     // distinct host tier structures in LDS
+  static constexpr int kDC = 64;     // distinct slot experts per problem
+  static constexpr int kPL = 11;     // count bit-planes: counts <= R*K <= 1024
+  static constexpr int kMaxS = 1024; // R*K
+  static constexpr int kNEC = 256;   // candidate experts (spill > 0) in LDS
+};
+struct LdsLarge {
+  static constexpr int kT = 1024;
+  static constexpr int kTW = 16;     // R <= 1024
+  static constexpr int kSC = 128;
+  static constexpr int kDC = 128;
+  static constexpr int kPL = 13;     // counts <= R*K <= 4096
+  static constexpr int kMaxS = 4096;
+  static constexpr int kNEC = 1024;
+};
+// list entries pack (slot, slot-expert index, host structure): 12 + 7 + 7 bits
+constexpr int kItemSlotBits = 12, kItemExpertBits = 7;
 
 // Tier structure of column h of Bauct: its distinct bonuses in descending
-// order and the rank set of each; ntier[h] = -1 if there are more than
-// kTierMax.  NaN and -inf bonuses never win a bid and belong to no tier.
+// order and the rank set of each ([h][kTierMax][TW] words); ntier[h] = -1 if
+// there are more than kTierMax.  NaN and -inf bonuses never win a bid and
+// belong to no tier.
+template <int TW>
 __global__ void __launch_bounds__(256)
 auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __restrict__ ntier,
                      double* __restrict__ tv, uint64_t* __restrict__ tmask) {
-  __shared__ double col[kTierWords * kWave];
+  __shared__ double col[TW * kWave];
   __shared__ double vals[kTierMax];
   __shared__ int32_t nv;
-  __shared__ unsigned long long msk[kTierMax * kTierWords];
+  __shared__ unsigned long long msk[kTierMax * TW];
   const int32_t h = blockIdx.x, tid = threadIdx.x;
-  if (tid < kTierMax * kTierWords) msk[tid] = 0ull;
+  for (int32_t q = tid; q < kTierMax * TW; q += blockDim.x) msk[q] = 0ull;
   for (int32_t r = tid; r < R; r += blockDim.x) col[r] = Bauct[(int64_t)r * R + h];
   __syncthreads();
   if (tid == 0) {
@@ -490,48 +508,64 @@ auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __res
   for (int32_t r = tid; r < R && n > 0; r += blockDim.x) {
     const double v = col[r];
     for (int32_t i = 0; i < n; ++i)
-      if (vals[i] == v) atomicOr(&msk[i * kTierWords + (r >> 6)], 1ull << (r & 63));
+      if (vals[i] == v) atomicOr(&msk[i * TW + (r >> 6)], 1ull << (r & 63));
   }
   __syncthreads();
   if (tid == 0) ntier[h] = n;
   if (tid < kTierMax) tv[(int64_t)h * kTierMax + tid] = tid < n ? vals[tid] : -INFINITY;
-  if (tid < kTierMax * kTierWords)
-    tmask[(int64_t)h * kTierMax * kTierWords + tid] = tid / kTierWords < n ? msk[tid] : 0ull;
+  for (int32_t q = tid; q < kTierMax * TW; q += blockDim.x)
+    tmask[(int64_t)h * kTierMax * TW + q] = q / TW < n ? msk[q] : 0ull;
 }
 
-// Deduplicates the host tier structures into a table of at most kStructCap
-// (one block, one thread per host) and ranks the table's distinct bonuses
-// (ascending): sidx[h] is host h's entry, cvr the bonus rank of each tier,
-// hdr[0] the table size and hdr[1] = 1 when the LDS-resident auction is exact for
-// this Bauct and price step: every column has at most kTierMax values, none
-// is +inf, the table fits, and both the step (if not 0) and every gap between
-// distinct bonuses exceed twice the spacing of doubles at
-// max|bonus| + S * step (prices stay below S * step: a rank serves each slot
-// at most once).
-__global__ void __launch_bounds__(256)
+// Deduplicates the host tier structures into a table of at most SC entries
+// (one block, one thread per host; equal structures are found through a hash
+// of each and then compared in full) and ranks the table's distinct bonuses
+// (ascending): sidx[h] is host h's entry, cw the words that hold ranks of
+// each tier, cvr the bonus rank of each tier, hdr[0] the table size and
+// hdr[1] = 1 when the LDS-resident auction is exact for this Bauct and price
+// step: every column has at most kTierMax values, none is +inf, the table
+// fits, and both the step (if not 0) and every gap between distinct bonuses
+// exceed twice the spacing of doubles at max|bonus| + S * step (prices stay
+// below S * step: a rank serves each slot at most once).
+template <class CF>
+__global__ void __launch_bounds__(CF::kT)
 auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restrict__ tv_g,
-                      const uint64_t* __restrict__ tmask_g, int32_t R, int64_t S, double step,
+                      const uint64_t* __restrict__ tmask, int32_t R, int64_t S, double step,
                       int32_t* __restrict__ sidx, int32_t* __restrict__ cn, double* __restrict__ cv,
-                      int32_t* __restrict__ cvr, uint64_t* __restrict__ cm, int32_t* __restrict__ hdr) {
-  constexpr int kRow = kTierMax * kTierWords;
-  constexpr int kMaxR = kTierWords * kWave;
-  __shared__ int32_t ntier[kMaxR], first[kMaxR], sid[kMaxR], tab[kStructCap];
+                      int32_t* __restrict__ cvr, uint32_t* __restrict__ cw, uint64_t* __restrict__ cm,
+                      int32_t* __restrict__ hdr) {
+  constexpr int kRow = kTierMax * CF::kTW;
+  constexpr int kMaxR = CF::kTW * kWave;
+  __shared__ int32_t ntier[kMaxR], first[kMaxR], sid[kMaxR], tab[CF::kSC];
+  __shared__ uint64_t hsh[kMaxR];
   __shared__ double tv[kMaxR * kTierMax];
-  __shared__ uint64_t tmask[kMaxR * kRow];
-  __shared__ double dv[kValueCap];
+  __shared__ double dv[CF::kSC * kTierMax];
   __shared__ int32_t sh_ns, sh_ok;
   const int32_t h = threadIdx.x;
-  for (int32_t q = h; q < R; q += blockDim.x) ntier[q] = ntier_g[q];
   for (int32_t q = h; q < R * kTierMax; q += blockDim.x) tv[q] = tv_g[q];
-  for (int32_t q = h; q < R * kRow; q += blockDim.x) tmask[q] = tmask_g[q];
+  if (h < R) {
+    const int32_t nh = ntier_g[h];
+    ntier[h] = nh;
+    uint64_t x = 0x9E3779B97F4A7C15ull ^ (uint64_t)(uint32_t)nh;
+    for (int32_t t = 0; t < kTierMax; ++t) {
+      x = (x ^ (uint64_t)__double_as_longlong(tv_g[h * kTierMax + t])) * 0x100000001B3ull;
+      x ^= x >> 29;
+    }
+    for (int32_t q = 0; q < kRow; ++q) {
+      x = (x ^ tmask[(int64_t)h * kRow + q]) * 0x100000001B3ull;
+      x ^= x >> 29;
+    }
+    hsh[h] = x;
+  }
   __syncthreads();
   if (h < R) {
     const int32_t nh = ntier[h];
     int32_t f = h;
     for (int32_t g = 0; g < h && f == h; ++g) {
-      bool eq = ntier[g] == nh;
+      if (hsh[g] != hsh[h] || ntier[g] != nh) continue;
+      bool eq = true;
       for (int32_t t = 0; t < kTierMax && eq; ++t) eq = tv[g * kTierMax + t] == tv[h * kTierMax + t];
-      for (int32_t q = 0; q < kRow && eq; ++q) eq = tmask[g * kRow + q] == tmask[h * kRow + q];
+      for (int32_t q = 0; q < kRow && eq; ++q) eq = tmask[(int64_t)g * kRow + q] == tmask[(int64_t)h * kRow + q];
       if (eq) f = g;
     }
     first[h] = f;
@@ -553,7 +587,7 @@ auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restr
         ok &= v != INFINITY;
         vm = fmax(vm, fabs(v));
       }
-      if (ns < kStructCap) {
+      if (ns < CF::kSC) {
         tab[ns] = g;
         // distinct bonuses of the table, ascending
         for (int32_t t = 0; t < nt; ++t) {
@@ -573,12 +607,12 @@ auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restr
       sid[g] = ns;
       ++ns;
     }
-    ok &= ns <= kStructCap;
+    ok &= ns <= CF::kSC;
     const double top = vm + (double)S * step * 1.01 + 1.0;
     const double spacing2 = 2.0 * (nextafter(top, INFINITY) - top);
     ok &= step == 0.0 || (step > 0.0 && step > spacing2);
     for (int32_t i = 0; i + 1 < nd; ++i) ok &= dv[i + 1] - dv[i] > spacing2;
-    sh_ns = ns < kStructCap ? ns : kStructCap;
+    sh_ns = ns < CF::kSC ? ns : CF::kSC;
     sh_ok = ok ? 1 : 0;
     // bonus ranks of the table's tiers
     for (int32_t i = 0; i < sh_ns; ++i) {
@@ -595,32 +629,41 @@ auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restr
   const int32_t ns = sh_ns;
   for (int32_t q = h; q < R; q += blockDim.x) sidx[q] = sid[q];
   for (int32_t q = h; q < ns; q += blockDim.x) cn[q] = ntier[tab[q]] > 0 ? ntier[tab[q]] : 0;
-  for (int32_t q = h; q < ns * kTierMax; q += blockDim.x) cv[q] = tv[tab[q / kTierMax] * kTierMax + q % kTierMax];
-  for (int32_t q = h; q < ns * kRow; q += blockDim.x) cm[q] = tmask[tab[q / kRow] * kRow + q % kRow];
+  for (int32_t q = h; q < ns * kTierMax; q += blockDim.x) {
+    const int32_t g = tab[q / kTierMax], t = q % kTierMax;
+    cv[q] = tv[g * kTierMax + t];
+    uint32_t words = 0;
+    for (int32_t w = 0; w < CF::kTW; ++w) words |= (tmask[(int64_t)g * kRow + t * CF::kTW + w] != 0ull ? 1u : 0u) << w;
+    cw[q] = words;
+  }
+  for (int32_t q = h; q < ns * kRow; q += blockDim.x) cm[q] = tmask[(int64_t)tab[q / kRow] * kRow + q % kRow];
   if (h == 0) {
     hdr[0] = ns;
     hdr[1] = sh_ok;
   }
 }
 
+template <class CF>
 struct LdsState {
   // both phases
   int32_t* slot_ec;   // [S] candidate index of the slot's expert or -1
-  int32_t* amt;       // [S] slot amounts (Phase 2)
+  int32_t* amt;       // [S] slot amounts (Phase 2), tokens still planned (Phase 3)
   int32_t* ce;        // [NEC] candidate experts (spill > 0), ascending
   // Phase 2
   int32_t* hce; double* den; int32_t* cr; int32_t* spare_p; int32_t* matched; int32_t* prop_e;
   double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
   // Phase 3 (aliases the Phase-2 region)
   double* price; uint32_t* rkey; int32_t* work;
-  uint64_t* vmask; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
-  int32_t* cn; double* cv; int32_t* cvr; uint64_t* cm;
+  uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
+  int32_t* cn; double* cv; int32_t* cvr; uint32_t* cw; uint64_t* cm;
   size_t bytes;
 };
 
-__host__ __device__ inline LdsState carve_lds(char* base, int32_t R, int32_t K, int32_t NEC) {
-  LdsState w;
+template <class CF>
+__host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t K, int32_t NEC) {
+  LdsState<CF> w;
   const size_t S1 = R * K > 0 ? (size_t)R * K : 1, R_ = (size_t)R, N_ = (size_t)NEC;
+  constexpr size_t TW = CF::kTW, SC = CF::kSC, DC = CF::kDC;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     char* q = base + off;
@@ -639,12 +682,13 @@ __host__ __device__ inline LdsState carve_lds(char* base, int32_t R, int32_t K, 
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
   w.work = (int32_t*)take(2 * 4 * S1);
-  w.vmask = (uint64_t*)take(8 * (size_t)kDistinctCap * kTierWords);
-  w.dexp = (int32_t*)take(4 * kDistinctCap); w.dmap = (int32_t*)take(4 * N_);
-  w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * kPlanes * kTierWords);
-  w.cn = (int32_t*)take(4 * kStructCap);
-  w.cv = (double*)take(8 * kStructCap * kTierMax); w.cvr = (int32_t*)take(4 * kStructCap * kTierMax);
-  w.cm = (uint64_t*)take(8 * kStructCap * kTierMax * kTierWords);
+  w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(4 * DC);
+  w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
+  w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * CF::kPL * TW);
+  w.cn = (int32_t*)take(4 * SC);
+  w.cv = (double*)take(8 * SC * kTierMax); w.cvr = (int32_t*)take(4 * SC * kTierMax);
+  w.cw = (uint32_t*)take(4 * SC * kTierMax);
+  w.cm = (uint64_t*)take(8 * SC * kTierMax * TW);
   w.bytes = end2 > off ? end2 : off;
   return w;
 }
@@ -652,25 +696,49 @@ __host__ __device__ inline LdsState carve_lds(char* base, int32_t R, int32_t K, 
 struct LdsParams {
   SchParams s;
   const int32_t* sidx;   // [R] host -> tier structure
-  const int32_t* cn;     // [kStructCap] tiers per structure
-  const double* cv;      // [kStructCap][kTierMax] tier bonuses, descending
-  const int32_t* cvr;    // [kStructCap][kTierMax] rank of each tier bonus among the table's
-  const uint64_t* cm;    // [kStructCap][kTierMax][kTierWords] tier rank sets
+  const int32_t* cn;     // [SC] tiers per structure
+  const double* cv;      // [SC][kTierMax] tier bonuses, descending
+  const int32_t* cvr;    // [SC][kTierMax] rank of each tier bonus among the table's
+  const uint32_t* cw;    // [SC][kTierMax] words holding ranks of the tier
+  const uint64_t* cm;    // [SC][kTierMax][TW] tier rank sets
   const int32_t* hdr;    // [0] structures, [1] LDS-resident auction exact
   int32_t* fallback;     // [B] 1 = left to schedule_kernel
-  int32_t* nprime;       // [B][kDistinctCap][R]
+  int32_t* nprime;       // [B][DC][R]
   int32_t NEC;           // candidate-expert capacity of the LDS layout
 };
 
-// Block-wide OR with one barrier; flags alternate between two halves of buf
-// ([2][kSchWaves]) so that a call never overwrites flags still being read.
-__device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
+// Exclusive position of `flag` among the NT threads (ascending thread id) and
+// the chunk total.  All threads must call it.
+template <int NT>
+__device__ __forceinline__ int32_t compact_pos_n(bool flag, int32_t* wave_cnt, int32_t& total) {
+  constexpr int NW = NT / kWave;
+  const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
   const uint64_t m = __ballot(flag);
-  if ((threadIdx.x & (kWave - 1)) == 0) buf[parity * kSchWaves + threadIdx.x / kWave] = m != 0;
+  const int32_t lp = __popcll(m & ((1ull << lane) - 1ull));
+  if (lane == 0) wave_cnt[wid] = __popcll(m);
+  __syncthreads();
+  int32_t off = 0, tot = 0;
+  for (int w = 0; w < NW; ++w) {
+    const int32_t c = wave_cnt[w];
+    off += w < wid ? c : 0;
+    tot += c;
+  }
+  __syncthreads();
+  total = tot;
+  return off + lp;
+}
+
+// Block-wide OR with one barrier; flags alternate between two halves of buf
+// ([2][NT / 64]) so that a call never overwrites flags still being read.
+template <int NT>
+__device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
+  constexpr int NW = NT / kWave;
+  const uint64_t m = __ballot(flag);
+  if ((threadIdx.x & (kWave - 1)) == 0) buf[parity * NW + threadIdx.x / kWave] = m != 0;
   __syncthreads();
   bool any = false;
 #pragma unroll
-  for (int w = 0; w < kSchWaves; ++w) any |= buf[parity * kSchWaves + w] != 0;
+  for (int w = 0; w < NW; ++w) any |= buf[parity * NW + w] != 0;
   parity ^= 1;
   return any;
 }
@@ -695,13 +763,14 @@ __device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
   return v;
 }
 
-// One problem per 256-thread workgroup; thread i owns Phase-3 slots
-// i, i + 256, ... (SPL of them).
-template <int SPL>
-__global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp) {
+// One problem per workgroup of CF::kT threads; thread i bids for list entries
+// i, i + kT, ... (SPL of them).
+template <class CF, int SPL>
+__global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
+  constexpr int NT = CF::kT, NW = NT / kWave, TW = CF::kTW;
   extern __shared__ __attribute__((aligned(16))) char lds_dyn[];
-  __shared__ int32_t wave_cnt[kSchWaves];
-  __shared__ int32_t flagbuf[2 * kSchWaves];
+  __shared__ int32_t wave_cnt[NW];
+  __shared__ int32_t flagbuf[2 * NW];
   __shared__ int32_t sh_maxc, sh_nw[2];
   __shared__ unsigned long long sh_sum, sh_big;
   const SchParams& p = wp.s;
@@ -710,7 +779,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
   const int32_t R = p.R, E = p.E, K = p.K;
   const int32_t S = R * K;
   int parity = 0;
-  LdsState L = carve_lds(lds_dyn, R, K, wp.NEC);
+  LdsState<CF> L = carve_lds<CF>(lds_dyn, R, K, wp.NEC);
 
   if (wp.hdr[1] == 0) {  // the LDS-resident auction would not be exact for this Bauct and step
     if (tid == 0) wp.fallback[b] = 1;
@@ -728,14 +797,14 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
 
   // ---- validation, candidates, cold ranks ------------------------------------------
   bool badh = false;
-  for (int32_t e = tid; e < E; e += kSchThreads) {
+  for (int32_t e = tid; e < E; e += NT) {
     const int32_t h = p.home[e];
     badh |= h < 0 || h >= R;
   }
   if (tid == 0) { sh_sum = 0; sh_big = 0; sh_maxc = 0; }
-  if (block_or(badh, flagbuf, parity)) {
-    for (int32_t s = tid; s < S; s += kSchThreads) { se[s] = -1; sa[s] = 0; }
-    for (int64_t q = tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
+  if (block_or<NT>(badh, flagbuf, parity)) {
+    for (int32_t s = tid; s < S; s += NT) { se[s] = -1; sa[s] = 0; }
+    for (int64_t q = tid; q < (int64_t)R * S; q += NT) Xb[q] = 0;
     if (tid == 0) {
       p.unfilled[b] = 0;
       if (p.rounds_used) { p.rounds_used[2 * b] = 0; p.rounds_used[2 * b + 1] = 0; }
@@ -746,12 +815,12 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
   }
   int32_t ne = 0, nc = 0;
   int64_t mass = 0, big = 0;  // amounts must fit the 32-bit LDS state
-  for (int32_t base = 0; base < E; base += kSchThreads) {
+  for (int32_t base = 0; base < E; base += NT) {
     const int32_t e = base + tid;
     const int64_t v = e < E ? spill[e] : 0;
     const bool f = v > 0;
     int32_t tot;
-    const int32_t pos = ne + compact_pos(f, wave_cnt, tot);
+    const int32_t pos = ne + compact_pos_n<NT>(f, wave_cnt, tot);
     if (f && pos < wp.NEC) {
       L.ce[pos] = e;
       L.spill_p[pos] = (int32_t)(v < INT_MAX ? v : INT_MAX);
@@ -760,12 +829,12 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
     ne += tot;
     mass += f ? v : 0;
   }
-  for (int32_t base = 0; base < R; base += kSchThreads) {
+  for (int32_t base = 0; base < R; base += NT) {
     const int32_t r = base + tid;
     const int64_t v = r < R ? spare[r] : 0;
     const bool f = v > 0;
     int32_t tot;
-    const int32_t pos = nc + compact_pos(f, wave_cnt, tot);
+    const int32_t pos = nc + compact_pos_n<NT>(f, wave_cnt, tot);
     if (f) { L.cr[pos] = r; L.spare_p[pos] = (int32_t)(v < INT_MAX ? v : INT_MAX); }
     nc += tot;
     big = v > big ? v : big;
@@ -785,20 +854,20 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
     if (tid == 0) wp.fallback[b] = 1;
     return;
   }
-  for (int32_t q = tid; q < nc * K; q += kSchThreads) L.assigned[q] = -1;
-  for (int32_t ec = tid; ec < ne; ec += kSchThreads) { L.ekey[ec] = 0; L.ewin[ec] = INT_MAX; }
-  for (int32_t s = tid; s < S; s += kSchThreads) { L.slot_ec[s] = -1; L.amt[s] = 0; se[s] = -1; }
+  for (int32_t q = tid; q < nc * K; q += NT) L.assigned[q] = -1;
+  for (int32_t ec = tid; ec < ne; ec += NT) { L.ekey[ec] = 0; L.ewin[ec] = INT_MAX; }
+  for (int32_t s = tid; s < S; s += NT) { L.slot_ec[s] = -1; L.amt[s] = 0; se[s] = -1; }
   __syncthreads();
 
   // ---- Phase 2: column-priority iterative matching ---------------------------------
   int32_t used2 = 0;
   for (int32_t k = 0; k < K; ++k) {
-    for (int32_t rc = tid; rc < nc; rc += kSchThreads) { L.matched[rc] = 0; L.prop_e[rc] = -1; }
+    for (int32_t rc = tid; rc < nc; rc += NT) { L.matched[rc] = 0; L.prop_e[rc] = -1; }
     __syncthreads();
     for (int32_t inner = 0; inner < nc; ++inner) {
       // Step 1: every unmatched cold rank proposes its best candidate expert
       bool proposed = false;
-      for (int32_t rc = tid; rc < nc; rc += kSchThreads) {
+      for (int32_t rc = tid; rc < nc; rc += NT) {
         if (L.matched[rc]) continue;
         int32_t best = -1;
         double bs = -INFINITY;
@@ -845,19 +914,19 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
         L.prop_s[rc] = bs;
         proposed |= best >= 0;
       }
-      if (!block_or(proposed, flagbuf, parity)) break;  // nothing can change any more
+      if (!block_or<NT>(proposed, flagbuf, parity)) break;  // nothing can change any more
       // Steps 2-3: each proposed expert keeps its best proposer: max score, then lowest rank
-      for (int32_t rc = tid; rc < nc; rc += kSchThreads)
+      for (int32_t rc = tid; rc < nc; rc += NT)
         if (L.prop_e[rc] >= 0)
           atomicMax(reinterpret_cast<unsigned long long*>(&L.ekey[L.prop_e[rc]]),
                     (unsigned long long)ordered_key(L.prop_s[rc]));
       __syncthreads();
-      for (int32_t rc = tid; rc < nc; rc += kSchThreads)
+      for (int32_t rc = tid; rc < nc; rc += NT)
         if (L.prop_e[rc] >= 0 && ordered_key(L.prop_s[rc]) == L.ekey[L.prop_e[rc]])
           atomicMin(&L.ewin[L.prop_e[rc]], rc);
       __syncthreads();
       // Step 4: winners take g = min(spill, spare) into slot k of their rank
-      for (int32_t ec = tid; ec < ne; ec += kSchThreads) {
+      for (int32_t ec = tid; ec < ne; ec += NT) {
         const int32_t w = L.ewin[ec];
         if (w != INT_MAX) {
           const int32_t g = L.spill_p[ec] < L.spare_p[w] ? L.spill_p[ec] : L.spare_p[w];
@@ -878,65 +947,76 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
       ++used2;
     }
   }
-  for (int32_t s = tid; s < S; s += kSchThreads) sa[s] = L.amt[s];
+  for (int32_t s = tid; s < S; s += NT) sa[s] = L.amt[s];
 
   // ---- Phase 3: Lagrangian auction ---------------------------------------------------
   // distinct slot experts, in ascending candidate (= expert) order
   __syncthreads();
-  for (int32_t ec = tid; ec < ne; ec += kSchThreads) L.dmap[ec] = 0;
+  for (int32_t ec = tid; ec < ne; ec += NT) L.dmap[ec] = 0;
   __syncthreads();
-  for (int32_t s = tid; s < S; s += kSchThreads)
+  for (int32_t s = tid; s < S; s += NT)
     if (L.slot_ec[s] >= 0) L.dmap[L.slot_ec[s]] = 1;
   __syncthreads();
   int32_t D = 0;
-  for (int32_t base = 0; base < ne; base += kSchThreads) {
+  for (int32_t base = 0; base < ne; base += NT) {
     const int32_t ec = base + tid;
     const bool f = ec < ne && L.dmap[ec] == 1;
     int32_t tot;
-    const int32_t pos = D + compact_pos(f, wave_cnt, tot);
+    const int32_t pos = D + compact_pos_n<NT>(f, wave_cnt, tot);
     if (ec < ne) L.dmap[ec] = f ? pos : -1;
-    if (f && pos < kDistinctCap) L.dexp[pos] = L.ce[ec];
+    if (f && pos < CF::kDC) L.dexp[pos] = L.ce[ec];
     D += tot;
   }
-  if (D > kDistinctCap) {
+  if (D > CF::kDC) {
     if (tid == 0) wp.fallback[b] = 1;
     return;
   }
   __syncthreads();
-  // tokens of each slot expert per rank (device memory) and the valid-rank
-  // sets; wave w covers ranks 64w .. 64w+63
-  int32_t* np = wp.nprime + b * (int64_t)kDistinctCap * R;
+  // tokens of each slot expert per rank (device memory), the valid-rank sets
+  // and the words of each set that hold ranks
+  int32_t* np = wp.nprime + b * (int64_t)CF::kDC * R;
   const int32_t* nb = p.n + b * (int64_t)R * E;
+  for (int32_t d = tid; d < D; d += NT) L.vwords[d] = 0u;
+  __syncthreads();
   for (int32_t d = 0; d < D; ++d) {
     const int32_t e = L.dexp[d];
-    const int32_t r = wid * kWave + lane;
-    const int32_t v = r < R ? nb[(int64_t)r * E + e] : 0;
-    if (r < R) np[(int64_t)d * R + r] = v;
-    const uint64_t m = __ballot(v > 0);
-    if (lane == 0) L.vmask[d * kTierWords + wid] = m;
+    for (int32_t w = wid; w < TW; w += NW) {
+      const int32_t r = w * kWave + lane;
+      const int32_t v = r < R ? nb[(int64_t)r * E + e] : 0;
+      if (r < R) np[(int64_t)d * R + r] = v;
+      const uint64_t m = __ballot(v > 0);
+      if (lane == 0) {
+        L.vmask[d * TW + w] = m;
+        if (m) atomicOr(&L.vwords[d], 1u << w);
+      }
+    }
   }
-  // the active-slot list of the first round: every slot with tokens planned;
-  // an entry packs (slot, slot-expert index, host tier structure)
+  // the active-slot list of the first round: every slot with tokens planned
   if (tid < 2) sh_nw[tid] = 0;
   __syncthreads();
-  for (int32_t base = 0; base < S; base += kSchThreads) {
+  for (int32_t base = 0; base < S; base += NT) {
     const int32_t s = base + tid;
     const int32_t ec = s < S ? L.slot_ec[s] : -1;
     const bool f = ec >= 0 && L.amt[s] > 0;
-    const int32_t item = f ? s | (L.dmap[ec] << 10) | (wp.sidx[s / K] << 16) : 0;
+    const int32_t item =
+        f ? s | (L.dmap[ec] << kItemSlotBits) | (wp.sidx[s / K] << (kItemSlotBits + kItemExpertBits)) : 0;
     list_append(f, item, L.work + S, &sh_nw[1]);  // the list of round 1 (odd)
   }
-  for (int32_t r = tid; r < R; r += kSchThreads) {
+  for (int32_t r = tid; r < R; r += NT) {
     L.price[r] = 0.0;
     L.rkey[r] = 0;
     L.rkey[R + r] = 0;
     L.cnt[r] = 0;
   }
-  for (int32_t q = tid; q < kPlanes * kTierWords; q += kSchThreads) L.planes[q] = 0ull;
+  for (int32_t q = tid; q < CF::kPL * TW; q += NT) L.planes[q] = 0ull;
   const int32_t ns = wp.hdr[0];
-  for (int32_t q = tid; q < ns; q += kSchThreads) L.cn[q] = wp.cn[q];
-  for (int32_t q = tid; q < ns * kTierMax; q += kSchThreads) { L.cv[q] = wp.cv[q]; L.cvr[q] = wp.cvr[q]; }
-  for (int32_t q = tid; q < ns * kTierMax * kTierWords; q += kSchThreads) L.cm[q] = wp.cm[q];
+  for (int32_t q = tid; q < ns; q += NT) L.cn[q] = wp.cn[q];
+  for (int32_t q = tid; q < ns * kTierMax; q += NT) {
+    L.cv[q] = wp.cv[q];
+    L.cvr[q] = wp.cvr[q];
+    L.cw[q] = wp.cw[q];
+  }
+  for (int32_t q = tid; q < ns * kTierMax * TW; q += NT) L.cm[q] = wp.cm[q];
   // X starts at zero; every (rank, slot) pair is served at most once (after a
   // transfer either the rank holds no more tokens of the slot's expert or the
   // slot is full), so transfers below are plain stores
@@ -944,10 +1024,10 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
     int4* x4 = reinterpret_cast<int4*>(Xb);
     const int64_t n4 = ((int64_t)R * S) / 4;
     if ((reinterpret_cast<uintptr_t>(Xb) & 15u) == 0) {
-      for (int64_t q = tid; q < n4; q += kSchThreads) x4[q] = make_int4(0, 0, 0, 0);
-      for (int64_t q = n4 * 4 + tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
+      for (int64_t q = tid; q < n4; q += NT) x4[q] = make_int4(0, 0, 0, 0);
+      for (int64_t q = n4 * 4 + tid; q < (int64_t)R * S; q += NT) Xb[q] = 0;
     } else {
-      for (int64_t q = tid; q < (int64_t)R * S; q += kSchThreads) Xb[q] = 0;
+      for (int64_t q = tid; q < (int64_t)R * S; q += NT) Xb[q] = 0;
     }
   }
   __syncthreads();
@@ -962,6 +1042,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
   const double step = p.price_step;
   const bool track = step > 0.0;  // counts order the prices; with step 0 all prices stay 0
   const int64_t tmax = p.t_max > 0 ? p.t_max : (int64_t)S * (R + 1);
+  constexpr uint32_t kSlotMask = (1u << kItemSlotBits) - 1u, kExpMask = (1u << kItemExpertBits) - 1u;
   int64_t rounds = 0;
   for (int64_t t = 1; t <= tmax; ++t) {
     const int cur = (int)(t & 1), prv = cur ^ 1;
@@ -971,14 +1052,14 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
     const int32_t maxc = sh_maxc;
     const int32_t nplanes = maxc > 0 ? 32 - __builtin_clz((uint32_t)maxc) : 0;
     if (tid == 0) sh_nw[prv] = 0;
-    for (int32_t r = tid; r < R; r += kSchThreads) L.rkey[prv * R + r] = 0;
+    for (int32_t r = tid; r < R; r += NT) L.rkey[prv * R + r] = 0;
     // ---- X: bids --------------------------------------------------------------------------
     int32_t item[SPL], bid[SPL], held[SPL];
     uint32_t key[SPL];
     bool any = false;
 #pragma unroll
     for (int i = 0; i < SPL; ++i) {
-      const int32_t q = i * kSchThreads + tid;
+      const int32_t q = i * NT + tid;
       item[i] = -1;
       bid[i] = -1;
       key[i] = 0;
@@ -986,72 +1067,107 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
       if (q >= nw) continue;
       const int32_t it = list[q];
       item[i] = it;
-      const int32_t s = it & 1023, d = (it >> 10) & 63, st = it >> 16;
+      const int32_t s = it & kSlotMask, d = (it >> kItemSlotBits) & kExpMask;
+      const int32_t st = it >> (kItemSlotBits + kItemExpertBits);
       // argmax over ranks holding tokens of the slot's expert of
       // Bauct[r][host] - price[r], lowest rank on ties, by tiers
       const int32_t nt = L.cn[st];
-      uint64_t valid[kTierWords];
-      double tvv[kTierMax];
-#pragma unroll
-      for (int w = 0; w < kTierWords; ++w) valid[w] = L.vmask[d * kTierWords + w];
-#pragma unroll
-      for (int ti = 0; ti < kTierMax; ++ti) tvv[ti] = L.cv[st * kTierMax + ti];
+      const uint64_t* vm = L.vmask + d * TW;
       double bs = -INFINITY;
       int32_t br = INT_MAX, bv = 0;
+      if constexpr (TW <= 4) {
+        // rank sets of at most 4 words live in registers: a candidate set in
+        // one word takes a one-word bit-slice, others a joint one
+        uint64_t valid[TW];
 #pragma unroll
-      for (int ti = 0; ti < kTierMax; ++ti) {
-        if (ti >= nt || tvv[ti] < bs) break;  // every score in this tier and the next is <= its bonus
-        const uint64_t* tm = L.cm + (st * kTierMax + ti) * kTierWords;
-        uint64_t c[kTierWords];
-        uint32_t wm = 0;  // words holding candidates
+        for (int w = 0; w < TW; ++w) valid[w] = vm[w];
+        for (int32_t ti = 0; ti < nt; ++ti) {
+          const double v = L.cv[st * kTierMax + ti];
+          if (v < bs) break;  // every score in this tier and the next is <= its bonus
+          const uint64_t* tm = L.cm + (st * kTierMax + ti) * TW;
+          uint64_t c[TW];
+          uint32_t wm = 0;  // words holding candidates
 #pragma unroll
-        for (int w = 0; w < kTierWords; ++w) {
-          c[w] = tm[w] & valid[w];
-          wm |= (c[w] != 0ull ? 1u : 0u) << w;
-        }
-        if (!wm) continue;
-        int32_t r;
-        if ((wm & (wm - 1)) == 0) {
-          // candidates within one 64-rank word (always so for tiers that are
-          // aligned groups of at most 64 ranks)
-          const int w = __builtin_ctz(wm);
-          uint64_t x = w == 0 ? c[0] : w == 1 ? c[1] : w == 2 ? c[2] : c[3];
-          if (track && (x & (x - 1))) {
-            // fewest services: keep the ranks with a 0 in each bit-plane, top
-            // down, whenever any remain (four planes per load batch)
-            for (int32_t j0 = nplanes - 1; j0 >= 0; j0 -= 4) {
-              uint64_t pl[4];
+          for (int w = 0; w < TW; ++w) {
+            c[w] = tm[w] & valid[w];
+            wm |= (c[w] != 0ull ? 1u : 0u) << w;
+          }
+          if (!wm) continue;
+          int32_t r;
+          if ((wm & (wm - 1)) == 0) {
+            const int w = __builtin_ctz(wm);
+            uint64_t x = 0;
 #pragma unroll
-              for (int u = 0; u < 4; ++u) pl[u] = j0 - u >= 0 ? L.planes[(j0 - u) * kTierWords + w] : 0ull;
+            for (int u = 0; u < TW; ++u) x = u == w ? c[u] : x;
+            if (track && (x & (x - 1))) {
+              // fewest services: keep the ranks with a 0 in each bit-plane, top
+              // down, whenever any remain (four planes per load batch)
+              for (int32_t j0 = nplanes - 1; j0 >= 0; j0 -= 4) {
+                uint64_t pl[4];
 #pragma unroll
-              for (int u = 0; u < 4; ++u) {
-                const uint64_t m = x & ~pl[u];
-                x = m ? m : x;
+                for (int u = 0; u < 4; ++u) pl[u] = j0 - u >= 0 ? L.planes[(j0 - u) * TW + w] : 0ull;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                  const uint64_t m = x & ~pl[u];
+                  x = m ? m : x;
+                }
               }
             }
-          }
-          r = w * kWave + __builtin_ctzll(x);
-        } else {
-          if (track) {
-            // the same over all words
-            for (int32_t j = nplanes - 1; j >= 0; --j) {
-              uint64_t m[kTierWords];
-              uint64_t mm = 0;
+            r = w * kWave + __builtin_ctzll(x);
+          } else {
+            if (track) {
+              for (int32_t j = nplanes - 1; j >= 0; --j) {
+                uint64_t m[TW];
+                uint64_t mm = 0;
 #pragma unroll
-              for (int w = 0; w < kTierWords; ++w) { m[w] = c[w] & ~L.planes[j * kTierWords + w]; mm |= m[w]; }
-              if (mm) {
+                for (int w = 0; w < TW; ++w) { m[w] = c[w] & ~L.planes[j * TW + w]; mm |= m[w]; }
+                if (mm) {
 #pragma unroll
-                for (int w = 0; w < kTierWords; ++w) c[w] = m[w];
+                  for (int w = 0; w < TW; ++w) c[w] = m[w];
+                }
               }
             }
-          }
-          r = INT_MAX;
+            r = INT_MAX;
 #pragma unroll
-          for (int w = kTierWords - 1; w >= 0; --w)
-            if (c[w]) r = w * kWave + __builtin_ctzll(c[w]);
+            for (int w = TW - 1; w >= 0; --w)
+              if (c[w]) r = w * kWave + __builtin_ctzll(c[w]);
+          }
+          const double sc = v - L.price[r];
+          if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; bv = L.cvr[st * kTierMax + ti]; }
         }
-        const double sc = tvv[ti] - L.price[r];
-        if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; bv = L.cvr[st * kTierMax + ti]; }
+      } else {
+        const uint32_t vw = L.vwords[d];
+        for (int32_t ti = 0; ti < nt; ++ti) {
+          const double v = L.cv[st * kTierMax + ti];
+          if (v < bs) break;  // every score in this tier and the next is <= its bonus
+          const uint64_t* tm = L.cm + (st * kTierMax + ti) * TW;
+          // fewest services among the tier's valid ranks, word by word over the
+          // words that hold both: keep the ranks with a 0 in each bit-plane, top
+          // down, whenever any remain; a word's minimum count is the planes
+          // where none remained
+          int32_t rr = INT_MAX;
+          uint32_t cmin = 0xFFFFFFFFu;
+          for (uint32_t words = L.cw[st * kTierMax + ti] & vw; words; words &= words - 1) {
+            const int w = __builtin_ctz(words);
+            uint64_t x = tm[w] & vm[w];
+            if (!x) continue;
+            uint32_t mn = 0;
+            if (track) {
+              for (int32_t j = nplanes - 1; j >= 0; --j) {
+                const uint64_t m = x & ~L.planes[j * TW + w];
+                if (m) x = m;
+                else mn |= 1u << j;
+              }
+            }
+            if (mn < cmin) {  // words ascend: equal counts keep the lower rank
+              cmin = mn;
+              rr = w * kWave + __builtin_ctzll(x);
+            }
+          }
+          if (rr == INT_MAX) continue;
+          const double sc = v - L.price[rr];
+          if (sc > bs || (sc == bs && rr < br)) { bs = sc; br = rr; bv = L.cvr[st * kTierMax + ti]; }
+        }
       }
       if (br != INT_MAX) {
         bid[i] = br;
@@ -1061,7 +1177,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
         any = true;
       }
     }
-    if (!block_or(any, flagbuf, parity)) break;  // no bid: the state is final
+    if (!block_or<NT>(any, flagbuf, parity)) break;  // no bid: the state is final
     // ---- Y: transfers -----------------------------------------------------------------------
     int32_t newmax = 0;
 #pragma unroll
@@ -1069,7 +1185,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
       const int32_t r = bid[i];
       bool keep = false;
       if (r >= 0) {
-        const int32_t s = item[i] & 1023, d = (item[i] >> 10) & 63;
+        const int32_t s = item[i] & kSlotMask, d = (item[i] >> kItemSlotBits) & kExpMask;
         int32_t a = L.amt[s];
         if (rk[r] == key[i]) {
           const int32_t have = held[i];
@@ -1086,13 +1202,15 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
               L.cnt[r] = c1;
               newmax = c1 > newmax ? c1 : newmax;
               for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
-                atomicXor(reinterpret_cast<unsigned long long*>(
-                              &L.planes[__builtin_ctz(flip) * kTierWords + (r >> 6)]),
+                atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]),
                           bit);
             }
           }
-          if (have - x <= 0)
-            atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * kTierWords + (r >> 6)]), ~bit);
+          if (have - x <= 0) {
+            const uint64_t old = atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * TW + (r >> 6)]), ~bit);
+            if constexpr (TW > 4)  // the word list only guides the per-word search
+              if ((old & ~bit) == 0ull) atomicAnd(&L.vwords[d], ~(1u << (r >> 6)));
+          }
         }
         keep = a > 0;
       }
@@ -1105,7 +1223,7 @@ __global__ void __launch_bounds__(kSchThreads) schedule_lds_kernel(LdsParams wp)
   }
 
   int64_t left = 0;
-  for (int32_t s = tid; s < S; s += kSchThreads) left += L.slot_ec[s] >= 0 ? L.amt[s] : 0;
+  for (int32_t s = tid; s < S; s += NT) left += L.slot_ec[s] >= 0 ? L.amt[s] : 0;
   left = wave_sum_i64(left);
   __syncthreads();
   if (tid == 0) sh_sum = 0;
@@ -1131,44 +1249,89 @@ struct SchWs {
   int32_t* fallback;   // [B]
   int32_t* ntier;      // [R]
   double* tv;          // [R][kTierMax]
-  uint64_t* tmask;     // [R][kTierMax][kTierWords]
+  uint64_t* tmask;     // [R][kTierMax][TW]
   int32_t* sidx;       // [R]
-  int32_t* cn;         // [kStructCap]
-  double* cv;          // [kStructCap][kTierMax]
-  int32_t* cvr;        // [kStructCap][kTierMax]
-  uint64_t* cm;        // [kStructCap][kTierMax][kTierWords]
+  int32_t* cn;         // [SC]
+  double* cv;          // [SC][kTierMax]
+  int32_t* cvr;        // [SC][kTierMax]
+  uint32_t* cw;        // [SC][kTierMax]
+  uint64_t* cm;        // [SC][kTierMax][TW]
   int32_t* hdr;        // [2]
-  int32_t* nprime;     // [B][kDistinctCap][R]
+  int32_t* nprime;     // [B][DC][R]
   int64_t slab_bytes;
   size_t bytes;
 };
 
+// The tables are sized for the larger configuration, which either may use.
 SchWs carve_sched(void* ws, int32_t B, int32_t R, int32_t E, int32_t K) {
   Carver c{static_cast<char*>(ws)};
   SchWs w;
+  const bool lds_path = R <= LdsLarge::kTW * kWave;
+  const size_t TW = LdsLarge::kTW, SC = LdsLarge::kSC, DC = lds_path ? LdsLarge::kDC : 0;
   w.slab_bytes = round_up((int64_t)carve_slab(nullptr, R, E, K).bytes, 256);
   w.slab = c.take<char>((size_t)w.slab_bytes * (B > 0 ? sched_grid(B) : 0));
   w.fallback = c.take<int32_t>((size_t)B);
   w.ntier = c.take<int32_t>((size_t)R);
   w.tv = c.take<double>((size_t)R * kTierMax);
-  w.tmask = c.take<uint64_t>((size_t)R * kTierMax * kTierWords);
+  w.tmask = c.take<uint64_t>((size_t)R * kTierMax * TW);
   w.sidx = c.take<int32_t>((size_t)R);
-  w.cn = c.take<int32_t>(kStructCap);
-  w.cv = c.take<double>(kStructCap * kTierMax);
-  w.cvr = c.take<int32_t>(kStructCap * kTierMax);
-  w.cm = c.take<uint64_t>(kStructCap * kTierMax * kTierWords);
+  w.cn = c.take<int32_t>(SC);
+  w.cv = c.take<double>(SC * kTierMax);
+  w.cvr = c.take<int32_t>(SC * kTierMax);
+  w.cw = c.take<uint32_t>(SC * kTierMax);
+  w.cm = c.take<uint64_t>(SC * kTierMax * TW);
   w.hdr = c.take<int32_t>(2);
-  w.nprime = c.take<int32_t>((size_t)B * kDistinctCap * R);
+  w.nprime = c.take<int32_t>((size_t)B * DC * R);
   w.bytes = c.off;
   return w;
 }
 
-constexpr size_t kLdsMax = 64 * 1024;
-
-template <int SPL>
-taot_status launch_lds(const LdsParams& wp, int32_t B, size_t lds, hipStream_t stream) {
-  hipLaunchKernelGGL(schedule_lds_kernel<SPL>, dim3((unsigned)B), dim3(kSchThreads), lds, stream, wp);
+template <class CF, int SPL>
+taot_status launch_lds_kernel(const LdsParams& wp, int32_t B, size_t lds, hipStream_t stream) {
+  if (lds > 65536 && hipFuncSetAttribute((const void*)schedule_lds_kernel<CF, SPL>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL((schedule_lds_kernel<CF, SPL>), dim3((unsigned)B), dim3(CF::kT), lds, stream, wp);
   return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
+}
+
+// Largest dynamic LDS a workgroup may use on the current device.
+size_t max_lds_per_block() {
+  static size_t cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536;
+  if (cached[dev] == 0) {
+    int v = 0;
+    cached[dev] = hipDeviceGetAttribute(&v, hipDeviceAttributeSharedMemPerBlockOptin, dev) == hipSuccess && v > 0
+                      ? (size_t)v
+                      : 65536;
+  }
+  return cached[dev];
+}
+
+// Prepasses and the LDS-resident kernel of configuration CF; false when its
+// layout does not fit (the general kernel then takes every problem).
+template <class CF>
+taot_status launch_lds_path(const SchParams& p, const SchWs& w, int32_t B, int32_t R, int32_t E, int32_t K,
+                            double price_step, hipStream_t stream, bool& launched) {
+  launched = false;
+  const int32_t NEC = E < CF::kNEC ? E : CF::kNEC;  // candidate experts (spill > 0) held in LDS
+  const int64_t S = (int64_t)R * K;
+  const size_t slds = carve_lds<CF>(nullptr, R, K, NEC).bytes;
+  if (R > CF::kTW * kWave || S <= 0 || S > CF::kMaxS || slds > max_lds_per_block()) return TAOT_OK;
+  hipLaunchKernelGGL(auction_tiers_kernel<CF::kTW>, dim3((unsigned)R), dim3(256), 0, stream, p.Bauct, R, w.ntier,
+                     w.tv, w.tmask);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(auction_struct_kernel<CF>, dim3(1), dim3(CF::kT), 0, stream, w.ntier, w.tv, w.tmask, R, S,
+                     price_step, w.sidx, w.cn, w.cv, w.cvr, w.cw, w.cm, w.hdr);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  const LdsParams wp{p, w.sidx, w.cn, w.cv, w.cvr, w.cw, w.cm, w.hdr, w.fallback, w.nprime, NEC};
+  taot_status st;
+  if (S <= CF::kT) st = launch_lds_kernel<CF, 1>(wp, B, slds, stream);
+  else if (S <= 2 * CF::kT) st = launch_lds_kernel<CF, 2>(wp, B, slds, stream);
+  else st = launch_lds_kernel<CF, 4>(wp, B, slds, stream);
+  launched = st == TAOT_OK;
+  return st;
 }
 
 }  // namespace
@@ -1186,27 +1349,11 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
   SchWs w = carve_sched(ws, B, R, E, K);
   SchParams p{n, spill, spare, excess, alpha, home, T, Bpref, Bauct, B, R, E, K, price_step, t_max,
               slot_expert, slot_amount, X, unfilled, rounds_used, status, w.slab, w.slab_bytes, w.fallback};
-  // LDS-resident path when its layout fits
-  const int32_t NEC = E < 256 ? E : 256;  // candidate experts (spill > 0) held in LDS
-  const int64_t S = (int64_t)R * K;
-  const size_t slds = carve_lds(nullptr, R, K, NEC).bytes;
-  const bool lds_ok = R <= kTierWords * kWave && S > 0 && S <= kMaxSlots && slds <= kLdsMax;
-  if (lds_ok) {
-    hipLaunchKernelGGL(auction_tiers_kernel, dim3((unsigned)R), dim3(256), 0, stream, Bauct, R, w.ntier, w.tv,
-                       w.tmask);
-    if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-    hipLaunchKernelGGL(auction_struct_kernel, dim3(1), dim3(256), 0, stream, w.ntier, w.tv, w.tmask, R, S,
-                       price_step, w.sidx, w.cn, w.cv, w.cvr, w.cm, w.hdr);
-    if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-    const LdsParams wp{p, w.sidx, w.cn, w.cv, w.cvr, w.cm, w.hdr, w.fallback, w.nprime, NEC};
-    taot_status st;
-    if (S <= 256) st = launch_lds<1>(wp, B, slds, stream);
-    else if (S <= 512) st = launch_lds<2>(wp, B, slds, stream);
-    else st = launch_lds<4>(wp, B, slds, stream);
-    if (st != TAOT_OK) return st;
-  } else {
-    p.fallback = nullptr;  // the general kernel takes every problem
-  }
+  bool launched = false;
+  taot_status st = launch_lds_path<LdsSmall>(p, w, B, R, E, K, price_step, stream, launched);
+  if (st == TAOT_OK && !launched) st = launch_lds_path<LdsLarge>(p, w, B, R, E, K, price_step, stream, launched);
+  if (st != TAOT_OK) return st;
+  if (!launched) p.fallback = nullptr;  // the general kernel takes every problem
   const size_t lds = (size_t)R * (sizeof(double) + sizeof(uint64_t) + 2 * sizeof(int32_t));
   if (lds > 65536 && hipFuncSetAttribute((const void*)schedule_kernel,
                                          hipFuncAttributeMaxDynamicSharedMemorySize,

@@ -100,8 +100,9 @@ def _instance(seed, R, E=None, N=None, B=2):
 
 @pytest.mark.parametrize("R", [63, 64, 65, 130, 200, 256, 300])
 def test_rank_counts(R, gpu):
-    """Rank sets span one to four 64-bit words (ragged last word); R = 300
-    exceeds the one-wave layout and runs on the general kernel."""
+    """Rank sets span one to five 64-bit words (ragged last word).  With E in
+    [R, 2R] some instances hold more distinct slot experts than the LDS layout
+    and run on the general kernel."""
     print(f"[schedule parity] R={R}", flush=True)
     _, L, home, T32, Bp, Ba = _instance(300 + R, R)
     _compare(L, home, T32, Bp, Ba, 2, label=f"R{R}")
@@ -140,3 +141,31 @@ def test_bonus_structures(kind, gpu):
         Ba = O.topology_pref(W.cost_matrix_for(R, ("two_tier", 1.0, 4.0)))[1]
         Ba[3, :] = np.inf
     _compare(L, home, T32, Bp, Ba, 2, label=kind)
+
+
+@pytest.mark.parametrize("R", [300, 512, 777, 1024])
+def test_large_rank_counts(R, gpu):
+    """R > 256 with few experts: the 1024-thread LDS layout (rank sets of up
+    to 16 words, fat-tree tiers aligned and unaligned to 64-rank words)."""
+    print(f"[schedule parity] large R={R}", flush=True)
+    rng = np.random.default_rng(900 + R)
+    E, N, B = 96, 200, 2
+    p = rng.dirichlet(np.full(E, 0.4))
+    ids = rng.choice(E, size=(B, R, N), p=p).astype(np.int32)
+    home = rng.integers(0, R, size=E).astype(np.int32)
+    L = O.plan_loads(ids, home, E)
+    C = W.cost_matrix_for(R, ("fat_tree", 1.0, 4.0, 16.0, 64) if R % 2 == 0 else ("three_tier", 1.0, 3.0, 8.0, 40))
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), 0.3, 40)
+    Bp, Ba = O.topology_pref(C)
+    _compare(L, home, P.T.astype(np.float32), Bp, Ba, 2, label=f"R{R}")
+
+
+def test_workload4_problem(gpu):
+    """One problem of the R = 1024 workload (4096 experts, ~11000 auction rounds)."""
+    w = W.WORKLOADS[4]
+    print("[schedule parity] workload 4 problem 0", flush=True)
+    _, L = oracle_inputs(w, [0])
+    C = W.cost_matrix(w)
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), w.eps, w.iters)
+    Bp, Ba = O.topology_pref(C)
+    _compare(L, W.home_map(w), P.T.astype(np.float32), Bp, Ba, w.K, label="cfg4")
