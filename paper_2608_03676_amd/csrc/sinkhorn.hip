@@ -34,6 +34,7 @@ namespace {
 
 constexpr int kSkThreads = 256;
 constexpr int kSkWaves = kSkThreads / kWave;
+constexpr int kSkStreamThreads = 1024;  // threads per problem of the streamed kernel
 constexpr float kLo = 0x1p-20f;
 constexpr float kHi = 0x1p20f;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -77,7 +78,8 @@ struct SkParams {
   int32_t all_streamed;  // every problem goes to the streamed kernel
 };
 
-// Block-wide exclusive compaction position of `flag` within a 256-thread chunk.
+// Block-wide exclusive compaction position of `flag` within an NT-thread chunk.
+template <int NT = kSkThreads>
 __device__ __forceinline__ int32_t chunk_compact(bool flag, int32_t* wave_cnt, int32_t& total) {
   const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
   const uint64_t m = __ballot(flag);
@@ -85,7 +87,7 @@ __device__ __forceinline__ int32_t chunk_compact(bool flag, int32_t* wave_cnt, i
   if (lane == 0) wave_cnt[wid] = __popcll(m);
   __syncthreads();
   int32_t off = 0, tot = 0;
-  for (int w = 0; w < kSkWaves; ++w) {
+  for (int w = 0; w < NT / kWave; ++w) {
     const int32_t c = wave_cnt[w];
     off += w < wid ? c : 0;
     tot += c;
@@ -95,11 +97,14 @@ __device__ __forceinline__ int32_t chunk_compact(bool flag, int32_t* wave_cnt, i
   return off + lp;
 }
 
-template <bool STREAM>
-__global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
+// NT threads per problem: 256 for the LDS variant (several problems per
+// compute unit), 1024 for the streamed one (few, large problems).
+template <bool STREAM, int NT>
+__global__ void __launch_bounds__(NT) sinkhorn_kernel(SkParams p) {
+  constexpr int NW = NT / kWave;
   extern __shared__ float lds[];
-  __shared__ int32_t wave_cnt[kSkWaves];
-  __shared__ double red_d[2][kSkWaves];
+  __shared__ int32_t wave_cnt[NW];
+  __shared__ double red_d[2][NW];
   __shared__ int32_t sh_bad;
 
   const int64_t pb = blockIdx.x;
@@ -128,7 +133,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   if (tid == 0) sh_bad = 0;
   __syncthreads();
   double sa = 0.0, sd = 0.0;
-  for (int32_t i = tid; i < R; i += kSkThreads) {
+  for (int32_t i = tid; i < R; i += NT) {
     const float ai = a[i], bi = bd[i];
     if (!(ai >= 0.f && ai <= 3.402823466e38f) || !(bi >= 0.f && bi <= 3.402823466e38f)) sh_bad = 1;
     sa += (double)ai;
@@ -141,19 +146,19 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   if (lane == 0) { red_d[0][wid] = sa; red_d[1][wid] = sd; }
   __syncthreads();
   double Sa = 0.0, Sd = 0.0;
-  for (int w = 0; w < kSkWaves; ++w) { Sa += red_d[0][w]; Sd += red_d[1][w]; }
+  for (int w = 0; w < NW; ++w) { Sa += red_d[0][w]; Sd += red_d[1][w]; }
   double gamma = Sd / (Sa > kEps0 ? Sa : kEps0);
   gamma = gamma < 1.0 ? gamma : 1.0;
 
   int32_t nh = 0, nc = 0;
-  for (int32_t base = 0; base < R; base += kSkThreads) {
+  for (int32_t base = 0; base < R; base += NT) {
     const int32_t i = base + tid;
     const bool in = i < R;
     const float ai = in ? a[i] : 0.f, bi = in ? bd[i] : 0.f;
     int32_t th, tc;
-    const int32_t ph = chunk_compact(in && ai > 0.f, wave_cnt, th);
+    const int32_t ph = chunk_compact<NT>(in && ai > 0.f, wave_cnt, th);
     if (in && ai > 0.f) { hidx[nh + ph] = i; hpos[i] = nh + ph; sA[nh + ph] = (float)(gamma * (double)ai); }
-    const int32_t pc = chunk_compact(in && bi > 0.f, wave_cnt, tc);
+    const int32_t pc = chunk_compact<NT>(in && bi > 0.f, wave_cnt, tc);
     if (in && bi > 0.f) { cidx[nc + pc] = i; cpos[i] = nc + pc; sB[nc + pc] = bi; }
     nh += th;
     nc += tc;
@@ -177,7 +182,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
 
   // ---- first row update over all R columns (g = 0): F_i = log2 s~_i - LSE2_j(-C'_ij)
   if (!degenerate) {
-    for (int32_t ii = wid; ii < nh; ii += kSkWaves) {
+    for (int32_t ii = wid; ii < nh; ii += NW) {
       const float* crow = Cb + (int64_t)hidx[ii] * R;
       float mx = -INFINITY;
       bool badc = false;
@@ -193,7 +198,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
       s = wave_sum(s);
       if (lane == 0) { F[ii] = flog2(sA[ii]) - (mx + flog2(s)); u[ii] = 1.f; }
     }
-    for (int32_t jj = tid; jj < nc; jj += kSkThreads) { G[jj] = 0.f; v[jj] = 1.f; }
+    for (int32_t jj = tid; jj < nc; jj += NT) { G[jj] = 0.f; v[jj] = 1.f; }
   }
   __syncthreads();
 
@@ -202,8 +207,8 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   else if (nh == 0 || nc == 0) st = TAOT_ST_ZERO_MASS;
   if (st) {
     if (p.T)
-      for (int64_t q = tid; q < (int64_t)R * R; q += kSkThreads) p.T[pb * R * R + q] = 0.f;
-    for (int32_t i = tid; i < R; i += kSkThreads) {
+      for (int64_t q = tid; q < (int64_t)R * R; q += NT) p.T[pb * R * R + q] = 0.f;
+    for (int32_t i = tid; i < R; i += NT) {
       if (p.f) p.f[pb * R + i] = -INFINITY;
       if (p.g) p.g[pb * R + i] = -INFINITY;
     }
@@ -212,7 +217,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   }
 
   // ---- build Kt = exp2(F_i + G_j - C'_ij) on H x C ----------------------------
-  for (int64_t q = tid; q < need; q += kSkThreads) {
+  for (int64_t q = tid; q < need; q += NT) {
     const int32_t ii = (int32_t)(q / nc), jj = (int32_t)(q % nc);
     const float c = Cb[(int64_t)hidx[ii] * R + cidx[jj]];
     K[q] = fexp2((F[ii] + G[jj]) - c * kappa);
@@ -222,7 +227,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
   for (int32_t it = 1; it <= p.iters; ++it) {
     if (it > 1) {
       // ---- row update: u_i = s~_i / sum_j Kt_ij v_j  (one wave per row) -------
-      for (int32_t ii = wid; ii < nh; ii += kSkWaves) {
+      for (int32_t ii = wid; ii < nh; ii += NW) {
         const float* krow = K + (int64_t)ii * nc;
         float y = 0.f;
         for (int32_t jj = lane; jj < nc; jj += kWave) y = __builtin_fmaf(krow[jj], v[jj], y);
@@ -251,7 +256,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
       __syncthreads();
     }
     // ---- column update: v_j = d_j / sum_i u_i Kt_ij  (one thread per column) ---
-    for (int32_t jj = tid; jj < nc; jj += kSkThreads) {
+    for (int32_t jj = tid; jj < nc; jj += NT) {
       float x = 0.f;
       for (int32_t ii = 0; ii < nh; ++ii) x = __builtin_fmaf(u[ii], K[(int64_t)ii * nc + jj], x);
       const float vn = sB[jj] * frcp(x);
@@ -278,7 +283,7 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
 
   // ---- plan, column cap, outputs -----------------------------------------------
   const bool colcap = !(p.flags & TAOT_SK_NO_COLCAP);
-  for (int32_t jj = tid; jj < nc; jj += kSkThreads) {
+  for (int32_t jj = tid; jj < nc; jj += NT) {
     float c = 0.f;
     if (colcap)
       for (int32_t ii = 0; ii < nh; ++ii) c += u[ii] * K[(int64_t)ii * nc + jj] * v[jj];
@@ -290,14 +295,14 @@ __global__ void __launch_bounds__(kSkThreads) sinkhorn_kernel(SkParams p) {
     float* Tb = p.T + pb * R * R;
     for (int32_t i = 0; i < R; ++i) {
       const int32_t ii = hpos[i];
-      for (int32_t j = tid; j < R; j += kSkThreads) {
+      for (int32_t j = tid; j < R; j += NT) {
         const int32_t jj = cpos[j];
         Tb[(int64_t)i * R + j] = (ii >= 0 && jj >= 0) ? u[ii] * K[(int64_t)ii * nc + jj] * cap[jj] : 0.f;
       }
     }
   }
   const float to_nat = p.eps * kLn2;  // log2 units -> eps * ln
-  for (int32_t i = tid; i < R; i += kSkThreads) {
+  for (int32_t i = tid; i < R; i += NT) {
     const int32_t ii = hpos[i], jj = cpos[i];
     if (p.f) p.f[pb * R + i] = ii >= 0 ? (F[ii] + flog2(u[ii])) * to_nat : -INFINITY;
     if (p.g) p.g[pb * R + i] = jj >= 0 ? (G[jj] + flog2(v[jj])) * to_nat : -INFINITY;
@@ -1136,20 +1141,21 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
   if (lds_path) {
     p.lds_kt_cap = (int32_t)max_block(R);
     const size_t lds = vec_bytes + (size_t)p.lds_kt_cap * sizeof(float);
-    if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_kernel<false>,
+    if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_kernel<false, kSkThreads>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)lds) != hipSuccess)
       return TAOT_ERR_LAUNCH;
-    hipLaunchKernelGGL(sinkhorn_kernel<false>, dim3((unsigned)B), dim3(kSkThreads), lds, stream, p);
+    hipLaunchKernelGGL((sinkhorn_kernel<false, kSkThreads>), dim3((unsigned)B), dim3(kSkThreads), lds, stream, p);
     if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   } else {
     p.all_streamed = 1;
   }
-  if (vec_bytes > 65536 && hipFuncSetAttribute((const void*)sinkhorn_kernel<true>,
+  if (vec_bytes > 65536 && hipFuncSetAttribute((const void*)sinkhorn_kernel<true, kSkStreamThreads>,
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)vec_bytes) != hipSuccess)
     return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(sinkhorn_kernel<true>, dim3((unsigned)B), dim3(kSkThreads), vec_bytes, stream, p);
+  hipLaunchKernelGGL((sinkhorn_kernel<true, kSkStreamThreads>), dim3((unsigned)B), dim3(kSkStreamThreads), vec_bytes,
+                     stream, p);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   return TAOT_OK;
 }
