@@ -38,6 +38,8 @@ def parse():
                     help="oracle Sinkhorn passes over the sample repeat until this much time has passed")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (HBM counter calibration)")
+    ap.add_argument("--other-steps", type=int, default=3,
+                    help="timed steps for the planner latency of workloads 1-4 other than --workload (0: skip)")
     ap.add_argument("--json-out", default=None)
     return ap.parse_args()
 
@@ -90,6 +92,79 @@ def copy_calibration(mib):
                       "launches": 5}), flush=True)
 
 
+def run_workload(w, K, steps, warmup, dev):
+    """Device-generated inputs, preallocated outputs, `warmup` untimed steps,
+    then `steps` timed steps (HIP events on the launch stream)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_03676_amd as taot
+    import workloads as W
+    B, R, E, N = w.B, w.R, w.E, w.N
+    t0 = time.time()
+    thr, seeds = W.tables(w)
+    ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
+    W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
+                     B, E, R, w.tokens, w.k, ids)
+    home_np = W.home_map(w)
+    C_np = W.cost_matrix(w)
+    Bp_np, Ba_np = taot.topology_pref(C_np)
+    home = torch.from_numpy(home_np).to(dev)
+    C = torch.from_numpy(C_np).to(dev)
+    Bp = torch.from_numpy(Bp_np).to(dev)
+    Ba = torch.from_numpy(Ba_np).to(dev)
+    torch.cuda.synchronize()
+    log(f"[bench] generated {ids.numel() / 1e9:.2f} G ids ({ids.numel() * 4 / 2**30:.1f} GiB) in {time.time() - t0:.1f}s")
+
+    # preallocated outputs and workspaces
+    ws = taot.workspace_bytes(B, R, E, K)
+    wl = torch.empty(max(ws["plan_loads"], 1), dtype=torch.uint8, device=dev)
+    wsk = torch.empty(max(ws["sinkhorn"], 1), dtype=torch.uint8, device=dev)
+    wsc = torch.empty(max(ws["round_schedule"], 1), dtype=torch.uint8, device=dev)
+    loads = taot.plan_loads(ids, home, E, workspace=wl)
+    flow = taot.sinkhorn_batched(loads.supply, loads.demand, C, w.eps, w.iters, workspace=wsk)
+    sched = taot.round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T,
+                                Bp, Ba, K, w.price_step, 0, workspace=wsc)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        taot.plan_loads(ids, home, E, out=loads, workspace=wl)
+        if ev is not None:
+            ev[1].record(stream)
+        taot.sinkhorn_batched(loads.supply, loads.demand, C, w.eps, w.iters, out=flow, workspace=wsk)
+        if ev is not None:
+            ev[2].record(stream)
+        taot.round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T, Bp, Ba,
+                            K, w.price_step, 0, out=sched, workspace=wsc)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {warmup} done")
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for s in range(steps):
+        step(events[s])
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / steps
+    loads_ms = [e[0].elapsed_time(e[1]) for e in events]
+    sk_ms = [e[1].elapsed_time(e[2]) for e in events]
+    sch_ms = [e[2].elapsed_time(e[3]) for e in events]
+    log(f"[bench] {steps} steps: {ms_step:.3f} ms/step (plan_loads {statistics.mean(loads_ms):.3f}, "
+        f"sinkhorn {statistics.mean(sk_ms):.3f}, round_schedule {statistics.mean(sch_ms):.3f} ms)")
+    del ids
+    return dict(loads=loads, flow=flow, sched=sched, home_np=home_np, C_np=C_np, Bp_np=Bp_np, Ba_np=Ba_np,
+                loads_ms=loads_ms, sk_ms=sk_ms, sch_ms=sch_ms, ms_step=ms_step)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -110,70 +185,10 @@ def main():
     K = w.K if args.K is None else args.K
     B, R, E, N = w.B, w.R, w.E, w.N
     log(f"[bench] workload {w.index}: {w.name}; B={B} R={R} E={E} N={N} iters={w.iters} K={K}")
-
-    # ---- inputs, generated on the device --------------------------------------
-    t0 = time.time()
-    thr, seeds = W.tables(w)
-    ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
-    W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
-                     B, E, R, w.tokens, w.k, ids)
-    home_np = W.home_map(w)
-    C_np = W.cost_matrix(w)
-    Bp_np, Ba_np = taot.topology_pref(C_np)
-    home = torch.from_numpy(home_np).to(dev)
-    C = torch.from_numpy(C_np).to(dev)
-    Bp = torch.from_numpy(Bp_np).to(dev)
-    Ba = torch.from_numpy(Ba_np).to(dev)
-    torch.cuda.synchronize()
-    log(f"[bench] generated {ids.numel() / 1e9:.2f} G ids ({ids.numel() * 4 / 2**30:.1f} GiB) in {time.time() - t0:.1f}s")
-
-    # ---- preallocated outputs and workspaces ------------------------------------
-    ws = taot.workspace_bytes(B, R, E, K)
-    wl = torch.empty(max(ws["plan_loads"], 1), dtype=torch.uint8, device=dev)
-    wsk = torch.empty(max(ws["sinkhorn"], 1), dtype=torch.uint8, device=dev)
-    wsc = torch.empty(max(ws["round_schedule"], 1), dtype=torch.uint8, device=dev)
-    loads = taot.plan_loads(ids, home, E, workspace=wl)
-    flow = taot.sinkhorn_batched(loads.supply, loads.demand, C, w.eps, w.iters, workspace=wsk)
-    sched = taot.round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T,
-                                Bp, Ba, K, w.price_step, 0, workspace=wsc)
-    torch.cuda.synchronize()
-
-    stream = torch.cuda.current_stream()
-
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        taot.plan_loads(ids, home, E, out=loads, workspace=wl)
-        if ev is not None:
-            ev[1].record(stream)
-        taot.sinkhorn_batched(loads.supply, loads.demand, C, w.eps, w.iters, out=flow, workspace=wsk)
-        if ev is not None:
-            ev[2].record(stream)
-        taot.round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T, Bp, Ba,
-                            K, w.price_step, 0, out=sched, workspace=wsc)
-        if ev is not None:
-            ev[3].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} done")
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for s in range(args.steps):
-        step(events[s])
-    end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms_step = total_ms / args.steps
-    loads_ms = [e[0].elapsed_time(e[1]) for e in events]
-    sk_ms = [e[1].elapsed_time(e[2]) for e in events]
-    sch_ms = [e[2].elapsed_time(e[3]) for e in events]
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (plan_loads {statistics.mean(loads_ms):.3f}, "
-        f"sinkhorn {statistics.mean(sk_ms):.3f}, round_schedule {statistics.mean(sch_ms):.3f} ms)")
+    run = run_workload(w, K, args.steps, args.warmup, dev)
+    loads, flow, sched = run["loads"], run["flow"], run["sched"]
+    home_np, C_np, Bp_np, Ba_np = run["home_np"], run["C_np"], run["Bp_np"], run["Ba_np"]
+    loads_ms, sk_ms, sch_ms, ms_step = run["loads_ms"], run["sk_ms"], run["sch_ms"], run["ms_step"]
 
     # ---- algorithmic work of each stage --------------------------------------------
     st_loads = loads.status.cpu().numpy().view(np.uint32)
@@ -226,6 +241,26 @@ def main():
         "status": {"loads_nonzero": int((st_loads != 0).sum()), "sinkhorn_nonzero": int((st_flow != 0).sum()),
                    "schedule_unfilled": unfilled, "schedule_nonzero": int((st_sched != 0).sum())},
     }
+
+    # ---- planner latency of the other full-size workloads (fewer steps) -------------
+    if args.other_steps > 0:
+        lat = {str(w.index): {"problems": B, "ranks": R, "ms_per_step": ms_step, "plan_loads_ms": mean(loads_ms),
+                              "sinkhorn_ms": mean(sk_ms), "round_schedule_ms": mean(sch_ms)}}
+        del run, loads, flow, sched
+        torch.cuda.empty_cache()
+        for wi in (1, 2, 3, 4):
+            if wi == w.index:
+                continue
+            wo = W.WORKLOADS[wi]
+            log(f"[bench] planner latency, workload {wi}: {wo.name}")
+            r2 = run_workload(wo, wo.K, args.other_steps, 1, dev)
+            lat[str(wi)] = {"problems": wo.B, "ranks": wo.R, "ms_per_step": r2["ms_step"],
+                            "plan_loads_ms": mean(r2["loads_ms"]), "sinkhorn_ms": mean(r2["sk_ms"]),
+                            "round_schedule_ms": mean(r2["sch_ms"]),
+                            "unfilled": int(r2["sched"].unfilled.sum().item())}
+            del r2
+            torch.cuda.empty_cache()
+        rec["planner_latency_by_workload"] = dict(sorted(lat.items()))
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----------
     if args.cpu_sample > 0:
