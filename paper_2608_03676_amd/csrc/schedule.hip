@@ -743,6 +743,23 @@ __device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
   return any;
 }
 
+// block_or whose barrier orders LDS only: device-memory loads issued before it
+// may still be in flight after it (for values this thread itself uses later).
+template <int NT>
+__device__ __forceinline__ bool block_or_lds(bool flag, int32_t* buf, int& parity) {
+  constexpr int NW = NT / kWave;
+  const uint64_t m = __ballot(flag);
+  if ((threadIdx.x & (kWave - 1)) == 0) buf[parity * NW + threadIdx.x / kWave] = m != 0;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  bool any = false;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) any |= buf[parity * NW + w] != 0;
+  parity ^= 1;
+  return any;
+}
+
 // Appends the flagged items of a wave to a list whose length lives in LDS
 // (*count); the order of the list is unspecified.  All lanes must call it.
 __device__ __forceinline__ void list_append(bool flag, int32_t item, int32_t* list, int32_t* count) {
@@ -1177,7 +1194,9 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
         any = true;
       }
     }
-    if (!block_or<NT>(any, flagbuf, parity)) break;  // no bid: the state is final
+    // no bid: the state is final.  The barrier orders the keys (LDS); the
+    // token loads above complete on their own before Y uses them.
+    if (!block_or_lds<NT>(any, flagbuf, parity)) break;
     // ---- Y: transfers -----------------------------------------------------------------------
     int32_t newmax = 0;
 #pragma unroll
