@@ -56,8 +56,12 @@ typedef enum {
 #define TAOT_SK_NO_COLCAP 0x1u    /* skip the column-cap safeguard                      */
 #define TAOT_SK_FORCE_STREAM 0x2u /* keep the plan block in device memory even when it
                                      would fit on chip (exercises the large-R path)  */
-#define TAOT_SK_NO_REGISTER 0x4u  /* do not use the register-resident one-wave path
+#define TAOT_SK_NO_REGISTER 0x4u  /* do not use the register-resident path
                                      (exercises the LDS-resident path)               */
+#define TAOT_SK_WAVES_1 0x8u      /* run each register-resident problem on one wave
+                                     where its rows fit one wave's registers (by
+                                     default small batches spread a problem over
+                                     up to four waves)                              */
 
 /* Returns a static description of a status code (host, never NULL). */
 const char* taot_status_string(taot_status s);

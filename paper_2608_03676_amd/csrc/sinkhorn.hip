@@ -25,7 +25,7 @@
 // all iterations fused); problems whose block does not fit are flagged and
 // handled by sinkhorn_kernel<true>, which streams Kt through device memory
 // (L2-resident at the sizes used here).
-#include <mutex>
+#include <algorithm>
 
 #include "common.h"
 
@@ -46,9 +46,9 @@ __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(
 __device__ __forceinline__ float flog2(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ float frcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
-// Register-resident one-wave path: the |H| x |C| block lives on one wave, CPL
-// columns per lane (|C| <= 64*CPL) and 8*C8 rows (|H| <= 8*C8).  Class 0 is
-// every other problem (degenerate, larger, or the path switched off).
+// Register classes: CPL columns per lane (|C| <= 64*CPL) and 8*C8 rows
+// (|H| <= 8*C8).  Class 0 is every other problem (degenerate, larger, or the
+// register path switched off).
 __host__ __device__ constexpr int cpl_index(int cpl) { return cpl == 1 ? 0 : cpl == 2 ? 1 : 2; }
 __host__ __device__ constexpr int wave_class(int cpl, int c8) { return 1 + cpl_index(cpl) * 8 + (c8 - 1); }
 __device__ __forceinline__ int classify(int32_t nh, int32_t nc, uint32_t flags) {
@@ -311,18 +311,64 @@ __global__ void __launch_bounds__(NT) sinkhorn_kernel(SkParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Register-resident path: one 64-lane wave per problem, no barriers between
-// half-steps.  Lane l owns compact columns l, l+64, ... (CPL of them) and holds
-// Kt[i][c] for all 8*C8 rows: in VGPRs for the first 8*RC rows, in a per-wave
-// LDS tile for the rest (only when CPL = 4 and |H| > 48, which keeps the
-// kernel at <= 256 registers and two waves per SIMD).
-//   column half-step: x_c = sum_i u_i Kt_ic  (u_i broadcast with v_readlane)
+// Register-resident path.  A problem's |H| x |C| block of Kt lives in the
+// VGPRs of NW waves of one workgroup (NW = 1, 2 or 4).  Lane l of every wave
+// owns compact columns l, l+64, ... (CPL of them); wave w holds the rows of
+// chunks w*C8W .. w*C8W + C8W-1 (8 rows per chunk).
 //   row half-step:    p_i = sum_c Kt_ic v_c per lane, then a transposed
 //                     butterfly reduce-scatter over the 64 lanes (8 rows at a
 //                     time: permlane32/16 swaps, then DPP) leaves the total of
-//                     row 8q + (l >> 3) in lane l.
-// An out-of-range scaling triggers the exact log-domain update of all rows
-// (or all columns) with Kt rebuilt from the new potentials.
+//                     row 8q + (l >> 3) in lane l; rows never leave their wave.
+//   column half-step: x_c = sum_i u_i Kt_ic over the wave's rows, the row
+//                     scalings broadcast through LDS; with NW > 1 the waves'
+//                     partial sums meet in LDS (one barrier per iteration) and
+//                     are added in wave order, so every wave derives the same
+//                     v and takes the same branches.
+// An out-of-range scaling triggers the exact log-domain update of the wave's
+// rows (or of all columns), absorbed into the potentials, with Kt rebuilt.
+//
+// Launch shape.  One kernel runs every register problem of a batch, with
+// workgroups of W waves (W = 4 when the batch is small enough that every
+// problem can hold four waves at once, else W = 2).  A workgroup runs either
+// one problem on all W waves ("multi") or W problems on one wave each
+// ("single"), never two multi-wave problems, so workgroup barriers only ever
+// join the waves of one problem.
+//   W = 4 (at most 128 VGPRs, four waves per SIMD): problems of one chunk are
+//     single; the rest are multi with ceil(C8 / 4) chunks per wave.
+//   W = 2 (at most 256 VGPRs, two waves per SIMD): a problem is single when
+//     its block fits one wave's 192 Kt registers, else (4 columns per lane and
+//     more than 48 hot ranks) multi with ceil(C8 / 2) chunks per wave.
+// Small batches thus spread a problem over more waves (a shorter dependent
+// chain per wave, more waves per SIMD), while a batch that fills the chip
+// with one wave per problem avoids the per-iteration exchange.
+
+__host__ __device__ constexpr int max_c8_single(int W, int cpl) {
+  return W == 4 ? 1 : (192 / (8 * cpl) < 8 ? 192 / (8 * cpl) : 8);
+}
+__host__ __device__ constexpr bool is_single(int W, int cpl, int c8) { return c8 <= max_c8_single(W, cpl); }
+__host__ __device__ constexpr int c8_per_wave(int W, int cpl, int c8) {
+  return is_single(W, cpl, c8) ? c8 : (c8 + W - 1) / W;
+}
+// Shapes compiled into the W-wave kernel for NW = 1 (single) or NW = W.
+__host__ __device__ constexpr bool shape_ok(int W, int nw, int cpl, int c8w) {
+  return nw == 1 ? c8w >= 1 && c8w <= max_c8_single(W, cpl)
+                 : nw == W && (W == 4 ? c8w >= 1 && c8w <= 2 : cpl == 4 && c8w == 4);
+}
+__host__ __device__ constexpr bool shapes_covered() {
+  for (int W = 2; W <= 4; W += 2)
+    for (int ci = 0; ci < 3; ++ci)
+      for (int c8 = 1; c8 <= 8; ++c8) {
+        const int cpl = 1 << ci;
+        const int nw = is_single(W, cpl, c8) ? 1 : W;
+        if (!shape_ok(W, nw, cpl, c8_per_wave(W, cpl, c8))) return false;
+      }
+  return true;
+}
+static_assert(shapes_covered(), "every register class must map to a compiled shape");
+
+// Decoded register class.
+__device__ __forceinline__ int class_cpl(int32_t cls) { return 1 << ((cls - 1) / 8); }
+__device__ __forceinline__ int class_c8(int32_t cls) { return (cls - 1) % 8 + 1; }
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {
@@ -339,9 +385,6 @@ __device__ __forceinline__ void swap16(float& lo, float& hi) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(lo), __float_as_uint(hi), false, false);
   lo = __uint_as_float(r[0]);
   hi = __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float bcast(float x, int lane) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
 }
 __device__ __forceinline__ float first_lane(float x) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
@@ -366,381 +409,241 @@ __device__ __forceinline__ float reduce8(float (&p)[8], int lane) {
   return y;
 }
 
-// Iterations and outputs for one problem of class (CPL, C8); the caller has
-// filled the LDS vectors and the first-update potentials Fl.
-template <int CPL, int C8>
+// LDS of the register kernels, per workgroup: floats sA, F, u [64], the
+// waves' column potentials [NW][4][64] and column demands [NW][64][4], for
+// NW > 1 the column exchange [2 parities][NW][4][64]; then ints: a flag [4],
+// cpos, hpos [R], cidx [256], hidx [64].
+__host__ __device__ constexpr size_t wave_lds_floats(int nw) {
+  return (size_t)3 * 64 + (size_t)2 * nw * 4 * 64 + (nw > 1 ? (size_t)2 * nw * 4 * 64 : 0);
+}
+__host__ __device__ constexpr size_t wave_lds_bytes(int32_t R, int nw) {
+  return wave_lds_floats(nw) * 4 + (size_t)(4 + 2 * R + 256 + 64) * 4;
+}
+
+// Synchronisation among the waves of one problem: the workgroup barrier when
+// the problem has the whole workgroup; for a one-wave problem (possibly beside
+// other one-wave problems of the workgroup) an LDS fence of the wave.
+template <int NW>
+__device__ __forceinline__ void psync() {
+  if constexpr (NW > 1) {
+    __syncthreads();
+  } else {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// Iterations and outputs of one problem on NW waves of CPL columns per lane
+// and C8W chunks per wave; the caller has filled the LDS vectors and the
+// first-update potentials Fl.
+template <int CPL, int C8W, int NW, int WV>
 __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
                                            const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
                                            const int32_t* hidx, const float* sAl, float* Fl, float* ul,
-                                           float kappa) {
-  constexpr int MAXH = 8 * C8;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int32_t R = p.R;
-  const float* bd = p.b + pb * R;
-  const float* Cb = p.C + pb * p.C_stride;
-
-  float K[MAXH][CPL];
-  // row i (static after unrolling) of the lane's columns
-  auto kget = [&](int i, int c) -> float { return K[i][c]; };
-  auto kset = [&](int i, int c, float val) { K[i][c] = val; };
-
-  // per-lane column state; the column ids and validity are recomputed from
-  // LDS / the lane index where needed to keep the kernel within 256 VGPRs
-#define CV(c) (lane + kWave * (c) < nc)
-#define CJ(c) (CV(c) ? cidx[lane + kWave * (c)] : 0)
-  // xb / yb are 1 for padding columns / rows and 0 otherwise: added to the
-  // sums of zero padding they keep the scalings finite (0) without selects,
-  // and added to the scalings they keep padding inside the range check
-  float sB[CPL], G[CPL], v[CPL], xb[CPL];
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    sB[c] = CV(c) ? bd[CJ(c)] : 0.f;
-    G[c] = 0.f;
-    v[c] = CV(c) ? 1.f : 0.f;
-    xb[c] = CV(c) ? 0.f : 1.f;
-  }
-  // row-owned values: lane l carries row 8q + (l >> 3) of chunk q
-#define RV(q) (8 * (q) + (lane >> 3) < nh)
-  float uq[C8], yb[C8];
-#pragma unroll
-  for (int q = 0; q < C8; ++q) {
-    uq[q] = RV(q) ? 1.f : 0.f;
-    yb[q] = RV(q) ? 0.f : 1.f;
-  }
-#pragma unroll
-  for (int i = 0; i < MAXH; ++i) {
-    if (i < nh) {
-      const float Fi = Fl[i];
-      const float* crow = Cb + (int64_t)hidx[i] * R;
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) kset(i, c, CV(c) ? fexp2(Fi - crow[CJ(c)] * kappa) : 0.f);
-    } else {
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) kset(i, c, 0.f);
-    }
-  }
-
-  for (int32_t it = 1; it <= p.iters; ++it) {
-    if (it > 1) {
-      // ---- row half-step: u_i = s~_i / sum_c Kt_ic v_c ------------------------------
-      uint32_t lo = 0xFFFFFFFFu, hi = 0u;  // range of the scalings' bit patterns
-#pragma unroll
-      for (int q = 0; q < C8; ++q) {
-        float pp[8];
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          float acc = kget(8 * q + r, 0) * v[0];
-#pragma unroll
-          for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(kget(8 * q + r, c), v[c], acc);
-          pp[r] = acc;
-        }
-        const float y = reduce8(pp, lane);
-        const float un = sAl[8 * q + (lane >> 3)] * frcp(y + yb[q]);
-        const uint32_t bits = __float_as_uint(un + yb[q]);
-        lo = bits < lo ? bits : lo;
-        hi = bits > hi ? bits : hi;
-        uq[q] = un;
-      }
-      // outside [kLo, kHi], negative, infinite or NaN
-      const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
-      if (__ballot(fail) != 0) {
-        // exact log-domain update of every row, absorbed into F
-#pragma unroll
-        for (int i = 0; i < MAXH; ++i) {
-          if (i < nh) {
-            const float* crow = Cb + (int64_t)hidx[i] * R;
-            float t[CPL];
-            float mx = -INFINITY;
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-              t[c] = CV(c) ? (G[c] + flog2(v[c])) - crow[CJ(c)] * kappa : -INFINITY;
-              mx = fmaxf(mx, t[c]);
-            }
-            mx = wave_max(mx);
-            float sum = 0.f;
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
-            sum = first_lane(wave_sum(sum));
-            const float fi = flog2(sAl[i]) - (mx + flog2(sum));
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) kset(i, c, CV(c) ? fexp2((fi + G[c]) - crow[CJ(c)] * kappa) : 0.f);
-            if (lane == 0) Fl[i] = fi;
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < C8; ++q) uq[q] = RV(q) ? 1.f : 0.f;
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-      }
-    }
-    // ---- column half-step: v_c = d_c / sum_i u_i Kt_ic -------------------------------
-    // the row scalings reach every lane through LDS (one store per row, two
-    // broadcast 16-byte loads per 8 rows; a wave's LDS accesses run in order)
-#pragma unroll
-    for (int q = 0; q < C8; ++q)
-      if ((lane & 7) == 0) ul[8 * q + (lane >> 3)] = uq[q];
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    float x[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) x[c] = xb[c];
-#pragma unroll
-    for (int q = 0; q < C8; ++q) {
-      const float4 ua = *reinterpret_cast<const float4*>(ul + 8 * q);
-      const float4 ub = *reinterpret_cast<const float4*>(ul + 8 * q + 4);
-      const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
-#pragma unroll
-      for (int r = 0; r < 8; ++r)
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], kget(8 * q + r, c), x[c]);
-    }
-    uint32_t clo = 0xFFFFFFFFu, chi = 0u;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      const float vn = sB[c] * frcp(x[c]);
-      const uint32_t bits = __float_as_uint(vn + xb[c]);
-      clo = bits < clo ? bits : clo;
-      chi = bits > chi ? bits : chi;
-      v[c] = vn;
-    }
-    const bool failc = !(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi));
-    if (__ballot(failc) != 0) {
-      // exact log-domain update of every column, absorbed into G (online LSE)
-      float mx[CPL], sum[CPL];
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) { mx[c] = -INFINITY; sum[c] = 0.f; }
-#pragma unroll
-      for (int i = 0; i < MAXH; ++i) {
-        if (i < nh) {
-          const float fi = Fl[i] + flog2(bcast(uq[i / 8], 8 * (i % 8)));
-          const float* crow = Cb + (int64_t)hidx[i] * R;
-#pragma unroll
-          for (int c = 0; c < CPL; ++c) {
-            if (CV(c)) {
-              const float t = fi - crow[CJ(c)] * kappa;
-              const float m2 = fmaxf(mx[c], t);
-              sum[c] = sum[c] * fexp2(mx[c] - m2) + fexp2(t - m2);
-              mx[c] = m2;
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        G[c] = CV(c) ? flog2(sB[c]) - (mx[c] + flog2(sum[c])) : 0.f;
-        v[c] = CV(c) ? 1.f : 0.f;
-      }
-#pragma unroll
-      for (int i = 0; i < MAXH; ++i) {
-        if (i < nh) {
-          const float Fi = Fl[i];
-          const float* crow = Cb + (int64_t)hidx[i] * R;
-#pragma unroll
-          for (int c = 0; c < CPL; ++c) kset(i, c, CV(c) ? fexp2((Fi + G[c]) - crow[CJ(c)] * kappa) : 0.f);
-        }
-      }
-    }
-  }
-
-  // ---- plan, column cap, outputs -------------------------------------------------
-  const bool colcap = !(p.flags & TAOT_SK_NO_COLCAP);
-  float fac[CPL];
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) fac[c] = 1.f;
-  if (colcap) {
-    float cs[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) cs[c] = 0.f;
-#pragma unroll
-    for (int i = 0; i < MAXH; ++i) {
-      const float ui = bcast(uq[i / 8], 8 * (i % 8));
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) cs[c] += ui * kget(i, c) * v[c];
-    }
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) fac[c] = CV(c) ? fminf(1.f, sB[c] / (cs[c] + 1e-12f)) : 1.f;
-  }
-#pragma unroll
-  for (int q = 0; q < C8; ++q)
-    if ((lane & 7) == 0 && RV(q)) ul[8 * q + (lane >> 3)] = uq[q];
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-  if (p.T) {
-    float* Tb = p.T + pb * R * R;
-    for (int32_t i = 0; i < R; ++i) {
-      const bool hot = hpos[i] >= 0;
-      for (int32_t j = lane; j < R; j += kWave)
-        if (!hot || cpos[j] < 0) Tb[(int64_t)i * R + j] = 0.f;
-    }
-#pragma unroll
-    for (int i = 0; i < MAXH; ++i) {
-      if (i < nh) {
-        const float ui = bcast(uq[i / 8], 8 * (i % 8));
-        float* trow = Tb + (int64_t)hidx[i] * R;
-#pragma unroll
-        for (int c = 0; c < CPL; ++c)
-          if (CV(c)) trow[CJ(c)] = ui * kget(i, c) * (v[c] * fac[c]);
-      }
-    }
-  }
-  const float to_nat = p.eps * kLn2;
-  for (int32_t i = lane; i < R; i += kWave) {
-    const int32_t ih = hpos[i];
-    if (p.f) p.f[pb * R + i] = ih >= 0 ? (Fl[ih] + flog2(ul[ih])) * to_nat : -INFINITY;
-    if (p.g && cpos[i] < 0) p.g[pb * R + i] = -INFINITY;
-  }
-  if (p.g) {
-#pragma unroll
-    for (int c = 0; c < CPL; ++c)
-      if (CV(c)) p.g[pb * R + CJ(c)] = (G[c] + flog2(v[c])) * to_nat;
-  }
-  if (lane == 0 && p.status) p.status[pb] = 0u;
-#undef RV
-#undef CJ
-#undef CV
-}
-
-// Two waves per problem where the row block does not fit one wave's
-// registers (|H| > 48 at CPL = 4): wave w holds rows 32w .. 32w+31 and all of
-// the lane's columns.  Row sums stay within a wave.  Each column half-step
-// adds the two waves' partial sums in a fixed order after an exchange through
-// LDS (one barrier per iteration, buffers alternating by parity), so both
-// waves derive the same v and take the same branches.
-template <int CPL, int C8W>
-__device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
-                                            const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
-                                            const int32_t* hidx, const float* sAl, float* Fl, float* ul,
-                                            float* xbuf, float kappa) {
+                                           float* Gall, float* Sall, float* xbuf, float kappa) {
   constexpr int MW = 8 * C8W;  // rows per wave
-  const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-  const int rb = MW * wv;      // first row of this wave
+  const int lane = threadIdx.x & (kWave - 1);
+  constexpr int wv = WV;  // this wave (a compile-time constant, so per-wave LDS offsets are immediates)
+  constexpr int rb = MW * wv;  // first row of this wave
   const int32_t R = p.R;
   const float* bd = p.b + pb * R;
   const float* Cb = p.C + pb * p.C_stride;
-  float K[MW][CPL];
+  // the column potentials G (log2 units) are only touched by the log-domain
+  // updates: they live in this wave's LDS slice, one value per lane and column
+  float* Gw = Gall + wv * 4 * kWave + lane;
+  // the column demands, read once per iteration: this wave's slice, the
+  // lane's CPL values contiguous
+  float* Sw = Sall + (wv * kWave + lane) * 4;
 #define CV(c) (lane + kWave * (c) < nc)
 #define CJ(c) (CV(c) ? cidx[lane + kWave * (c)] : 0)
 #define RV(q) (rb + 8 * (q) + (lane >> 3) < nh)
-  float sB[CPL], G[CPL], v[CPL], xb[CPL];
+#define GL(c) Gw[(c) * kWave]
+
+  float K[MW][CPL];
+  float v[CPL];
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
-    sB[c] = CV(c) ? bd[CJ(c)] : 0.f;
-    G[c] = 0.f;
+    Sw[c] = CV(c) ? bd[CJ(c)] : 0.f;
     v[c] = CV(c) ? 1.f : 0.f;
-    xb[c] = CV(c) ? 0.f : 1.f;
+    GL(c) = 0.f;
   }
-  float uq[C8W], yb[C8W];
-#pragma unroll
-  for (int q = 0; q < C8W; ++q) {
-    uq[q] = RV(q) ? 1.f : 0.f;
-    yb[q] = RV(q) ? 0.f : 1.f;
-  }
-#pragma unroll
-  for (int i = 0; i < MW; ++i) {
-    const int gi = rb + i;
-    if (gi < nh) {
-      const float Fi = Fl[gi];
-      const float* crow = Cb + (int64_t)hidx[gi] * R;
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2(Fi - crow[CJ(c)] * kappa) : 0.f;
+  // the lane's column demands (padding columns 0)
+  auto demands = [&](float (&sB)[CPL]) {
+    if constexpr (CPL == 4) {
+      const float4 d = *reinterpret_cast<const float4*>(Sw);
+      sB[0] = d.x; sB[1] = d.y; sB[2] = d.z; sB[3] = d.w;
+    } else if constexpr (CPL == 2) {
+      const float2 d = *reinterpret_cast<const float2*>(Sw);
+      sB[0] = d.x; sB[1] = d.y;
     } else {
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) K[i][c] = 0.f;
+      sB[0] = Sw[0];
     }
-  }
+  };
+  // Kt of this wave's rows from the potentials (after the exact log-domain
+  // update of each row's potential when row_update is set:
+  // F_i = log2 s~_i - LSE2_c(G_c + log2 v_c - C'_ic), absorbing u_i).  Each
+  // row's support index is read at an opaque position, so that the row's cost
+  // address is formed here and not kept in registers for the whole iteration
+  // loop.
+  auto build = [&](bool row_update) {
+#pragma unroll
+    for (int i = 0; i < MW; ++i) {
+      const int gi = rb + i;
+      if (gi < nh) {
+        int32_t go = __builtin_amdgcn_readfirstlane(gi);
+        asm volatile("" : "+s"(go));
+        const float* crow = Cb + (int64_t)__builtin_amdgcn_readfirstlane(hidx[go]) * R;
+        float cc[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) cc[c] = CV(c) ? crow[CJ(c)] * kappa : 0.f;
+        float fi;
+        if (row_update) {
+          float t[CPL];
+          float mx = -INFINITY;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            t[c] = CV(c) ? (GL(c) + flog2(v[c])) - cc[c] : -INFINITY;
+            mx = fmaxf(mx, t[c]);
+          }
+          mx = wave_max(mx);
+          float sum = 0.f;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
+          sum = first_lane(wave_sum(sum));
+          fi = flog2(sAl[gi]) - (mx + flog2(sum));
+          if (lane == 0) Fl[gi] = fi;
+        } else {
+          fi = Fl[gi];
+        }
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2((fi + GL(c)) - cc[c]) : 0.f;
+      } else {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) K[i][c] = 0.f;
+      }
+    }
+  };
 
-  for (int32_t it = 1; it <= p.iters; ++it) {
-    if (it > 1) {
-      // ---- row half-step on this wave's rows ----------------------------------------
-      uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+  // The row scalings live in LDS (ul): lane l computes that of row
+  // rb + 8q + (l >> 3) of chunk q, and lanes l = 8k store them.
+#define UST(q, val) \
+  if ((lane & 7) == 0) ul[rb + 8 * (q) + (lane >> 3)] = (val)
+#pragma unroll
+  for (int q = 0; q < C8W; ++q) UST(q, RV(q) ? 1.f : 0.f);
+  // the scaled supply of the lane's row of each chunk, held in registers
+  float sAq[C8W];
+#pragma unroll
+  for (int q = 0; q < C8W; ++q) sAq[q] = sAl[rb + 8 * q + (lane >> 3)];
+
+  // The iterations run in an inner loop that only ever reads Kt.  An
+  // out-of-range scaling leaves it; the log-domain update is then taken and Kt
+  // rebuilt before the iterations resume, so Kt is never live across an update.
+  int32_t it = 1;
+  bool skip_row = true;     // iteration 1 has no row half-step (u follows from v = 1)
+  bool row_update = false;  // this wave's rows take the log-domain update first
+  for (;;) {
+    build(row_update);
+    if (row_update) {
+#pragma unroll
+      for (int q = 0; q < C8W; ++q) UST(q, RV(q) ? 1.f : 0.f);
+      row_update = false;
+    }
+    bool done = false, col_fail = false;
+    for (;;) {
+      if (!skip_row) {
+        // ---- row half-step on this wave's rows: u_i = s~_i / sum_c Kt_ic v_c ---------
+        // padding rows (all-zero Kt) divide by 1 and count as 1 in the range test
+        uint32_t lo = 0xFFFFFFFFu, hi = 0u;  // range of the scalings' bit patterns
+#pragma unroll
+        for (int q = 0; q < C8W; ++q) {
+          float pp[8];
+#pragma unroll
+          for (int r = 0; r < 8; ++r) {
+            float acc = K[8 * q + r][0] * v[0];
+#pragma unroll
+            for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[8 * q + r][c], v[c], acc);
+            pp[r] = acc;
+          }
+          const float y = reduce8(pp, lane);
+          const bool rv = RV(q);
+          const float un = sAq[q] * frcp(rv ? y : 1.f);
+          const uint32_t bits = __float_as_uint(rv ? un : 1.f);
+          lo = bits < lo ? bits : lo;
+          hi = bits > hi ? bits : hi;
+          UST(q, un);
+        }
+        // outside [kLo, kHi], negative, infinite or NaN: this wave's rows are
+        // updated exactly, then the iteration continues with its column half-step
+        const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
+        if (__ballot(fail) != 0) {
+          row_update = true;
+          skip_row = true;
+          break;
+        }
+      }
+      skip_row = false;
+      // ---- column half-step: v_c = d_c / sum_i u_i Kt_ic -------------------------------
+      // this wave's row scalings reach its lanes through LDS (two broadcast
+      // 16-byte loads per 8 rows; a wave's LDS accesses run in order)
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      float x[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) x[c] = 0.f;
+      // the loads of chunk q + 1 are issued before chunk q's FMAs
+      float4 ua = *reinterpret_cast<const float4*>(ul + rb);
+      float4 ub = *reinterpret_cast<const float4*>(ul + rb + 4);
 #pragma unroll
       for (int q = 0; q < C8W; ++q) {
-        float pp[8];
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          float acc = K[8 * q + r][0] * v[0];
-#pragma unroll
-          for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[8 * q + r][c], v[c], acc);
-          pp[r] = acc;
+        float4 na = ua, nb = ub;
+        if (q + 1 < C8W) {
+          na = *reinterpret_cast<const float4*>(ul + rb + 8 * (q + 1));
+          nb = *reinterpret_cast<const float4*>(ul + rb + 8 * (q + 1) + 4);
         }
-        const float y = reduce8(pp, lane);
-        const float un = sAl[rb + 8 * q + (lane >> 3)] * frcp(y + yb[q]);
-        const uint32_t bits = __float_as_uint(un + yb[q]);
-        lo = bits < lo ? bits : lo;
-        hi = bits > hi ? bits : hi;
-        uq[q] = un;
+        const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], K[8 * q + r][c], x[c]);
+        ua = na;
+        ub = nb;
       }
-      const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
-      if (__ballot(fail) != 0) {
-        // exact log-domain update of this wave's rows, absorbed into F
+      if constexpr (NW > 1) {
+        float* xs = xbuf + (size_t)((it & 1) * NW + wv) * CPL * kWave;
 #pragma unroll
-        for (int i = 0; i < MW; ++i) {
-          const int gi = rb + i;
-          if (gi < nh) {
-            const float* crow = Cb + (int64_t)hidx[gi] * R;
-            float t[CPL];
-            float mx = -INFINITY;
+        for (int c = 0; c < CPL; ++c) xs[c * kWave + lane] = x[c];
+        psync<NW>();
+        const float* x0 = xbuf + (size_t)(it & 1) * NW * CPL * kWave;
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-              t[c] = CV(c) ? (G[c] + flog2(v[c])) - crow[CJ(c)] * kappa : -INFINITY;
-              mx = fmaxf(mx, t[c]);
-            }
-            mx = wave_max(mx);
-            float sum = 0.f;
+        for (int c = 0; c < CPL; ++c) {
+          float sx = x0[c * kWave + lane];
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
-            sum = first_lane(wave_sum(sum));
-            const float fi = flog2(sAl[gi]) - (mx + flog2(sum));
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2((fi + G[c]) - crow[CJ(c)] * kappa) : 0.f;
-            if (lane == 0) Fl[gi] = fi;
-          }
+          for (int w = 1; w < NW; ++w) sx = sx + x0[(w * CPL + c) * kWave + lane];
+          x[c] = sx;
         }
-#pragma unroll
-        for (int q = 0; q < C8W; ++q) uq[q] = RV(q) ? 1.f : 0.f;
       }
+      // padding columns (all-zero Kt) divide by 1 and count as 1 in the range test
+      float sB[CPL];
+      demands(sB);
+      uint32_t clo = 0xFFFFFFFFu, chi = 0u;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const float vn = sB[c] * frcp(CV(c) ? x[c] : 1.f);
+        const uint32_t bits = __float_as_uint(CV(c) ? vn : 1.f);
+        clo = bits < clo ? bits : clo;
+        chi = bits > chi ? bits : chi;
+        v[c] = vn;
+      }
+      // the same decision on every wave
+      col_fail = __ballot(!(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi))) != 0;
+      done = it == p.iters;
+      if (!done) ++it;
+      if (col_fail || done) break;
     }
-    // ---- column half-step: partial sums of both waves, added in wave order ------------
-    // row scalings to every lane through this wave's part of ul (as in wave_solve)
-#pragma unroll
-    for (int q = 0; q < C8W; ++q)
-      if ((lane & 7) == 0) ul[rb + 8 * q + (lane >> 3)] = uq[q];
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    float x[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) x[c] = wv == 0 ? xb[c] : 0.f;
-#pragma unroll
-    for (int q = 0; q < C8W; ++q) {
-      const float4 ua = *reinterpret_cast<const float4*>(ul + rb + 8 * q);
-      const float4 ub = *reinterpret_cast<const float4*>(ul + rb + 8 * q + 4);
-      const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
-#pragma unroll
-      for (int r = 0; r < 8; ++r)
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], K[8 * q + r][c], x[c]);
-    }
-    float* xs = xbuf + (size_t)((it & 1) * 2 + wv) * CPL * kWave;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) xs[c * kWave + lane] = x[c];
-    __syncthreads();
-    const float* x0 = xbuf + (size_t)((it & 1) * 2) * CPL * kWave;
-    const float* x1 = x0 + CPL * kWave;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) x[c] = x0[c * kWave + lane] + x1[c * kWave + lane];
-    uint32_t clo = 0xFFFFFFFFu, chi = 0u;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      const float vn = sB[c] * frcp(x[c]);
-      const uint32_t bits = __float_as_uint(vn + xb[c]);
-      clo = bits < clo ? bits : clo;
-      chi = bits > chi ? bits : chi;
-      v[c] = vn;
-    }
-    const bool failc = !(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi));
-    if (__ballot(failc) != 0) {  // the same decision on both waves
+    if (col_fail) {
       // exact log-domain update of every column, absorbed into G (online LSE
-      // over all rows: each wave publishes its row scalings first)
-#pragma unroll
-      for (int q = 0; q < C8W; ++q)
-        if ((lane & 7) == 0 && RV(q)) ul[rb + 8 * q + (lane >> 3)] = uq[q];
-      __syncthreads();
+      // over all rows, whose scalings every wave has stored in ul); Kt is
+      // rebuilt at the top of the loop, or below after the last iteration
+      psync<NW>();
       float mx[CPL], sum[CPL];
 #pragma unroll
       for (int c = 0; c < CPL; ++c) { mx[c] = -INFINITY; sum[c] = 0.f; }
@@ -757,26 +660,25 @@ __device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32
           }
         }
       }
+      float sB[CPL];
+      demands(sB);
 #pragma unroll
       for (int c = 0; c < CPL; ++c) {
-        G[c] = CV(c) ? flog2(sB[c]) - (mx[c] + flog2(sum[c])) : 0.f;
+        GL(c) = CV(c) ? flog2(sB[c]) - (mx[c] + flog2(sum[c])) : 0.f;
         v[c] = CV(c) ? 1.f : 0.f;
       }
-#pragma unroll
-      for (int i = 0; i < MW; ++i) {
-        const int gi = rb + i;
-        if (gi < nh) {
-          const float Fi = Fl[gi];
-          const float* crow = Cb + (int64_t)hidx[gi] * R;
-#pragma unroll
-          for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2((Fi + G[c]) - crow[CJ(c)] * kappa) : 0.f;
-        }
+      psync<NW>();  // every wave has read ul and F
+      if (done) {
+        build(false);
+        break;
       }
-      __syncthreads();  // both waves have read ul
+      continue;
     }
+    if (done) break;
   }
 
   // ---- plan, column cap, outputs -------------------------------------------------
+  psync<NW>();  // the row scalings of every wave are in ul
   const bool colcap = !(p.flags & TAOT_SK_NO_COLCAP);
   float fac[CPL];
 #pragma unroll
@@ -787,28 +689,33 @@ __device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32
     for (int c = 0; c < CPL; ++c) cs[c] = 0.f;
 #pragma unroll
     for (int i = 0; i < MW; ++i) {
-      const float ui = bcast(uq[i / 8], 8 * (i % 8));
+      const float ui = ul[rb + i];
 #pragma unroll
       for (int c = 0; c < CPL; ++c) cs[c] += ui * K[i][c] * v[c];
     }
-    // the iteration loop's last exchange used parity iters & 1
-    float* xs = xbuf + (size_t)(((p.iters + 1) & 1) * 2 + wv) * CPL * kWave;
+    if constexpr (NW > 1) {
+      // the iteration loop's last exchange used parity iters & 1
+      float* xs = xbuf + (size_t)(((p.iters + 1) & 1) * NW + wv) * CPL * kWave;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) xs[c * kWave + lane] = cs[c];
-    __syncthreads();
-    const float* c0 = xbuf + (size_t)(((p.iters + 1) & 1) * 2) * CPL * kWave;
-    const float* c1 = c0 + CPL * kWave;
+      for (int c = 0; c < CPL; ++c) xs[c * kWave + lane] = cs[c];
+      psync<NW>();
+      const float* c0 = xbuf + (size_t)((p.iters + 1) & 1) * NW * CPL * kWave;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c)
-      fac[c] = CV(c) ? fminf(1.f, sB[c] / ((c0[c * kWave + lane] + c1[c * kWave + lane]) + 1e-12f)) : 1.f;
+      for (int c = 0; c < CPL; ++c) {
+        float s = c0[c * kWave + lane];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) s = s + c0[(w * CPL + c) * kWave + lane];
+        cs[c] = s;
+      }
+    }
+    float sB[CPL];
+    demands(sB);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) fac[c] = CV(c) ? fminf(1.f, sB[c] / (cs[c] + 1e-12f)) : 1.f;
   }
-#pragma unroll
-  for (int q = 0; q < C8W; ++q)
-    if ((lane & 7) == 0 && RV(q)) ul[rb + 8 * q + (lane >> 3)] = uq[q];
-  __syncthreads();
   if (p.T) {
     float* Tb = p.T + pb * R * R;
-    for (int32_t i = wv; i < R; i += 2) {
+    for (int32_t i = wv; i < R; i += NW) {
       const bool hot = hpos[i] >= 0;
       for (int32_t j = lane; j < R; j += kWave)
         if (!hot || cpos[j] < 0) Tb[(int64_t)i * R + j] = 0.f;
@@ -817,7 +724,7 @@ __device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32
     for (int i = 0; i < MW; ++i) {
       const int gi = rb + i;
       if (gi < nh) {
-        const float ui = bcast(uq[i / 8], 8 * (i % 8));
+        const float ui = ul[gi];
         float* trow = Tb + (int64_t)hidx[gi] * R;
 #pragma unroll
         for (int c = 0; c < CPL; ++c)
@@ -835,54 +742,70 @@ __device__ __forceinline__ void wave2_solve(const SkParams& p, int64_t pb, int32
     if (p.g) {
 #pragma unroll
       for (int c = 0; c < CPL; ++c)
-        if (CV(c)) p.g[pb * R + CJ(c)] = (G[c] + flog2(v[c])) * to_nat;
+        if (CV(c)) p.g[pb * R + CJ(c)] = (GL(c) + flog2(v[c])) * to_nat;
     }
     if (lane == 0 && p.status) p.status[pb] = 0u;
   }
+#undef UST
+#undef GL
 #undef RV
 #undef CJ
 #undef CV
 }
 
-// LDS of the wave kernels: sA, F, u [64] floats, for the two-wave solver the
-// column exchange [2 parities][2 waves][4][64] floats, then cpos, hpos [R] +
-// cidx [256] + hidx [64] ints.
-__host__ __device__ constexpr size_t wave_lds_bytes(int32_t R, bool two) {
-  return (size_t)(2 * R + 256 + 64) * 4 + 3 * 64 * 4 + (two ? (size_t)2 * 2 * 4 * kWave * 4 : 0);
-}
-__host__ __device__ constexpr bool two_wave_class(int cls) {
-  return cls == wave_class(4, 7) || cls == wave_class(4, 8);
+// The solver instance of wave wv (uniform over the wave).
+template <int CPL, int C8W, int NW>
+__device__ __forceinline__ void solve_on_wave(int wv, const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
+                                              const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
+                                              const int32_t* hidx, const float* sAl, float* Fl, float* ul,
+                                              float* Gall, float* Sall, float* xbuf, float kappa) {
+  if constexpr (NW == 1) {
+    wave_solve<CPL, C8W, 1, 0>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa);
+  } else if constexpr (NW == 2) {
+    if (wv == 0) wave_solve<CPL, C8W, 2, 0>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa);
+    else wave_solve<CPL, C8W, 2, 1>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa);
+  } else {
+    switch (wv) {
+      case 0: wave_solve<CPL, C8W, 4, 0>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa); break;
+      case 1: wave_solve<CPL, C8W, 4, 1>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa); break;
+      case 2: wave_solve<CPL, C8W, 4, 2>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa); break;
+      default: wave_solve<CPL, C8W, 4, 3>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, kappa); break;
+    }
+  }
 }
 
-// Problem pb on one wave (TWO = false: the row block fits one wave's
-// registers) or on a two-wave workgroup (TWO = true: the rest of the register
-// classes); returns at once for the other kind.  Uniform over the workgroup.
-template <bool TWO>
+// One problem on NW waves (NW = 1: this wave alone, beside other one-wave
+// problems of the workgroup; NW = W: the whole workgroup of the W-wave kernel).
+template <int NW, int W>
 __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int32_t* wl) {
   const int lane = threadIdx.x & (kWave - 1);
+  const int wv = NW == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform
+  const int gt = NW == 1 ? lane : (int)threadIdx.x;  // thread index within the problem's waves
   const int32_t R = p.R;
   // float arrays first: ul is read 16 bytes at a time
   float* sAl = reinterpret_cast<float*>(wl);  // [64] scaled supply
-  float* Fl = sAl + 64;            // [64] absorbed row potentials (log2 units)
-  float* ul = Fl + 64;             // [64] row scalings (broadcast, final, exchanges)
-  float* xbuf = ul + 64;           // [2][2][4][64] column partial sums (TWO only)
-  int32_t* cpos = reinterpret_cast<int32_t*>(TWO ? xbuf + 2 * 2 * 4 * kWave : xbuf);  // [R] compact column, -1 if not cold
-  int32_t* hpos = cpos + R;        // [R] compact row of rank i, -1 if not hot
-  int32_t* cidx = hpos + R;        // [256]
-  int32_t* hidx = cidx + 256;      // [64]
+  float* Fl = sAl + 64;                       // [64] absorbed row potentials (log2 units)
+  float* ul = Fl + 64;                        // [64] row scalings
+  float* Gall = ul + 64;                      // [NW][4][64] column potentials
+  float* Sall = Gall + NW * 4 * kWave;        // [NW][64][4] column demands
+  float* xbuf = Sall + NW * 4 * kWave;        // [2][NW][4][64] column exchange (NW > 1)
+  int32_t* iw = reinterpret_cast<int32_t*>(reinterpret_cast<float*>(wl) + wave_lds_floats(NW));
+  int32_t* flag = iw;            // [4]: bad cost entry seen
+  int32_t* cpos = iw + 4;        // [R] compact column, -1 if not cold
+  int32_t* hpos = cpos + R;      // [R] compact row of rank i, -1 if not hot
+  int32_t* cidx = hpos + R;      // [256]
+  int32_t* hidx = cidx + 256;    // [64]
   const float* a = p.a + pb * R;
   const float* bd = p.b + pb * R;
   const float* Cb = p.C + pb * p.C_stride;
 
-  // ---- supports, validation, mass -------------------------------------------
+  // ---- supports and mass (every wave, identical results) --------------------
   double sa = 0.0, sd = 0.0;
-  bool bad = false;
   int32_t nh = 0, nc = 0;
   for (int32_t base = 0; base < R; base += kWave) {
     const int32_t i = base + lane;
     const bool in = i < R;
     const float ai = in ? a[i] : 0.f, bi = in ? bd[i] : 0.f;
-    bad |= !(ai >= 0.f && ai <= 3.402823466e38f) || !(bi >= 0.f && bi <= 3.402823466e38f);
     sa += (double)ai;
     sd += (double)bi;
     const uint64_t hm = __ballot(in && ai > 0.f), cm = __ballot(in && bi > 0.f);
@@ -897,19 +820,19 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
     nh += __popcll(hm);
     nc += __popcll(cm);
   }
-  const int cls = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
-  if (cls == 0 || two_wave_class(cls) != TWO) return;  // uniform: another kernel owns this problem
   sa = wave_sum_d(sa);
   sd = wave_sum_d(sd);
   double gamma = __shfl(sd, 0, kWave) / fmax(__shfl(sa, 0, kWave), kEps0);
   gamma = gamma < 1.0 ? gamma : 1.0;
   sAl[lane] = lane < nh ? (float)(gamma * (double)a[hidx[lane]]) : 0.f;  // zero padding to 64 rows
-  __syncthreads();
+  if (gt == 0) flag[0] = 0;
+  psync<NW>();
   const float kappa = kLog2e / p.eps;
 
-  // ---- first row update over all R columns (v = 1): F_i = log2 s~_i - LSE2_j(-C'_ij)
+  // ---- first row update over all R columns (v = 1): F_i = log2 s~_i - LSE2_j(-C'_ij),
+  // rows dealt out over the waves
   bool badc = false;
-  for (int32_t i = 0; i < nh; ++i) {
+  for (int32_t i = wv; i < nh; i += NW) {
     const float* crow = Cb + (int64_t)hidx[i] * R;
     float mx = -INFINITY;
     for (int32_t j = lane; j < R; j += kWave) {
@@ -923,59 +846,60 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
     sum = first_lane(wave_sum(sum));
     if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
   }
-  if (__ballot(badc) != 0) {
+  if (__ballot(badc) != 0 && lane == 0) flag[0] = 1;
+  psync<NW>();
+  if (flag[0] != 0) {
     if (p.T)
-      for (int64_t q = lane; q < (int64_t)R * R; q += kWave) p.T[pb * R * R + q] = 0.f;
-    for (int32_t i = lane; i < R; i += kWave) {
+      for (int64_t q = gt; q < (int64_t)R * R; q += NW * kWave) p.T[pb * R * R + q] = 0.f;
+    for (int32_t i = gt; i < R; i += NW * kWave) {
       if (p.f) p.f[pb * R + i] = -INFINITY;
       if (p.g) p.g[pb * R + i] = -INFINITY;
     }
-    if (lane == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
+    if (gt == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
     return;
   }
-  __syncthreads();
-  if constexpr (TWO) {
-    wave2_solve<4, 4>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, xbuf, kappa);
-    return;
-  } else {
-  switch (cls) {
-#define TAOT_WAVE_CASE(CPL_, C8_)                                                                      \
-  case wave_class(CPL_, C8_):                                                                          \
-    wave_solve<CPL_, C8_>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, kappa);                   \
+  const int cpl = nc <= 64 ? 1 : nc <= 128 ? 2 : 4;
+  const int c8w = ((nh + 7) / 8 + NW - 1) / NW;
+  switch (cpl * 16 + c8w) {
+#define TAOT_WAVE_CASE(CPL_, C8W_)                                                                    \
+  case CPL_ * 16 + C8W_:                                                                              \
+    if constexpr (shape_ok(W, NW, CPL_, C8W_))                                                        \
+      solve_on_wave<CPL_, C8W_, NW>(wv, p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, xbuf, \
+                                    kappa);                                                           \
     break;
-#define TAOT_WAVE_CPL(CPL_)                                                                            \
+#define TAOT_WAVE_CPL(CPL_)                                                                           \
   TAOT_WAVE_CASE(CPL_, 1) TAOT_WAVE_CASE(CPL_, 2) TAOT_WAVE_CASE(CPL_, 3) TAOT_WAVE_CASE(CPL_, 4)      \
   TAOT_WAVE_CASE(CPL_, 5) TAOT_WAVE_CASE(CPL_, 6) TAOT_WAVE_CASE(CPL_, 7) TAOT_WAVE_CASE(CPL_, 8)
-    TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2)
-    TAOT_WAVE_CASE(4, 1) TAOT_WAVE_CASE(4, 2) TAOT_WAVE_CASE(4, 3) TAOT_WAVE_CASE(4, 4)
-    TAOT_WAVE_CASE(4, 5) TAOT_WAVE_CASE(4, 6)
+    TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2) TAOT_WAVE_CPL(4)
 #undef TAOT_WAVE_CPL
 #undef TAOT_WAVE_CASE
     default: break;
   }
-  }
 }
 
-__global__ void __launch_bounds__(kWave, 2)
-sinkhorn_wave_kernel(SkParams p, const int32_t* __restrict__ ord, const int32_t* __restrict__ count) {
+// LDS of one wave of a single item, rounded to 16 bytes.
+__host__ __device__ constexpr size_t single_lds_bytes(int32_t R) { return (wave_lds_bytes(R, 1) + 15) / 16 * 16; }
+
+// The register problems of a batch on workgroups of W waves: item k < n_multi
+// is multi[k] on all W waves; item n_multi + g holds single[W g + w] on wave
+// w, each wave with its own LDS slice.
+template <int W>
+__global__ void __launch_bounds__(W * kWave, W == 4 ? 4 : 2)
+sinkhorn_reg_kernel(SkParams p, const int32_t* __restrict__ multi, const int32_t* __restrict__ single,
+                    const int32_t* __restrict__ counts) {
   extern __shared__ __attribute__((aligned(16))) int32_t wl[];
-  if ((int32_t)blockIdx.x >= *count) return;
-  wave_problem<false>(p, ord[blockIdx.x], wl);
-}
-
-// The listed two-wave problems, a small grid walking the list.
-__global__ void __launch_bounds__(2 * kWave, 2)
-sinkhorn_wave2_kernel(SkParams p, const int32_t* __restrict__ list, const int32_t* __restrict__ count) {
-  extern __shared__ __attribute__((aligned(16))) int32_t wl[];
-  const int32_t n = *count;
-  for (int32_t k = blockIdx.x; k < n; k += gridDim.x) {
-    wave_problem<true>(p, list[k], wl);
-    __syncthreads();  // LDS is reused by the next problem
+  const int32_t n_multi = counts[0], n_single = counts[1];
+  const int32_t k = blockIdx.x;
+  if (k < n_multi) {
+    wave_problem<W, W>(p, multi[k], wl);
+    return;
   }
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t j = (int64_t)(k - n_multi) * W + w;
+  if (j < n_single) wave_problem<1, W>(p, single[j], wl + (size_t)w * (single_lds_bytes(p.R) / 4));
 }
 
-// Register class of every problem (0: not a register problem), with the same
-// support scan and tests as wave_problem.
+// Register class of every problem (0: not a register problem).
 __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* __restrict__ cls) {
   const int lane = threadIdx.x;
   const int64_t pb = blockIdx.x;
@@ -996,100 +920,81 @@ __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* 
   if (lane == 0) cls[pb] = c;
 }
 
-// Per-iteration work of a register class: rows (8 C8) x columns per lane.
-__device__ __forceinline__ int32_t class_work(int32_t cls) {
-  const int32_t c8 = (cls - 1) % 8 + 1, ci = (cls - 1) / 8;
-  return c8 * (ci == 0 ? 1 : ci == 1 ? 2 : 4);
-}
-
-// Launch orders (one block): the two-wave problems ascending, and the
-// one-wave problems by descending work (ascending index within equal work),
-// so that workgroups dealt out in order mix heavy and light problems on every
-// compute unit.
-__global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* __restrict__ cls, int32_t B,
-                                                                int32_t* __restrict__ list2,
-                                                                int32_t* __restrict__ count2,
-                                                                int32_t* __restrict__ ord1,
-                                                                int32_t* __restrict__ count1) {
+// Multi and single lists of the W-wave kernel (one block), each by descending
+// per-wave work (ascending index within equal work), so that the workgroups
+// dealt out in order start with the heaviest and mix heavy and light work on
+// every compute unit; single groups join problems of similar work.
+__global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* __restrict__ cls, int32_t B, int32_t W,
+                                                                int32_t* __restrict__ multi,
+                                                                int32_t* __restrict__ single,
+                                                                int32_t* __restrict__ counts) {
   __shared__ int32_t wave_cnt[kSkWaves];
-  __shared__ unsigned long long present;  // bit w: some one-wave problem has work w
-  if (threadIdx.x == 0) present = 0ull;
+  __shared__ unsigned long long present[2];  // multi / single: bit w if some problem has per-wave work w
+  if (threadIdx.x == 0) present[0] = present[1] = 0ull;
   __syncthreads();
   for (int32_t b = threadIdx.x; b < B; b += kSkThreads) {
     const int32_t c = cls[b];
-    if (c != 0 && !two_wave_class(c)) atomicOr(&present, 1ull << class_work(c));
+    if (c == 0) continue;
+    const int cpl = class_cpl(c), c8 = class_c8(c);
+    atomicOr(&present[is_single(W, cpl, c8) ? 1 : 0], 1ull << (c8_per_wave(W, cpl, c8) * cpl));
   }
   __syncthreads();
-  const unsigned long long works = present;
-  int32_t n = 0;
-  for (int32_t base = 0; base < B; base += kSkThreads) {
-    const int32_t b = base + (int32_t)threadIdx.x;
-    const bool f = b < B && two_wave_class(cls[b]);
-    int32_t tot;
-    const int32_t pos = chunk_compact(f, wave_cnt, tot);
-    if (f) list2[n + pos] = b;
-    n += tot;
-  }
-  if (threadIdx.x == 0) *count2 = n;
-  n = 0;
-  for (int32_t wk = 63; wk > 0; --wk) {
-    if (!((works >> wk) & 1ull)) continue;
-    for (int32_t base = 0; base < B; base += kSkThreads) {
-      const int32_t b = base + (int32_t)threadIdx.x;
-      const int32_t c = b < B ? cls[b] : 0;
-      const bool f = c != 0 && !two_wave_class(c) && class_work(c) == wk;
-      int32_t tot;
-      const int32_t pos = chunk_compact(f, wave_cnt, tot);
-      if (f) ord1[n + pos] = b;
-      n += tot;
+  for (int k = 0; k < 2; ++k) {
+    const unsigned long long works = present[k];
+    int32_t* list = k == 0 ? multi : single;
+    int32_t n = 0;
+    for (int32_t wk = 63; wk > 0; --wk) {
+      if (!((works >> wk) & 1ull)) continue;
+      for (int32_t base = 0; base < B; base += kSkThreads) {
+        const int32_t b = base + (int32_t)threadIdx.x;
+        const int32_t c = b < B ? cls[b] : 0;
+        bool f = false;
+        if (c != 0) {
+          const int cpl = class_cpl(c), c8 = class_c8(c);
+          f = (is_single(W, cpl, c8) ? 1 : 0) == k && c8_per_wave(W, cpl, c8) * cpl == wk;
+        }
+        int32_t tot;
+        const int32_t pos = chunk_compact(f, wave_cnt, tot);
+        if (f) list[n + pos] = b;
+        n += tot;
+      }
     }
+    if (threadIdx.x == 0) counts[k] = n;
   }
-  if (threadIdx.x == 0) *count1 = n;
 }
 
-// A stream beside the caller's, so that the one- and two-wave kernels run
-// concurrently: created once per device and kept for the life of the
-// process, at the default priority.
-struct SideStream {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-};
-constexpr int kMaxDevices = 64;
-constexpr int kTwoWaveGrid = 64;  // workgroups of the two-wave kernel
-std::mutex g_side_mutex;
-SideStream g_side[kMaxDevices];
+template <int W>
+taot_status launch_reg_kernel(const SkParams& p, const int32_t* multi, const int32_t* single, const int32_t* counts,
+                              hipStream_t stream) {
+  const size_t lds = std::max(wave_lds_bytes(p.R, W), (size_t)W * single_lds_bytes(p.R));
+  if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_reg_kernel<W>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return TAOT_ERR_LAUNCH;
+  // one workgroup per item at most: B is an upper bound on the items
+  hipLaunchKernelGGL(sinkhorn_reg_kernel<W>, dim3((unsigned)p.B), dim3(W * kWave), lds, stream, p, multi, single,
+                     counts);
+  return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
+}
 
-// The register path: classes and the two-wave list on the caller's stream;
-// then the two-wave kernel (a small grid, launched first so that its
-// workgroups find room) on the caller's stream, beside the one-wave kernel on
-// the side stream; the caller's stream waits for both.
-taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* list, int32_t* count, int32_t* ord,
-                        int32_t* count1, hipStream_t stream) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TAOT_ERR_LAUNCH;
+// The register path on the caller's stream: classes, lists, then one
+// register kernel.  W = 4 when every problem can hold four 128-VGPR waves at
+// once (four SIMDs per compute unit, four such waves per SIMD), else 2
+// (TAOT_SK_WAVES_1 forces W = 2, i.e. one wave per problem where it fits).
+taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* lists, int32_t* counts, hipStream_t stream) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return TAOT_ERR_LAUNCH;
+  const int64_t cap = (int64_t)cus * 4 * 4;
+  const int W = (4 * (int64_t)p.B <= cap && !(p.flags & TAOT_SK_WAVES_1)) ? 4 : 2;
   hipLaunchKernelGGL(wave_class_kernel, dim3((unsigned)p.B), dim3(kWave), 0, stream, p, cls);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(wave_order_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, list, count, ord, count1);
+  int32_t* multi = lists;
+  int32_t* single = lists + p.B;
+  hipLaunchKernelGGL(wave_order_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, W, multi, single, counts);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  std::lock_guard<std::mutex> lock(g_side_mutex);
-  SideStream& sd = g_side[dev];
-  if (sd.s == nullptr) {
-    if (hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking) != hipSuccess ||
-        hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&sd.join, hipEventDisableTiming) != hipSuccess)
-      return TAOT_ERR_LAUNCH;
-  }
-  if (hipEventRecord(sd.fork, stream) != hipSuccess) return TAOT_ERR_LAUNCH;
-  const unsigned grid2 = (unsigned)(p.B < kTwoWaveGrid ? p.B : kTwoWaveGrid);
-  hipLaunchKernelGGL(sinkhorn_wave2_kernel, dim3(grid2), dim3(2 * kWave), wave_lds_bytes(p.R, true), stream, p,
-                     list, count);
-  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  if (hipStreamWaitEvent(sd.s, sd.fork, 0) != hipSuccess) return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(sinkhorn_wave_kernel, dim3((unsigned)p.B), dim3(kWave), wave_lds_bytes(p.R, false), sd.s, p,
-                     ord, count1);
-  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  if (hipEventRecord(sd.join, sd.s) != hipSuccess) return TAOT_ERR_LAUNCH;
-  return hipStreamWaitEvent(stream, sd.join, 0) == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
+  return W == 4 ? launch_reg_kernel<4>(p, multi, single, counts, stream)
+                : launch_reg_kernel<2>(p, multi, single, counts, stream);
 }
 
 // Largest nh * nc over disjoint supports of R ranks (nh + nc <= R).
@@ -1097,11 +1002,9 @@ int64_t max_block(int32_t R) { return (int64_t)(R / 2) * (R - R / 2); }
 
 struct SkWs {
   int32_t* flag;
-  int32_t* cls;    // [B] register class
-  int32_t* list;   // [B] two-wave problems
-  int32_t* count;  // [1]
-  int32_t* ord;    // [B] one-wave problems by descending work
-  int32_t* count1; // [1]
+  int32_t* cls;     // [B] register class
+  int32_t* lists;   // [2][B] register problems: multi, single
+  int32_t* counts;  // [2]
   float* kt;
   int64_t kt_stride;
   size_t bytes;
@@ -1112,10 +1015,8 @@ SkWs carve(void* ws, int32_t B, int32_t R) {
   SkWs w;
   w.flag = c.take<int32_t>((size_t)B);
   w.cls = c.take<int32_t>((size_t)B);
-  w.list = c.take<int32_t>((size_t)B);
-  w.count = c.take<int32_t>(1);
-  w.ord = c.take<int32_t>((size_t)B);
-  w.count1 = c.take<int32_t>(1);
+  w.lists = c.take<int32_t>((size_t)2 * B);
+  w.counts = c.take<int32_t>(2);
   w.kt_stride = round_up((int64_t)R * R, 64);
   w.kt = c.take<float>((size_t)B * w.kt_stride);
   w.bytes = c.off;
@@ -1135,7 +1036,7 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
   if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {
-    const taot_status st = launch_wave(p, w.cls, w.list, w.count, w.ord, w.count1, stream);
+    const taot_status st = launch_wave(p, w.cls, w.lists, w.counts, stream);
     if (st != TAOT_OK) return st;
   }
   if (lds_path) {

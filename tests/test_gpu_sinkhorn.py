@@ -189,3 +189,29 @@ def test_two_wave_rows(nh, nc, gpu):
     for eps, iters in ((0.5, 3), (0.08, 200), (0.02, 120)):
         print(f"[sinkhorn parity] two-wave nh={nh} nc={nc} eps={eps}", flush=True)
         _check_against_oracle(a, b, C, eps, iters)
+
+
+@pytest.mark.parametrize("flags", [0, taot.SK_WAVES_1])
+def test_register_shapes(flags, gpu):
+    """One problem of every register class (1, 2 or 4 columns per lane x 1..8
+    chunks of 8 hot ranks) in one batch.  By default a small batch spreads
+    each problem over up to four waves (one-chunk problems share a workgroup,
+    one wave each); SK_WAVES_1 takes the shapes of large batches (one wave per
+    problem where its rows fit, else two).  Small eps drives the scalings out
+    of range, so the log-domain updates run too."""
+    rng = np.random.default_rng(7 + flags)
+    R = 320
+    shapes = [(nh, nc) for lo, hi in ((1, 64), (65, 128), (129, 256))
+              for c8 in range(1, 9)
+              for nh, nc in [(8 * c8 - int(rng.integers(0, 8)), int(rng.integers(lo, hi + 1)))]]
+    B = len(shapes)
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p, (nh, nc) in enumerate(shapes):
+        perm = rng.permutation(R)
+        a[p, perm[:nh]] = rng.integers(1, 4000, size=nh)
+        b[p, perm[nh:nh + nc]] = rng.multinomial(int(a[p].sum()), np.full(nc, 1.0 / nc)) + 1
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32))
+    for eps, iters in ((0.5, 3), (0.08, 200), (0.02, 120)):
+        print(f"[sinkhorn parity] register shapes flags={flags} eps={eps}", flush=True)
+        _check_against_oracle(a, b, C, eps, iters, flags)
