@@ -554,24 +554,30 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
         // ---- row half-step on this wave's rows: u_i = s~_i / sum_c Kt_ic v_c ---------
         // padding rows (all-zero Kt) divide by 1 and count as 1 in the range test
         uint32_t lo = 0xFFFFFFFFu, hi = 0u;  // range of the scalings' bit patterns
+#define TAOT_ROW_SUMS(q, pp)                                                                          \
+  _Pragma("unroll") for (int r = 0; r < 8; ++r) {                                                     \
+    float acc = K[8 * (q) + r][0] * v[0];                                                             \
+    _Pragma("unroll") for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[8 * (q) + r][c], v[c], acc); \
+    pp[r] = acc;                                                                                      \
+  }
+#define TAOT_ROW_FINISH(q, y)                                                                         \
+  {                                                                                                   \
+    const bool rv = RV(q);                                                                            \
+    const float un = sAq[q] * frcp(rv ? (y) : 1.f);                                                   \
+    const uint32_t bits = __float_as_uint(rv ? un : 1.f);                                             \
+    lo = bits < lo ? bits : lo;                                                                       \
+    hi = bits > hi ? bits : hi;                                                                       \
+    UST(q, un);                                                                                       \
+  }
 #pragma unroll
         for (int q = 0; q < C8W; ++q) {
           float pp[8];
-#pragma unroll
-          for (int r = 0; r < 8; ++r) {
-            float acc = K[8 * q + r][0] * v[0];
-#pragma unroll
-            for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[8 * q + r][c], v[c], acc);
-            pp[r] = acc;
-          }
-          const float y = reduce8(pp, lane);
-          const bool rv = RV(q);
-          const float un = sAq[q] * frcp(rv ? y : 1.f);
-          const uint32_t bits = __float_as_uint(rv ? un : 1.f);
-          lo = bits < lo ? bits : lo;
-          hi = bits > hi ? bits : hi;
-          UST(q, un);
+          TAOT_ROW_SUMS(q, pp)
+          const float y = reduce8(pp, lane);  // all lanes take part
+          TAOT_ROW_FINISH(q, y)
         }
+#undef TAOT_ROW_FINISH
+#undef TAOT_ROW_SUMS
         // outside [kLo, kHi], negative, infinite or NaN: this wave's rows are
         // updated exactly, then the iteration continues with its column half-step
         const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
@@ -586,9 +592,11 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
       // this wave's row scalings reach its lanes through LDS (two broadcast
       // 16-byte loads per 8 rows; a wave's LDS accesses run in order)
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      float x[CPL];
+      // two partial sums per column (even and odd rows of each chunk), so
+      // that 2 CPL independent FMA chains interleave
+      float x[CPL], x2[CPL];
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) x[c] = 0.f;
+      for (int c = 0; c < CPL; ++c) x[c] = x2[c] = 0.f;
       // the loads of chunk q + 1 are issued before chunk q's FMAs
       float4 ua = *reinterpret_cast<const float4*>(ul + rb);
       float4 ub = *reinterpret_cast<const float4*>(ul + rb + 4);
@@ -601,12 +609,17 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
         }
         const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
 #pragma unroll
-        for (int r = 0; r < 8; ++r)
+        for (int r = 0; r < 8; r += 2)
 #pragma unroll
-          for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], K[8 * q + r][c], x[c]);
+          for (int c = 0; c < CPL; ++c) {
+            x[c] = __builtin_fmaf(us[r], K[8 * q + r][c], x[c]);
+            x2[c] = __builtin_fmaf(us[r + 1], K[8 * q + r + 1][c], x2[c]);
+          }
         ua = na;
         ub = nb;
       }
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) x[c] = x[c] + x2[c];
       if constexpr (NW > 1) {
         float* xs = xbuf + (size_t)((it & 1) * NW + wv) * CPL * kWave;
 #pragma unroll
