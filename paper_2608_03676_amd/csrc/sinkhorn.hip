@@ -58,6 +58,28 @@ __device__ __forceinline__ int classify(int32_t nh, int32_t nc, uint32_t flags) 
   return wave_class(cpl, (nh + 7) / 8);
 }
 
+// Wide register classes (see the wide register path below): up to 96 hot
+// and 1024 cold ranks, for problems no register class takes.
+constexpr int kWideWaves = 12;
+constexpr int kWideRows = 8 * kWideWaves;  // hot ranks
+constexpr int kWideMaxCpl = 16;            // LDS slots per lane
+constexpr int kWideCols = 64 * 15;         // cold ranks (15 columns per lane)
+constexpr int kWideThreads = kWideWaves * kWave;
+constexpr int kWideClassBase = 32;         // class codes 32 + CPL
+
+// Columns per lane: 4, an even count up to 14, or 15.
+__host__ __device__ constexpr int wide_cpl(int32_t nc) {
+  return nc <= 256 ? 4 : nc > 896 ? 15 : (int)((nc + 127) / 128) * 2;
+}
+__device__ __forceinline__ int wide_class(int32_t nh, int32_t nc, uint32_t flags) {
+  if (nh <= 0 || nc <= 0 || nh > kWideRows || nc > kWideCols) return 0;
+  if (flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER)) return 0;
+  if (classify(nh, nc, flags) != 0) return 0;  // a register class takes it
+  return kWideClassBase + wide_cpl(nc);
+}
+__host__ __device__ constexpr bool is_reg_class(int32_t c) { return c >= 1 && c < kWideClassBase; }
+__host__ __device__ constexpr bool is_wide_class(int32_t c) { return c > kWideClassBase; }
+
 struct SkParams {
   const float* a;
   const float* b;
@@ -168,7 +190,7 @@ __global__ void __launch_bounds__(NT) sinkhorn_kernel(SkParams p) {
   // ---- where the Kt block lives ----------------------------------------------
   const int64_t need = (int64_t)nh * nc;
   const bool degenerate = sh_bad || nh == 0 || nc == 0;
-  if (!degenerate && classify(nh, nc, p.flags) != 0) {  // the register path owns it
+  if (!degenerate && (classify(nh, nc, p.flags) != 0 || wide_class(nh, nc, p.flags) != 0)) {  // a register path owns it
     if (!STREAM && tid == 0) p.stream_flag[pb] = 0;
     return;
   }
@@ -929,7 +951,8 @@ __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* 
     nh += __popcll(__ballot(in && ai > 0.f));
     nc += __popcll(__ballot(in && bi > 0.f));
   }
-  const int c = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
+  int c = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
+  if (c == 0 && __ballot(bad) == 0) c = wide_class(nh, nc, p.flags);
   if (lane == 0) cls[pb] = c;
 }
 
@@ -940,6 +963,7 @@ __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* 
 __global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* __restrict__ cls, int32_t B, int32_t W,
                                                                 int32_t* __restrict__ multi,
                                                                 int32_t* __restrict__ single,
+                                                                int32_t* __restrict__ wide,
                                                                 int32_t* __restrict__ counts) {
   __shared__ int32_t wave_cnt[kSkWaves];
   __shared__ unsigned long long present[2];  // multi / single: bit w if some problem has per-wave work w
@@ -947,7 +971,7 @@ __global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* _
   __syncthreads();
   for (int32_t b = threadIdx.x; b < B; b += kSkThreads) {
     const int32_t c = cls[b];
-    if (c == 0) continue;
+    if (!is_reg_class(c)) continue;
     const int cpl = class_cpl(c), c8 = class_c8(c);
     atomicOr(&present[is_single(W, cpl, c8) ? 1 : 0], 1ull << (c8_per_wave(W, cpl, c8) * cpl));
   }
@@ -962,7 +986,7 @@ __global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* _
         const int32_t b = base + (int32_t)threadIdx.x;
         const int32_t c = b < B ? cls[b] : 0;
         bool f = false;
-        if (c != 0) {
+        if (is_reg_class(c)) {
           const int cpl = class_cpl(c), c8 = class_c8(c);
           f = (is_single(W, cpl, c8) ? 1 : 0) == k && c8_per_wave(W, cpl, c8) * cpl == wk;
         }
@@ -973,6 +997,412 @@ __global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* _
       }
     }
     if (threadIdx.x == 0) counts[k] = n;
+  }
+  // the wide problems, by index
+  int32_t n = 0;
+  for (int32_t base = 0; base < B; base += kSkThreads) {
+    const int32_t b = base + (int32_t)threadIdx.x;
+    const bool f = b < B && is_wide_class(cls[b]);
+    int32_t tot;
+    const int32_t pos = chunk_compact(f, wave_cnt, tot);
+    if (f) wide[n + pos] = b;
+    n += tot;
+  }
+  if (threadIdx.x == 0) counts[2] = n;
+}
+
+// ---------------------------------------------------------------------------
+// Wide register path: problems with up to 96 hot ranks and up to 1024 cold
+// ranks that the register classes do not take (large R).  One workgroup of
+// 12 waves per problem keeps the whole |H| x |C| block of Kt in VGPRs: wave w
+// holds rows 8w .. 8w+7, lane l the compact columns l + 64c (c < CPL).  The
+// row half-step is wave-local, as in the register path.  The column
+// half-step reduce-scatters the waves' partial sums through LDS: the owner of
+// column slot c (wave c mod 12) adds the 12 partials in wave order and
+// computes v for that slot, which every wave then reads back (two barriers
+// per iteration).  Out-of-range scalings trigger the same exact log-domain
+// updates.
+
+// LDS of the wide kernel: floats sA, F, u [96], the partial column sums
+// [12 waves][16 slots][64 lanes], v and G [16 slots][64 lanes]; then ints: flags [4], nh / nc
+// [4], cpos, hpos [R], cidx [960], hidx [96].
+__host__ __device__ constexpr size_t wide_lds_floats() {
+  return (size_t)3 * kWideRows + (size_t)(kWideWaves + 2) * kWave * kWideMaxCpl;
+}
+__host__ __device__ constexpr size_t wide_lds_bytes(int32_t R) {
+  return wide_lds_floats() * 4 + (size_t)(8 + 2 * R + kWideCols + kWideRows) * 4;
+}
+
+template <int CPL>
+__device__ __forceinline__ void wide_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
+                                           const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
+                                           const int32_t* hidx, const float* sAl, float* Fl, float* ul,
+                                           float* part, float* vsh, float* gsh, int32_t* flag, float kappa) {
+  constexpr int NO = (CPL + kWideWaves - 1) / kWideWaves;        // slots a wave owns, at most
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int rb = 8 * wv;
+  const int32_t R = p.R;
+  const float* bd = p.b + pb * R;
+  const float* Cb = p.C + pb * p.C_stride;
+#define CV(c) (lane + kWave * (c) < nc)
+#define CJ(c) (CV(c) ? cidx[lane + kWave * (c)] : 0)
+#define OWN(k) (wv + kWideWaves * (k) < CPL)
+#define OC(k) (wv + kWideWaves * (k))
+#define RV() (rb + (lane >> 3) < nh)
+  // slot c of this lane in the [slot][lane] arrays (consecutive lanes, distinct banks)
+  float* myv = vsh + lane;  // v, then the column-cap factors
+  float* myg = gsh + lane;  // G
+#define SLOT(c) ((c) * kWave)
+  // v lives in LDS (vsh) and is read where it is needed, which keeps the
+  // registers for the Kt block
+  float K[8][CPL];
+  float sBo[NO];  // demands of the slots this wave owns
+#pragma unroll
+  for (int k = 0; k < NO; ++k) {
+    sBo[k] = (OWN(k) && CV(OC(k))) ? bd[CJ(OC(k))] : 0.f;
+    if (OWN(k)) {
+      myg[SLOT(OC(k))] = 0.f;
+      myv[SLOT(OC(k))] = CV(OC(k)) ? 1.f : 0.f;
+    }
+  }
+  if ((lane & 7) == 0) ul[rb + (lane >> 3)] = RV() ? 1.f : 0.f;
+  const float sAq = sAl[rb + (lane >> 3)];
+  __syncthreads();  // every G slot is set
+
+  // Kt of this wave's rows from the potentials (optionally after the exact
+  // log-domain update of the row potentials), as in the register path; the
+  // costs are read again for Kt rather than kept, to bound the registers
+  auto build = [&](bool row_update) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int gi = rb + i;
+      if (gi < nh) {
+        int32_t go = __builtin_amdgcn_readfirstlane(gi);
+        asm volatile("" : "+s"(go));
+        const float* crow = Cb + (int64_t)__builtin_amdgcn_readfirstlane(hidx[go]) * R;
+        float fi;
+        if (row_update) {
+          float t[CPL];
+          float mx = -INFINITY;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            t[c] = CV(c) ? (myg[SLOT(c)] + flog2(myv[SLOT(c)])) - crow[CJ(c)] * kappa : -INFINITY;
+            mx = fmaxf(mx, t[c]);
+          }
+          mx = wave_max(mx);
+          float sum = 0.f;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
+          sum = first_lane(wave_sum(sum));
+          fi = flog2(sAl[gi]) - (mx + flog2(sum));
+          if (lane == 0) Fl[gi] = fi;
+        } else {
+          fi = Fl[gi];
+        }
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) K[i][c] = CV(c) ? fexp2((fi + myg[SLOT(c)]) - crow[CJ(c)] * kappa) : 0.f;
+      } else {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) K[i][c] = 0.f;
+      }
+    }
+  };
+
+  int32_t it = 1;
+  bool skip_row = true, row_update = false;
+  for (;;) {
+    build(row_update);
+    if (row_update) {
+      if ((lane & 7) == 0) ul[rb + (lane >> 3)] = RV() ? 1.f : 0.f;
+      row_update = false;
+    }
+    bool done = false, col_fail = false;
+    for (;;) {
+      if (!skip_row) {
+        // ---- row half-step on this wave's 8 rows ----------------------------------
+        float v[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) v[c] = myv[SLOT(c)];
+        float pp[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          float acc = K[r][0] * v[0];
+#pragma unroll
+          for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[r][c], v[c], acc);
+          pp[r] = acc;
+        }
+        const float y = reduce8(pp, lane);  // all lanes take part
+        const bool rv = RV();
+        const float un = sAq * frcp(rv ? y : 1.f);
+        const uint32_t bits = __float_as_uint(rv ? un : 1.f);
+        if ((lane & 7) == 0) ul[rb + (lane >> 3)] = un;
+        if (__ballot(!(bits >= __float_as_uint(kLo) && bits <= __float_as_uint(kHi))) != 0) {
+          row_update = true;
+          skip_row = true;
+          break;
+        }
+      }
+      skip_row = false;
+      // ---- column half-step: partial sums, reduce-scatter, v back to every wave ----
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      const float4 ua = *reinterpret_cast<const float4*>(ul + rb);
+      const float4 ub = *reinterpret_cast<const float4*>(ul + rb + 4);
+      const float us[8] = {ua.x, ua.y, ua.z, ua.w, ub.x, ub.y, ub.z, ub.w};
+      {
+        float x[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) x[c] = 0.f;
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) x[c] = __builtin_fmaf(us[r], K[r][c], x[c]);
+        float* mine = part + wv * kWideMaxCpl * kWave + lane;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) mine[SLOT(c)] = x[c];
+      }
+      __syncthreads();
+      uint32_t clo = 0xFFFFFFFFu, chi = 0u;
+#pragma unroll
+      for (int k = 0; k < NO; ++k) {
+        if (OWN(k)) {
+          const int c = OC(k);
+          float s = part[SLOT(c) + lane];
+#pragma unroll
+          for (int w = 1; w < kWideWaves; ++w) s = s + part[w * kWideMaxCpl * kWave + SLOT(c) + lane];
+          const float vn = sBo[k] * frcp(CV(c) ? s : 1.f);
+          const uint32_t bits = __float_as_uint(CV(c) ? vn : 1.f);
+          clo = bits < clo ? bits : clo;
+          chi = bits > chi ? bits : chi;
+          myv[SLOT(c)] = vn;
+        }
+      }
+      if (__ballot(!(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi))) != 0 && lane == 0)
+        atomicOr(&flag[1 + (it & 1)], 1);
+      __syncthreads();
+      col_fail = flag[1 + (it & 1)] != 0;  // the same on every wave
+      if (threadIdx.x == 0) flag[1 + ((it + 1) & 1)] = 0;  // read by every wave before the barrier above
+      done = it == p.iters;
+      if (!done) ++it;
+      if (col_fail || done) break;
+    }
+    if (col_fail) {
+      // exact log-domain update of the owned columns (online LSE over all
+      // rows), absorbed into G; Kt is rebuilt at the top of the loop
+#pragma unroll
+      for (int k = 0; k < NO; ++k) {
+        if (OWN(k)) {
+          const int c = OC(k);
+          float mx = -INFINITY, sum = 0.f;
+          if (CV(c)) {
+            const int32_t j = cidx[lane + kWave * c];
+            for (int32_t i = 0; i < nh; ++i) {
+              const float t = (Fl[i] + flog2(ul[i])) - Cb[(int64_t)hidx[i] * R + j] * kappa;
+              const float m2 = fmaxf(mx, t);
+              sum = sum * fexp2(mx - m2) + fexp2(t - m2);
+              mx = m2;
+            }
+          }
+          myg[SLOT(c)] = CV(c) ? flog2(sBo[k]) - (mx + flog2(sum)) : 0.f;
+          myv[SLOT(c)] = CV(c) ? 1.f : 0.f;
+        }
+      }
+      __syncthreads();  // every G is set; every owner has read F and u
+      if (done) {
+        build(false);
+        break;
+      }
+      continue;
+    }
+    if (done) break;
+  }
+
+  // ---- column cap, plan, potentials -----------------------------------------------
+  __syncthreads();  // every wave's row scalings are in ul
+  const float to_nat = p.eps * kLn2;
+  float v[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) v[c] = myv[SLOT(c)];
+  float fac[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) fac[c] = 1.f;
+  if (!(p.flags & TAOT_SK_NO_COLCAP)) {
+    {
+      float cs[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) cs[c] = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float ui = ul[rb + i];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) cs[c] += ui * K[i][c] * v[c];
+      }
+      float* mine = part + wv * kWideMaxCpl * kWave + lane;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) mine[SLOT(c)] = cs[c];
+    }
+    __syncthreads();  // also: every wave has read v
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+      if (OWN(k)) {
+        const int c = OC(k);
+        float s = part[SLOT(c) + lane];
+#pragma unroll
+        for (int w = 1; w < kWideWaves; ++w) s = s + part[w * kWideMaxCpl * kWave + SLOT(c) + lane];
+        myv[SLOT(c)] = CV(c) ? fminf(1.f, sBo[k] / (s + 1e-12f)) : 1.f;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) fac[c] = myv[SLOT(c)];
+  }
+  if (p.T) {
+    float* Tb = p.T + pb * R * R;
+    for (int32_t i = wv; i < R; i += kWideWaves) {
+      const bool hot = hpos[i] >= 0;
+      for (int32_t j = lane; j < R; j += kWave)
+        if (!hot || cpos[j] < 0) Tb[(int64_t)i * R + j] = 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int gi = rb + i;
+      if (gi < nh) {
+        const float ui = ul[gi];
+        float* trow = Tb + (int64_t)hidx[gi] * R;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+          if (CV(c)) trow[CJ(c)] = ui * K[i][c] * (v[c] * fac[c]);
+      }
+    }
+  }
+  for (int32_t i = threadIdx.x; i < R; i += kWideThreads) {
+    const int32_t ih = hpos[i];
+    if (p.f) p.f[pb * R + i] = ih >= 0 ? (Fl[ih] + flog2(ul[ih])) * to_nat : -INFINITY;
+    if (p.g && cpos[i] < 0) p.g[pb * R + i] = -INFINITY;
+  }
+  if (p.g) {
+#pragma unroll
+    for (int k = 0; k < NO; ++k)
+      if (OWN(k) && CV(OC(k))) p.g[pb * R + CJ(OC(k))] = (myg[SLOT(OC(k))] + flog2(v[OC(k)])) * to_nat;
+  }
+  if (threadIdx.x == 0 && p.status) p.status[pb] = 0u;
+#undef SLOT
+#undef RV
+#undef OC
+#undef OWN
+#undef CJ
+#undef CV
+}
+
+// One wide problem on the 12 waves of a workgroup.
+__device__ __forceinline__ void wide_problem(const SkParams& p, int64_t pb, int32_t* wl) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t R = p.R;
+  float* sAl = reinterpret_cast<float*>(wl);        // [96]
+  float* Fl = sAl + kWideRows;                      // [96]
+  float* ul = Fl + kWideRows;                       // [96]
+  float* part = ul + kWideRows;                     // [12][16][64]
+  float* vsh = part + kWideWaves * kWave * kWideMaxCpl;  // [16][64]
+  float* gsh = vsh + kWave * kWideMaxCpl;           // [16][64]
+  int32_t* iw = reinterpret_cast<int32_t*>(reinterpret_cast<float*>(wl) + wide_lds_floats());
+  int32_t* flag = iw;        // [4]: bad cost entry; column failure by parity
+  int32_t* cnt = iw + 4;     // [4]: nh, nc
+  int32_t* cpos = iw + 8;    // [R]
+  int32_t* hpos = cpos + R;  // [R]
+  int32_t* cidx = hpos + R;  // [1024]
+  int32_t* hidx = cidx + kWideCols;         // [96]
+  const float* a = p.a + pb * R;
+  const float* bd = p.b + pb * R;
+  const float* Cb = p.C + pb * p.C_stride;
+
+  // ---- supports and mass (wave 0) ---------------------------------------------
+  if (wv == 0) {
+    double sa = 0.0, sd = 0.0;
+    int32_t nh = 0, nc = 0;
+    for (int32_t base = 0; base < R; base += kWave) {
+      const int32_t i = base + lane;
+      const bool in = i < R;
+      const float ai = in ? a[i] : 0.f, bi = in ? bd[i] : 0.f;
+      sa += (double)ai;
+      sd += (double)bi;
+      const uint64_t hm = __ballot(in && ai > 0.f), cm = __ballot(in && bi > 0.f);
+      const uint64_t below = (1ull << lane) - 1ull;
+      const int32_t ph = nh + __popcll(hm & below), pc = nc + __popcll(cm & below);
+      if (in) {
+        hpos[i] = ai > 0.f ? ph : -1;
+        cpos[i] = bi > 0.f ? pc : -1;
+      }
+      if (in && ai > 0.f && ph < kWideRows) hidx[ph] = i;
+      if (in && bi > 0.f && pc < kWideCols) cidx[pc] = i;
+      nh += __popcll(hm);
+      nc += __popcll(cm);
+    }
+    sa = wave_sum_d(sa);
+    sd = wave_sum_d(sd);
+    double gamma = __shfl(sd, 0, kWave) / fmax(__shfl(sa, 0, kWave), kEps0);
+    gamma = gamma < 1.0 ? gamma : 1.0;
+    for (int32_t i = lane; i < kWideRows; i += kWave)
+      sAl[i] = i < nh ? (float)(gamma * (double)a[hidx[i]]) : 0.f;  // zero padding
+    if (lane == 0) {
+      cnt[0] = nh;
+      cnt[1] = nc;
+      flag[0] = flag[1] = flag[2] = 0;
+    }
+  }
+  __syncthreads();
+  const int32_t nh = cnt[0], nc = cnt[1];
+  const float kappa = kLog2e / p.eps;
+
+  // ---- first row update over all R columns (v = 1), rows dealt out over the waves
+  bool badc = false;
+  for (int32_t i = wv; i < nh; i += kWideWaves) {
+    const float* crow = Cb + (int64_t)hidx[i] * R;
+    float mx = -INFINITY;
+    for (int32_t j = lane; j < R; j += kWave) {
+      const float c = crow[j];
+      badc |= !(c == c) || c == INFINITY || c == -INFINITY;
+      mx = fmaxf(mx, -c * kappa);
+    }
+    mx = wave_max(mx);
+    float sum = 0.f;
+    for (int32_t j = lane; j < R; j += kWave) sum += fexp2(-crow[j] * kappa - mx);
+    sum = first_lane(wave_sum(sum));
+    if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
+  }
+  if (__ballot(badc) != 0 && lane == 0) atomicOr(&flag[0], 1);
+  __syncthreads();
+  if (flag[0] != 0) {
+    if (p.T)
+      for (int64_t q = threadIdx.x; q < (int64_t)R * R; q += kWideThreads) p.T[pb * R * R + q] = 0.f;
+    for (int32_t i = threadIdx.x; i < R; i += kWideThreads) {
+      if (p.f) p.f[pb * R + i] = -INFINITY;
+      if (p.g) p.g[pb * R + i] = -INFINITY;
+    }
+    if (threadIdx.x == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
+    return;
+  }
+  switch (wide_cpl(nc)) {
+#define TAOT_WIDE_CASE(CPL_)                                                                          \
+  case CPL_:                                                                                          \
+    wide_solve<CPL_>(p, pb, nh, nc, cpos, hpos, cidx, hidx, sAl, Fl, ul, part, vsh, gsh, flag, kappa); \
+    break;
+    TAOT_WIDE_CASE(4) TAOT_WIDE_CASE(6) TAOT_WIDE_CASE(8) TAOT_WIDE_CASE(10) TAOT_WIDE_CASE(12)
+    TAOT_WIDE_CASE(14) TAOT_WIDE_CASE(15)
+#undef TAOT_WIDE_CASE
+    default: break;
+  }
+}
+
+// The listed wide problems, a grid walking the list (one problem per
+// workgroup at a time; the workgroup's LDS is reused by its next problem).
+__global__ void __launch_bounds__(kWideThreads)
+sinkhorn_wide_kernel(SkParams p, const int32_t* __restrict__ list, const int32_t* __restrict__ count) {
+  extern __shared__ __attribute__((aligned(16))) int32_t wl[];
+  const int32_t n = *count;
+  for (int32_t k = blockIdx.x; k < n; k += gridDim.x) {
+    wide_problem(p, list[k], wl);
+    __syncthreads();
   }
 }
 
@@ -1004,10 +1434,21 @@ taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* lists, int32_t
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   int32_t* multi = lists;
   int32_t* single = lists + p.B;
-  hipLaunchKernelGGL(wave_order_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, W, multi, single, counts);
+  int32_t* wide = lists + 2 * (int64_t)p.B;
+  hipLaunchKernelGGL(wave_order_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, W, multi, single, wide,
+                     counts);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  return W == 4 ? launch_reg_kernel<4>(p, multi, single, counts, stream)
-                : launch_reg_kernel<2>(p, multi, single, counts, stream);
+  const taot_status st = W == 4 ? launch_reg_kernel<4>(p, multi, single, counts, stream)
+                                : launch_reg_kernel<2>(p, multi, single, counts, stream);
+  if (st != TAOT_OK) return st;
+  // the wide problems: at most one workgroup per compute unit at a time
+  const size_t lds = wide_lds_bytes(p.R);
+  if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_wide_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         (int)lds) != hipSuccess)
+    return TAOT_ERR_LAUNCH;
+  const unsigned grid = (unsigned)std::min<int64_t>(p.B, cus);
+  hipLaunchKernelGGL(sinkhorn_wide_kernel, dim3(grid), dim3(kWideThreads), lds, stream, p, wide, counts + 2);
+  return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
 }
 
 // Largest nh * nc over disjoint supports of R ranks (nh + nc <= R).
@@ -1016,8 +1457,8 @@ int64_t max_block(int32_t R) { return (int64_t)(R / 2) * (R - R / 2); }
 struct SkWs {
   int32_t* flag;
   int32_t* cls;     // [B] register class
-  int32_t* lists;   // [2][B] register problems: multi, single
-  int32_t* counts;  // [2]
+  int32_t* lists;   // [3][B] register problems: multi, single, wide
+  int32_t* counts;  // [3]
   float* kt;
   int64_t kt_stride;
   size_t bytes;
@@ -1028,8 +1469,8 @@ SkWs carve(void* ws, int32_t B, int32_t R) {
   SkWs w;
   w.flag = c.take<int32_t>((size_t)B);
   w.cls = c.take<int32_t>((size_t)B);
-  w.lists = c.take<int32_t>((size_t)2 * B);
-  w.counts = c.take<int32_t>(2);
+  w.lists = c.take<int32_t>((size_t)3 * B);
+  w.counts = c.take<int32_t>(3);
   w.kt_stride = round_up((int64_t)R * R, 64);
   w.kt = c.take<float>((size_t)B * w.kt_stride);
   w.bytes = c.off;

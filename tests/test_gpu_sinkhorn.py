@@ -72,14 +72,44 @@ def test_mixed_size_classes_in_one_batch(seed, gpu):
     _check_against_oracle(a, b, C, 0.08, 300)
 
 
-def test_workload4_streamed(gpu):
-    """R = 1024: the block never fits on chip and is streamed through device memory."""
+@pytest.mark.parametrize("flags", [0, taot.SK_NO_REGISTER])
+def test_workload4(flags, gpu):
+    """R = 1024 (about 85 hot and 940 cold ranks): by default the wide
+    register kernel holds the block in one workgroup's registers; with
+    SK_NO_REGISTER it is streamed through device memory."""
     w = W.WORKLOADS[4]
-    print("[sinkhorn parity] workload 4 problem 0 (streamed)", flush=True)
+    print(f"[sinkhorn parity] workload 4 problem 0 flags {flags}", flush=True)
     _, L = oracle_inputs(w, [0])
     C = W.cost_matrix(w)
-    _, st, rels = _check_against_oracle(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, w.iters)
-    assert np.all(st == taot.ST_STREAMED)
+    _, st, rels = _check_against_oracle(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, w.iters,
+                                        flags)
+    assert np.all(st == (taot.ST_STREAMED if flags else 0))
+
+
+@pytest.mark.parametrize("R", [300, 1100])
+def test_wide_shapes(R, gpu):
+    """Problems for the wide register kernel (65..96 hot ranks, or more than
+    256 cold ranks), one per columns-per-lane class, with eps small enough to
+    trigger the log-domain updates; beside them one problem too large for it
+    (streamed) in the same batch."""
+    rng = np.random.default_rng(R)
+    if R == 300:
+        shapes = [(65, 200), (80, 220), (96, 204), (40, 257), (8, 290)]
+    else:
+        shapes = [(1, 300), (50, 400), (96, 500), (33, 640), (70, 700), (90, 830), (60, 897), (96, 960), (20, 1000)]
+    B = len(shapes)
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p, (nh, nc) in enumerate(shapes):
+        perm = rng.permutation(R)
+        a[p, perm[:nh]] = rng.integers(1, 4000, size=nh)
+        b[p, perm[nh:nh + nc]] = rng.multinomial(int(a[p].sum()), np.full(nc, 1.0 / nc)) + 1
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32))
+    for eps, iters in ((0.5, 3), (0.08, 120)):
+        print(f"[sinkhorn parity] wide shapes R={R} eps={eps}", flush=True)
+        _, st, _ = _check_against_oracle(a, b, C, eps, iters)
+        streamed = [nc > 960 for _, nc in shapes]
+        assert np.array_equal(st == taot.ST_STREAMED, np.array(streamed)), st
 
 
 def test_forced_stream_matches_lds_path(gpu):
