@@ -7,7 +7,7 @@
 // sparse scaling algorithms for entropy regularized transport problems"):
 //     T = diag(u) Kt diag(v),  Kt_ij = exp2(F_i + G_j - C'_ij),  C' = C log2(e) / eps,
 // where F, G are absorbed potentials (log2 units) and u, v are scalings kept
-// in [2^-40, 2^40].  One half-step is one GEMV-like sweep with one FMA per
+// in [2^-60, 2^60].  One half-step is one GEMV-like sweep with one FMA per
 // entry; when a scaling leaves its range (or its sum under/overflows) that
 // row or column is recomputed exactly in the log domain (max-shifted
 // log-sum-exp over the current potentials), absorbed into F or G and its Kt
@@ -15,8 +15,8 @@
 // paper's update; the fp32 result agrees with the fp64 definition to
 // rounding.  The range is wide to keep the (costly) log-domain updates rare,
 // and narrow enough that a Kt entry lost to underflow (below 2^-149) carries
-// less than 2^-69 of plan mass (u v < 2^80) and no row or column sum comes
-// near overflow.
+// less than 2^-29 of plan mass (u v < 2^120).  A sum that overflows or
+// underflows gives an out-of-range scaling and so takes the exact update.
 //
 // Support.  Supply is zero off the hot set H = {a > 0} and demand is zero off
 // the cold set C = {b > 0} (Sec. A.2), so after the first column update every
@@ -38,8 +38,8 @@ namespace {
 constexpr int kSkThreads = 256;
 constexpr int kSkWaves = kSkThreads / kWave;
 constexpr int kSkStreamThreads = 1024;  // threads per problem of the streamed kernel
-constexpr float kLo = 0x1p-40f;
-constexpr float kHi = 0x1p40f;
+constexpr float kLo = 0x1p-60f;
+constexpr float kHi = 0x1p60f;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kLdsMaxR = 256;            // beyond this every problem is streamed
