@@ -411,9 +411,6 @@ __device__ __forceinline__ void swap16(float& lo, float& hi) {
   lo = __uint_as_float(r[0]);
   hi = __uint_as_float(r[1]);
 }
-__device__ __forceinline__ float first_lane(float x) {
-  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
-}
 
 // Sums 8 per-lane values over the wave; lane l ends with the total of value
 // (l >> 3).  Halving steps pair lanes l ^ 32 (permlane32 swap), l ^ 16
@@ -432,6 +429,34 @@ __device__ __forceinline__ float reduce8(float (&p)[8], int lane) {
   y = y + dpp<0x4E>(y);               // quad_perm [2,3,0,1]
   y = y + dpp<0xB1>(y);               // quad_perm [1,0,3,2]
   return y;
+}
+
+// Max and sum over the 64 lanes, every lane getting the result (bitwise the
+// same: each step combines symmetric partners): DPP steps within each
+// 16-lane row, then the permlane16 and permlane32 swaps across rows.
+__device__ __forceinline__ float lanes_max(float x) {
+  x = fmaxf(x, dpp<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = fmaxf(x, dpp<0x141>(x));  // row_half_mirror
+  x = fmaxf(x, dpp<0x140>(x));  // row_mirror
+  float y = x;
+  swap16(x, y);
+  x = fmaxf(x, y);
+  y = x;
+  swap32(x, y);
+  return fmaxf(x, y);
+}
+__device__ __forceinline__ float lanes_sum(float x) {
+  x = x + dpp<0xB1>(x);
+  x = x + dpp<0x4E>(x);
+  x = x + dpp<0x141>(x);
+  x = x + dpp<0x140>(x);
+  float y = x;
+  swap16(x, y);
+  x = x + y;
+  y = x;
+  swap32(x, y);
+  return x + y;
 }
 
 // LDS of the register kernels, per workgroup: floats sA, F, u [64], the
@@ -530,11 +555,11 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
             t[c] = CV(c) ? (GL(c) + flog2(v[c])) - cc[c] : -INFINITY;
             mx = fmaxf(mx, t[c]);
           }
-          mx = wave_max(mx);
+          mx = lanes_max(mx);
           float sum = 0.f;
 #pragma unroll
           for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
-          sum = first_lane(wave_sum(sum));
+          sum = lanes_sum(sum);
           fi = flog2(sAl[gi]) - (mx + flog2(sum));
           if (lane == 0) Fl[gi] = fi;
         } else {
@@ -878,10 +903,10 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
       badc |= !(c == c) || c == INFINITY || c == -INFINITY;
       mx = fmaxf(mx, -c * kappa);
     }
-    mx = wave_max(mx);
+    mx = lanes_max(mx);
     float sum = 0.f;
     for (int32_t j = lane; j < R; j += kWave) sum += fexp2(-crow[j] * kappa - mx);
-    sum = first_lane(wave_sum(sum));
+    sum = lanes_sum(sum);
     if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
   }
   if (__ballot(badc) != 0 && lane == 0) flag[0] = 1;
@@ -1093,11 +1118,11 @@ __device__ __forceinline__ void wide_solve(const SkParams& p, int64_t pb, int32_
             t[c] = CV(c) ? (myg[SLOT(c)] + flog2(myv[SLOT(c)])) - crow[CJ(c)] * kappa : -INFINITY;
             mx = fmaxf(mx, t[c]);
           }
-          mx = wave_max(mx);
+          mx = lanes_max(mx);
           float sum = 0.f;
 #pragma unroll
           for (int c = 0; c < CPL; ++c) sum += CV(c) ? fexp2(t[c] - mx) : 0.f;
-          sum = first_lane(wave_sum(sum));
+          sum = lanes_sum(sum);
           fi = flog2(sAl[gi]) - (mx + flog2(sum));
           if (lane == 0) Fl[gi] = fi;
         } else {
@@ -1367,10 +1392,10 @@ __device__ __forceinline__ void wide_problem(const SkParams& p, int64_t pb, int3
       badc |= !(c == c) || c == INFINITY || c == -INFINITY;
       mx = fmaxf(mx, -c * kappa);
     }
-    mx = wave_max(mx);
+    mx = lanes_max(mx);
     float sum = 0.f;
     for (int32_t j = lane; j < R; j += kWave) sum += fexp2(-crow[j] * kappa - mx);
-    sum = first_lane(wave_sum(sum));
+    sum = lanes_sum(sum);
     if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
   }
   if (__ballot(badc) != 0 && lane == 0) atomicOr(&flag[0], 1);
