@@ -944,8 +944,8 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
 __host__ __device__ constexpr size_t single_lds_bytes(int32_t R) { return (wave_lds_bytes(R, 1) + 15) / 16 * 16; }
 
 // The register problems of a batch on workgroups of W waves: item k < n_multi
-// is multi[k] on all W waves; item n_multi + g holds single[W g + w] on wave
-// w, each wave with its own LDS slice.
+// is multi[k] on all W waves; item n_multi + g holds W single problems, one
+// per wave, each wave with its own LDS slice.
 template <int W>
 __global__ void __launch_bounds__(W * kWave, W == 4 ? 4 : 2)
 sinkhorn_reg_kernel(SkParams p, const int32_t* __restrict__ multi, const int32_t* __restrict__ single,
@@ -957,9 +957,15 @@ sinkhorn_reg_kernel(SkParams p, const int32_t* __restrict__ multi, const int32_t
     wave_problem<W, W>(p, multi[k], wl);
     return;
   }
+  // single group g pairs the heavier half of the list (dealt from its front)
+  // with the lighter half (from its back), W / 2 problems each, so that the
+  // group's waves carry similar total work
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int64_t j = (int64_t)(k - n_multi) * W + w;
-  if (j < n_single) wave_problem<1, W>(p, single[j], wl + (size_t)w * (single_lds_bytes(p.R) / 4));
+  const int64_t g = k - n_multi, F = ((int64_t)n_single + 1) / 2;
+  const bool front = w < W / 2;
+  const int64_t j = front ? g * (W / 2) + w : (int64_t)n_single - 1 - (g * (W / 2) + (w - W / 2));
+  if (front ? j < F : (j >= F && j < n_single))
+    wave_problem<1, W>(p, single[j], wl + (size_t)w * (single_lds_bytes(p.R) / 4));
 }
 
 // Register class of every problem (0: not a register problem).
