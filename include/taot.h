@@ -89,7 +89,8 @@ const char* taot_status_string(taot_status s);
  *   alpha   [B]       double  score scale alpha = mean * R / E = L / E.
  *   bad_ids [B]       int64   ids outside [0, E), nullable.
  *   status  [B]       uint32  TAOT_ST_BAD_ID, TAOT_ST_BAD_INPUT (home out of range).
- * Limits: 1 <= R <= TAOT_MAX_RANKS, 1 <= E <= TAOT_MAX_EXPERTS, N >= 0, B >= 0.
+ * Limits: 1 <= R <= TAOT_MAX_RANKS, 1 <= E <= TAOT_MAX_EXPERTS, B >= 0,
+ * 0 <= N <= 2^31 - 1 and B * R <= 2^31 - 1 (else TAOT_ERR_UNSUPPORTED).
  */
 size_t taot_plan_loads_workspace_size(int32_t B, int32_t R, int32_t E);
 taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N, int32_t E,

@@ -40,7 +40,7 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
   if (B == 0) return TAOT_OK;
   if ((N > 0 && !ids) || !home || !n || !load_e || !load_r || !excess || !spare || !spill || !alpha)
     return TAOT_ERR_INVALID_ARG;
-  if ((int64_t)B * R > 0x7fffffffLL) return TAOT_ERR_UNSUPPORTED;
+  if ((int64_t)B * R > 0x7fffffffLL || N > 0x7fffffffLL) return TAOT_ERR_UNSUPPORTED;
   if (!ws || ws_bytes < plan_loads_ws(B, R, E)) return TAOT_ERR_WORKSPACE;
   return launch_plan_loads(ids, B, R, N, E, home, n, load_e, load_r, excess, spare, spill, supply,
                            demand, rho, alpha, bad_ids, status, ws, static_cast<hipStream_t>(stream));

@@ -28,10 +28,11 @@ typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
 // rank_ptr[R+1], rank_exp[E]: experts of rank r are rank_exp[rank_ptr[r] ..
 // rank_ptr[r+1]) in ascending id order.  bad_home = 1 if some home is outside
-// [0, R).
+// [0, R).  Also clears the per-problem counts of skipped ids, bad_prob[B].
 __global__ void __launch_bounds__(kCsrThreads)
-home_csr_kernel(const int32_t* __restrict__ home, int32_t R, int32_t E, int32_t* __restrict__ rank_ptr,
-                int32_t* __restrict__ rank_exp, int32_t* __restrict__ bad_home) {
+home_csr_kernel(const int32_t* __restrict__ home, int32_t B, int32_t R, int32_t E, int32_t* __restrict__ rank_ptr,
+                int32_t* __restrict__ rank_exp, int32_t* __restrict__ bad_home,
+                unsigned long long* __restrict__ bad_prob) {
   __shared__ int32_t cnt[TAOT_MAX_RANKS + 1];
   __shared__ int32_t bad;
   if (threadIdx.x == 0) bad = 0;
@@ -62,74 +63,96 @@ home_csr_kernel(const int32_t* __restrict__ home, int32_t R, int32_t E, int32_t*
       if (home[e] == r) rank_exp[pos++] = e;
   }
   if (threadIdx.x == 0) bad_home[0] = bad;
+  for (int32_t b = threadIdx.x; b < B; b += kCsrThreads) bad_prob[b] = 0;
 }
 
 // One block per (problem, source rank) row of N ids.  LDS holds `copies`
-// private histograms of E+1 words (the +1 rotates banks between copies); lane
-// group (tid & (copies-1)) owns one copy, which spreads the heavy Zipf bins
-// over distinct LDS addresses.  Ids outside [0, E) are counted per row.
+// private histograms of E+1 words; lane group (tid & (copies-1)) owns one
+// copy, which spreads the heavy Zipf bins over distinct LDS addresses.  Word E
+// of a copy is where ids outside [0, E) are counted, so the count carries no
+// branch and the extra word also rotates banks between copies.
+//
+// Ids are read exactly once, so they stream past the caches.  The bulk of a
+// row goes in batches of kHistUnroll 16-byte loads per thread, none of them
+// predicated, with the next batch in flight while the current one is counted
+// (two register sets, a and b, take turns).  The first batch is issued before
+// the counters are cleared.
 __global__ void __launch_bounds__(kHistThreads)
-histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t E, int32_t copies,
-                 int32_t* __restrict__ n, int32_t* __restrict__ bad_rows) {
+histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t E, int32_t copies,
+                 int32_t* __restrict__ n, unsigned long long* __restrict__ bad_prob) {
   extern __shared__ int32_t bins[];
   const int64_t row = blockIdx.x;
   const int32_t stride = E + 1;
   const int32_t words = copies * stride;
-  for (int32_t i = threadIdx.x; i < words; i += kHistThreads) bins[i] = 0;
-  __syncthreads();
   int32_t* my = bins + (int32_t)(threadIdx.x & (copies - 1)) * stride;
   const int32_t* src = ids + row * N;
   const uint32_t uE = (uint32_t)E;
-  int32_t bad = 0;
+  auto count = [&](int32_t q) { atomicAdd(&my[(uint32_t)q < uE ? q : E], 1); };
+  auto count4 = [&](const v4i& v) {
+    count(v.x);
+    count(v.y);
+    count(v.z);
+    count(v.w);
+  };
   const bool vec = (N % 4 == 0) && ((reinterpret_cast<uintptr_t>(src) & 15u) == 0);
-  if (vec) {
-    const v4i* s4 = reinterpret_cast<const v4i*>(src);
-    const int64_t n4 = N / 4;
-    for (int64_t base = threadIdx.x; base < n4; base += (int64_t)kHistThreads * kHistUnroll) {
-      v4i v[kHistUnroll];
+  const v4i* s4 = reinterpret_cast<const v4i*>(src);
+  constexpr int64_t kStep = (int64_t)kHistThreads * kHistUnroll;
+  const int64_t nb = vec ? (N / 4) / kStep : 0;  // full batches
+  const v4i* p = s4 + threadIdx.x;
+  v4i a[kHistUnroll], b[kHistUnroll];
+  if (nb > 0) {
 #pragma unroll
-      for (int u = 0; u < kHistUnroll; ++u) {
-        const int64_t i = base + (int64_t)u * kHistThreads;
-        // ids are read exactly once: stream them past the caches
-        v[u] = i < n4 ? __builtin_nontemporal_load(&s4[i]) : v4i{0, 0, 0, 0};
+    for (int u = 0; u < kHistUnroll; ++u) a[u] = __builtin_nontemporal_load(p + u * kHistThreads);
+  }
+  for (int32_t i = threadIdx.x; i < words; i += kHistThreads) bins[i] = 0;
+  __syncthreads();
+  if (nb > 0) {
+    int64_t m = 0;  // batch held in a (even turns) or b (odd turns)
+    for (;;) {
+      if (m + 1 == nb) {
+#pragma unroll
+        for (int u = 0; u < kHistUnroll; ++u) count4(a[u]);
+        break;
       }
+      p += kStep;
 #pragma unroll
-      for (int u = 0; u < kHistUnroll; ++u) {
-        const int64_t i = base + (int64_t)u * kHistThreads;
-        if (i >= n4) break;
-        const int32_t q[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      for (int u = 0; u < kHistUnroll; ++u) b[u] = __builtin_nontemporal_load(p + u * kHistThreads);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          if ((uint32_t)q[c] < uE) atomicAdd(&my[q[c]], 1);
-          else ++bad;
-        }
+      for (int u = 0; u < kHistUnroll; ++u) count4(a[u]);
+      if (++m + 1 == nb) {
+#pragma unroll
+        for (int u = 0; u < kHistUnroll; ++u) count4(b[u]);
+        break;
       }
-    }
-  } else {
-    for (int64_t i = threadIdx.x; i < N; i += kHistThreads) {
-      const int32_t q = src[i];
-      if ((uint32_t)q < uE) atomicAdd(&my[q], 1);
-      else ++bad;
+      p += kStep;
+#pragma unroll
+      for (int u = 0; u < kHistUnroll; ++u) a[u] = __builtin_nontemporal_load(p + u * kHistThreads);
+#pragma unroll
+      for (int u = 0; u < kHistUnroll; ++u) count4(b[u]);
+      ++m;
     }
   }
+  // what the full batches left: the vector tail, or the whole row when it is
+  // not 16-byte aligned
+  if (vec) {
+    for (int64_t i = nb * kStep + threadIdx.x; i < N / 4; i += kHistThreads)
+      count4(__builtin_nontemporal_load(&s4[i]));
+  } else {
+    for (int64_t i = threadIdx.x; i < N; i += kHistThreads) count(src[i]);
+  }
   __syncthreads();
+  // The counts are not read again by this kernel, and ordinary stores of them
+  // interleaved with the id stream cost far more read bandwidth than their
+  // size: they are written past the caches too.  Skipped ids are rare, so
+  // their count reaches memory only when it is not zero.
   int32_t* dst = n + row * E;
-  for (int32_t e = threadIdx.x; e < E; e += kHistThreads) {
+  for (int32_t e = threadIdx.x; e <= E; e += kHistThreads) {
     int32_t s = 0;
     for (int32_t c = 0; c < copies; ++c) s += bins[c * stride + e];
-    dst[e] = s;
-  }
-  // per-row count of skipped ids (fixed-order block reduction)
-  __shared__ int32_t red[kHistThreads / kWave];
-  int32_t w = bad;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) w += __shfl_xor(w, o, kWave);
-  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = w;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int32_t s = 0;
-    for (int i = 0; i < kHistThreads / kWave; ++i) s += red[i];
-    bad_rows[row] = s;
+    if (e < E)
+      __builtin_nontemporal_store(s, &dst[e]);
+    else if (s != 0)
+      atomicAdd(&bad_prob[row / R], (unsigned long long)s);
   }
 }
 
@@ -137,7 +160,7 @@ histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t E, int32_t 
 __global__ void __launch_bounds__(kMargThreads)
 marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int32_t* __restrict__ home,
                  const int32_t* __restrict__ rank_ptr, const int32_t* __restrict__ rank_exp,
-                 const int32_t* __restrict__ bad_home, const int32_t* __restrict__ bad_rows,
+                 const int32_t* __restrict__ bad_home, const unsigned long long* __restrict__ bad_prob,
                  int64_t* __restrict__ load_e, int64_t* __restrict__ load_r, int64_t* __restrict__ excess,
                  int64_t* __restrict__ spare, int64_t* __restrict__ spill, float* __restrict__ supply,
                  float* __restrict__ demand, double* __restrict__ rho, double* __restrict__ alpha,
@@ -145,21 +168,9 @@ marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int3
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x;
   __shared__ int64_t red_s[kMargThreads / kWave], red_m[kMargThreads / kWave];
-  __shared__ int64_t sh_L, sh_max, sh_bad;
+  __shared__ int64_t sh_L, sh_max;
   const bool home_bad = bad_home[0] != 0;
-
-  // skipped ids of this problem
-  int64_t nb = 0;
-  for (int32_t r = tid; r < R; r += kMargThreads) nb += bad_rows[b * R + r];
-  nb = wave_sum_i64(nb);
-  if ((tid & (kWave - 1)) == 0) red_s[tid / kWave] = nb;
-  __syncthreads();
-  if (tid == 0) {
-    int64_t s = 0;
-    for (int i = 0; i < kMargThreads / kWave; ++i) s += red_s[i];
-    sh_bad = s;
-  }
-  __syncthreads();
+  const int64_t skipped = (int64_t)bad_prob[b];  // ids of this problem outside [0, E)
 
   int64_t* xe = load_e + b * E;
   if (home_bad) {
@@ -172,8 +183,8 @@ marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int3
     if (tid == 0) {
       if (rho) rho[b] = 0.0;
       alpha[b] = 0.0;
-      if (bad_ids) bad_ids[b] = sh_bad;
-      if (status) status[b] = TAOT_ST_BAD_INPUT | (sh_bad ? TAOT_ST_BAD_ID : 0u);
+      if (bad_ids) bad_ids[b] = skipped;
+      if (status) status[b] = TAOT_ST_BAD_INPUT | (skipped ? TAOT_ST_BAD_ID : 0u);
     }
     return;
   }
@@ -229,8 +240,8 @@ marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int3
   if (tid == 0) {
     if (rho) rho[b] = L > 0 ? (double)((int64_t)R * sh_max - L) / (double)L : 0.0;
     alpha[b] = (double)L / (double)E;
-    if (bad_ids) bad_ids[b] = sh_bad;
-    if (status) status[b] = sh_bad ? TAOT_ST_BAD_ID : 0u;
+    if (bad_ids) bad_ids[b] = skipped;
+    if (status) status[b] = skipped ? TAOT_ST_BAD_ID : 0u;
   }
   // spill: prefix of the expert's rank in ascending (x, id) order, then
   // sigma_k - sigma_{k-1} with sigma = max(prefix - mean, 0)
@@ -253,7 +264,7 @@ struct LoadsWs {
   int32_t* rank_ptr;
   int32_t* rank_exp;
   int32_t* bad_home;
-  int32_t* bad_rows;
+  unsigned long long* bad_prob;
   size_t bytes;
 };
 
@@ -263,7 +274,7 @@ LoadsWs carve(void* ws, int32_t B, int32_t R, int32_t E) {
   w.rank_ptr = c.take<int32_t>((size_t)R + 1);
   w.rank_exp = c.take<int32_t>((size_t)E);
   w.bad_home = c.take<int32_t>(1);
-  w.bad_rows = c.take<int32_t>((size_t)B * R);
+  w.bad_prob = c.take<unsigned long long>((size_t)B);
   w.bytes = c.off;
   return w;
 }
@@ -279,8 +290,8 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
                               uint32_t* status, void* ws, hipStream_t stream) {
   if (B == 0) return TAOT_OK;
   LoadsWs w = carve(ws, B, R, E);
-  hipLaunchKernelGGL(home_csr_kernel, dim3(1), dim3(kCsrThreads), 0, stream, home, R, E, w.rank_ptr,
-                     w.rank_exp, w.bad_home);
+  hipLaunchKernelGGL(home_csr_kernel, dim3(1), dim3(kCsrThreads), 0, stream, home, B, R, E, w.rank_ptr,
+                     w.rank_exp, w.bad_home, w.bad_prob);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   int32_t copies = 16;
   while (copies > 1 && (int64_t)copies * (E + 1) > kHistLdsWords) copies >>= 1;
@@ -290,10 +301,10 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
                                           (int)lds) != hipSuccess)
     return TAOT_ERR_LAUNCH;
   hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
-                     ids, N, E, copies, n, w.bad_rows);
+                     ids, N, R, E, copies, n, w.bad_prob);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   hipLaunchKernelGGL(marginals_kernel, dim3((unsigned)B), dim3(kMargThreads), 0, stream, n, R, E, home,
-                     w.rank_ptr, w.rank_exp, w.bad_home, w.bad_rows, load_e, load_r, excess, spare,
+                     w.rank_ptr, w.rank_exp, w.bad_home, w.bad_prob, load_e, load_r, excess, spare,
                      spill, supply, demand, rho, alpha, bad_ids, status);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   return TAOT_OK;

@@ -60,6 +60,7 @@ def test_host_validation_plan_loads():
     assert args(1, 4, 8, 0) == 1            # E <= 0
     assert args(1, 2049, 8, 4) == 2         # R beyond TAOT_MAX_RANKS
     assert args(1, 4, 8, 40000) == 2        # E beyond TAOT_MAX_EXPERTS
+    assert args(1, 4, 1 << 31, 4) == 2      # N beyond what an int32 count holds
     assert args(1, 4, 8, 4, ids=None) == 1  # null ids
     assert args(1, 4, 8, 4, ws=None) == 3   # no workspace
     assert args(1, 4, 8, 4, wsb=8) == 3     # workspace too small

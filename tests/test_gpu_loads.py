@@ -51,8 +51,11 @@ def test_random_shapes(seed, gpu):
     _compare(_gpu_loads(ids, home, E), O.plan_loads(ids, home, E))
 
 
+# N = 4096 * k + 4 * t: k full batches of the vector path (1, 2, 3, 5; the
+# batches alternate between two register sets) and a vector tail of t.
 @pytest.mark.parametrize("R,E,N", [(1, 1, 5), (1, 7, 0), (3, 1, 13), (17, 5, 1), (64, 4097, 1003),
-                                   (300, 64, 66), (5, 1023, 4096), (2, 32768, 64), (2048, 3, 2)])
+                                   (300, 64, 66), (5, 1023, 4096), (2, 32768, 64), (2048, 3, 2),
+                                   (3, 40, 8260), (2, 384, 12292), (1, 64, 20480), (4, 9, 4092)])
 def test_edge_shapes_with_bad_ids(R, E, N, gpu):
     rng = np.random.default_rng(R * 31 + E)
     B = 2
