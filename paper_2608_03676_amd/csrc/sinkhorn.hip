@@ -352,12 +352,14 @@ __global__ void __launch_bounds__(NT) sinkhorn_kernel(SkParams p) {
 // An out-of-range scaling triggers the exact log-domain update of the wave's
 // rows (or of all columns), absorbed into the potentials, with Kt rebuilt.
 //
-// Launch shape.  One kernel runs every register problem of a batch, with
-// workgroups of W waves (W = 4 when the batch is small enough that every
-// problem can hold four waves at once, else W = 2).  A workgroup runs either
-// one problem on all W waves ("multi") or W problems on one wave each
-// ("single"), never two multi-wave problems, so workgroup barriers only ever
-// join the waves of one problem.
+// Launch shape.  One kernel runs every register problem of a batch.  Its
+// shapes use W waves per multi-wave problem (W = 4 when the batch is small
+// enough that every problem can hold four waves at once, else W = 2), and its
+// workgroups run either one problem on W waves ("multi") or one problem per
+// wave ("single"), never two multi-wave problems, so workgroup barriers only
+// ever join the waves of one problem.  Single groups of the two-wave shapes
+// span a whole compute unit (eight waves) so that the problems sharing a SIMD
+// can be paired by work.
 //   W = 4 (at most 128 VGPRs, four waves per SIMD): problems of one chunk are
 //     single; the rest are multi with ceil(C8 / 4) chunks per wave.
 //   W = 2 (at most 256 VGPRs, two waves per SIMD): a problem is single when
@@ -943,27 +945,58 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
 // LDS of one wave of a single item, rounded to 16 bytes.
 __host__ __device__ constexpr size_t single_lds_bytes(int32_t R) { return (wave_lds_bytes(R, 1) + 15) / 16 * 16; }
 
-// The register problems of a batch on workgroups of W waves: item k < n_multi
-// is multi[k] on all W waves; item n_multi + g holds W single problems, one
-// per wave, each wave with its own LDS slice.
-template <int W>
-__global__ void __launch_bounds__(W * kWave, W == 4 ? 4 : 2)
+// The register problems of a batch on workgroups of G waves (G = W, or G = 8
+// for the two-wave shapes): item k < n_multi is multi[k] on waves 0 .. W-1
+// (any further waves end at once, and a barrier only waits for the waves that
+// have not ended); item n_multi + g holds G single problems, one per wave,
+// each wave with its own LDS slice.
+//
+// Single group g pairs the heavier half of the list (dealt from its front)
+// with the lighter half (from its back), G / 2 problems each.  With G = 8 the
+// group is the whole compute unit (eight 256-VGPR waves, two per SIMD), and
+// the waves that share a SIMD share its issue slots: each wave reads its SIMD
+// from the HW_ID register, and the k-th heaviest problem of the group goes to
+// the first wave of the k-th SIMD, the k-th lightest to its second wave, so
+// that every SIMD carries about the same work.  Any placement still gives
+// every wave one distinct slot (slots ordered by rank within the SIMD, then
+// by SIMD).
+template <int W, int G>
+__global__ void __launch_bounds__(G * kWave, W == 4 ? 4 : 2)
 sinkhorn_reg_kernel(SkParams p, const int32_t* __restrict__ multi, const int32_t* __restrict__ single,
                     const int32_t* __restrict__ counts) {
   extern __shared__ __attribute__((aligned(16))) int32_t wl[];
+  __shared__ int32_t simd_of[G];
   const int32_t n_multi = counts[0], n_single = counts[1];
   const int32_t k = blockIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (k < n_multi) {
-    wave_problem<W, W>(p, multi[k], wl);
+    if (w < W) wave_problem<W, W>(p, multi[k], wl);
     return;
   }
-  // single group g pairs the heavier half of the list (dealt from its front)
-  // with the lighter half (from its back), W / 2 problems each, so that the
-  // group's waves carry similar total work
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t g = k - n_multi, F = ((int64_t)n_single + 1) / 2;
-  const bool front = w < W / 2;
-  const int64_t j = front ? g * (W / 2) + w : (int64_t)n_single - 1 - (g * (W / 2) + (w - W / 2));
+  if (g * (G / 2) >= F) return;  // past the last group (uniform over the workgroup)
+  int slot = w;
+  if constexpr (G > W) {
+    // HW_ID bits 5:4 hold the SIMD of the wave
+    const int simd = (int)__builtin_amdgcn_s_getreg((1 << 11) | (4 << 6) | 4);
+    if ((threadIdx.x & (kWave - 1)) == 0) simd_of[w] = simd;
+    __syncthreads();
+    auto rank = [&](int u) {
+      int r = 0;
+      for (int t = 0; t < u; ++t) r += simd_of[t] == simd_of[u];
+      return r;
+    };
+    const int mr = rank(w);
+    int pos = 0;
+    for (int u = 0; u < G; ++u) {
+      const int ru = rank(u);
+      pos += ru < mr || (ru == mr && simd_of[u] < simd);
+    }
+    slot = __builtin_amdgcn_readfirstlane(pos);
+  }
+  const bool front = slot < G / 2;
+  const int kk = front ? slot : slot - G / 2;
+  const int64_t j = front ? g * (G / 2) + kk : (int64_t)n_single - 1 - (g * (G / 2) + kk);
   if (front ? j < F : (j >= F && j < n_single))
     wave_problem<1, W>(p, single[j], wl + (size_t)w * (single_lds_bytes(p.R) / 4));
 }
@@ -1440,16 +1473,16 @@ sinkhorn_wide_kernel(SkParams p, const int32_t* __restrict__ list, const int32_t
   }
 }
 
-template <int W>
+template <int W, int G>
 taot_status launch_reg_kernel(const SkParams& p, const int32_t* multi, const int32_t* single, const int32_t* counts,
                               hipStream_t stream) {
-  const size_t lds = std::max(wave_lds_bytes(p.R, W), (size_t)W * single_lds_bytes(p.R));
-  if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_reg_kernel<W>,
+  const size_t lds = std::max(wave_lds_bytes(p.R, W), (size_t)G * single_lds_bytes(p.R));
+  if (lds > 65536 && hipFuncSetAttribute((const void*)sinkhorn_reg_kernel<W, G>,
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return TAOT_ERR_LAUNCH;
   // one workgroup per item at most: B is an upper bound on the items
-  hipLaunchKernelGGL(sinkhorn_reg_kernel<W>, dim3((unsigned)p.B), dim3(W * kWave), lds, stream, p, multi, single,
-                     counts);
+  hipLaunchKernelGGL((sinkhorn_reg_kernel<W, G>), dim3((unsigned)p.B), dim3(G * kWave), lds, stream, p, multi,
+                     single, counts);
   return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
 }
 
@@ -1472,8 +1505,11 @@ taot_status launch_wave(const SkParams& p, int32_t* cls, int32_t* lists, int32_t
   hipLaunchKernelGGL(wave_order_kernel, dim3(1), dim3(kSkThreads), 0, stream, cls, p.B, W, multi, single, wide,
                      counts);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  const taot_status st = W == 4 ? launch_reg_kernel<4>(p, multi, single, counts, stream)
-                                : launch_reg_kernel<2>(p, multi, single, counts, stream);
+  // two-wave shapes run in eight-wave groups while their LDS slices fit 64 KB
+  const bool g8 = 8 * single_lds_bytes(p.R) <= 65536;
+  const taot_status st = W == 4 ? launch_reg_kernel<4, 4>(p, multi, single, counts, stream)
+                         : g8   ? launch_reg_kernel<2, 8>(p, multi, single, counts, stream)
+                                : launch_reg_kernel<2, 2>(p, multi, single, counts, stream);
   if (st != TAOT_OK) return st;
   // the wide problems: at most one workgroup per compute unit at a time
   const size_t lds = wide_lds_bytes(p.R);
