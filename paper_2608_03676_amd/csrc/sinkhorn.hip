@@ -818,6 +818,360 @@ __device__ __forceinline__ void wave_solve(const SkParams& p, int64_t pb, int32_
 #undef CV
 }
 
+// ---------------------------------------------------------------------------
+// One-wave layout with the columns folded over the two half-waves.  Lane l
+// sits in half h = l >> 5 at column lane cl = l & 31 and owns compact columns
+// cl, cl + 32, ... (CPL of them, so the block is padded to 32-column rather
+// than 64-column steps); chunk q of 8 rows keeps rows 8q .. 8q+3 in half 0
+// and 8q+4 .. 8q+7 in half 1, four Kt values per column.
+//   row half-step:    per-lane partial sums of the half's 4 rows, then the
+//                     transposed butterfly over the 32 lanes of each half
+//                     (permlane16 swap, then DPP) leaves the total of row
+//                     8q + (l >> 3) in lane l, as in the full-wave layout.
+//   column half-step: partial sums over the half's rows; one permlane32 swap
+//                     and an add per pair of columns (c, c + P) leave the
+//                     totals of column c in half 0 and of column c + P in
+//                     half 1, each half derives those scalings, and a second
+//                     swap hands every lane both.
+// Against the full-wave layout this drops one swap level from every row
+// chunk (the halves' column partials meet once per iteration instead) and
+// pads the columns less.
+
+// Sums 4 per-lane values over the 32 lanes of each half-wave; lane l ends
+// with the total of value (l >> 3) & 3 of its half.  The steps pair lanes
+// l ^ 16 (permlane16 swap), l <-> 15 - l (row_mirror), l <-> l ^ 7
+// (row_half_mirror), l ^ 2 and l ^ 1 (quad_perm).
+__device__ __forceinline__ float reduce4(float (&p)[4], int lane) {
+#pragma unroll
+  for (int k = 0; k < 2; ++k) { swap16(p[k], p[k + 2]); p[k] = p[k] + p[k + 2]; }
+  const bool b3 = lane & 8;
+  const float keep = b3 ? p[1] : p[0];
+  const float send = b3 ? p[0] : p[1];
+  float y = keep + dpp<0x140>(send);  // row_mirror
+  y = y + dpp<0x141>(y);              // row_half_mirror
+  y = y + dpp<0x4E>(y);               // quad_perm [2,3,0,1]
+  y = y + dpp<0xB1>(y);               // quad_perm [1,0,3,2]
+  return y;
+}
+// Max and sum over the 32 lanes of each half-wave (bitwise the same in every
+// lane of the half).
+__device__ __forceinline__ float half_max(float x) {
+  x = fmaxf(x, dpp<0xB1>(x));
+  x = fmaxf(x, dpp<0x4E>(x));
+  x = fmaxf(x, dpp<0x141>(x));
+  x = fmaxf(x, dpp<0x140>(x));
+  float y = x;
+  swap16(x, y);
+  return fmaxf(x, y);
+}
+__device__ __forceinline__ float half_sum(float x) {
+  x = x + dpp<0xB1>(x);
+  x = x + dpp<0x4E>(x);
+  x = x + dpp<0x141>(x);
+  x = x + dpp<0x140>(x);
+  float y = x;
+  swap16(x, y);
+  return x + y;
+}
+// Both halves' values of v: a gets half 0's, b half 1's, in every lane.
+__device__ __forceinline__ void halves_both(float v, float& a, float& b) {
+  a = v;
+  b = v;
+  swap32(a, b);
+}
+
+// Chunks of 8 rows the folded layout holds for CPL columns per lane: 8 up to
+// 128 columns, 6 beyond (the two-wave kernel runs a problem of more than 128
+// columns on one wave only up to 6 chunks), at most 192 Kt registers.
+__host__ __device__ constexpr int half_max_c8(int cpl) { return cpl <= 4 ? 8 : 6; }
+
+// Iterations and outputs of one problem of c8 row chunks on this wave alone,
+// in the folded layout; the caller has filled sAl and the first-update
+// potentials Fl.  Gc [256] holds the column potentials by compact column, Sl
+// [64][4] the demands of each lane's folded columns.
+template <int CPL>
+__device__ __forceinline__ void half_solve(const SkParams& p, int64_t pb, int32_t nh, int32_t nc, int c8,
+                                           const int32_t* cpos, const int32_t* hpos, const int32_t* cidx,
+                                           const int32_t* hidx, const float* sAl, float* Fl, float* ul, float* Gc,
+                                           float* Sl, float kappa) {
+  constexpr int MC = half_max_c8(CPL);  // chunks the registers hold; chunks q >= c8 are skipped
+  constexpr int P = (CPL + 1) / 2;      // folded column pairs (c, c + P)
+  const int lane = threadIdx.x & (kWave - 1);
+  const int h = lane >> 5, cl = lane & 31;
+  const int32_t R = p.R;
+  const float* bd = p.b + pb * R;
+  const float* Cb = p.C + pb * p.C_stride;
+#define HV(c) (cl + 32 * (c) < nc)                 // column c of the lane exists
+#define HJ(c) (HV(c) ? cidx[cl + 32 * (c)] : 0)   // its rank
+#define FV(c) ((c) + P * h < CPL && cl + 32 * ((c) + P * h) < nc)  // folded column c of the lane exists
+#define RV(q) (8 * (q) + (lane >> 3) < nh)        // the row the lane holds after reduce4
+#define HR(q, r) (8 * (q) + 4 * h + (r))           // row r of chunk q in the lane's half
+#define GL(c) Gc[cl + 32 * (c)]
+  float* Sw = Sl + lane * 4;
+
+  float K[4 * MC][CPL];
+  float v[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    v[c] = HV(c) ? 1.f : 0.f;
+    GL(c) = 0.f;  // both halves store the same value
+  }
+  // padding columns take demand 1, and padding rows supply 1 below, so that
+  // their scalings come out as exactly 1 (in range, and Kt is 0 there)
+#pragma unroll
+  for (int c = 0; c < P; ++c) Sw[c] = FV(c) ? bd[cidx[cl + 32 * (c + P * h)]] : 1.f;
+  auto demands = [&](float (&sB)[P]) {
+#pragma unroll
+    for (int c = 0; c < P; ++c) sB[c] = Sw[c];
+  };
+  // Kt of the lane's rows from the potentials (after the exact log-domain
+  // update of each row's potential when row_update is set).  Rows past nh
+  // take the cost row of row 0 and a zero Kt.
+  auto build = [&](bool row_update) {
+#pragma unroll
+    for (int q = 0; q < MC; ++q) {
+      if (q >= c8) break;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int gi = HR(q, r);
+        const bool rv = gi < nh;
+        const int gs = rv ? gi : 0;
+        const float* crow = Cb + (int64_t)hidx[gs] * R;
+        float cc[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) cc[c] = HV(c) ? crow[HJ(c)] * kappa : 0.f;
+        float fi;
+        if (row_update) {
+          float t[CPL];
+          float mx = -INFINITY;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            t[c] = HV(c) ? (GL(c) + flog2(v[c])) - cc[c] : -INFINITY;
+            mx = fmaxf(mx, t[c]);
+          }
+          mx = half_max(mx);
+          float sum = 0.f;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) sum += HV(c) ? fexp2(t[c] - mx) : 0.f;
+          sum = half_sum(sum);
+          fi = flog2(sAl[gs]) - (mx + flog2(sum));
+          if (rv && cl == 0) Fl[gi] = fi;
+        } else {
+          fi = Fl[gs];
+        }
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) K[4 * q + r][c] = rv && HV(c) ? fexp2((fi + GL(c)) - cc[c]) : 0.f;
+      }
+    }
+  };
+
+#define UST(q, val) \
+  if ((lane & 7) == 0) ul[8 * (q) + (lane >> 3)] = (val)
+#pragma unroll
+  for (int q = 0; q < MC; ++q)
+    if (q < c8) UST(q, RV(q) ? 1.f : 0.f);
+  float sAq[MC];
+#pragma unroll
+  for (int q = 0; q < MC; ++q) sAq[q] = RV(q) ? sAl[8 * q + (lane >> 3)] : 1.f;
+
+  int32_t it = 1;
+  bool skip_row = true;
+  bool row_update = false;
+  for (;;) {
+    build(row_update);
+    if (row_update) {
+#pragma unroll
+      for (int q = 0; q < MC; ++q)
+        if (q < c8) UST(q, RV(q) ? 1.f : 0.f);
+      row_update = false;
+    }
+    bool done = false, col_fail = false;
+    for (;;) {
+      if (!skip_row) {
+        // ---- row half-step: u_i = s~_i / sum_c Kt_ic v_c ----------------------------
+        uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+        for (int q = 0; q < MC; ++q) {
+          if (q >= c8) break;
+          float pp[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float acc = K[4 * q + r][0] * v[0];
+#pragma unroll
+            for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[4 * q + r][c], v[c], acc);
+            pp[r] = acc;
+          }
+          const float y = reduce4(pp, lane);  // all lanes take part
+          const float un = sAq[q] * frcp(RV(q) ? y : 1.f);
+          const uint32_t bits = __float_as_uint(un);
+          lo = bits < lo ? bits : lo;
+          hi = bits > hi ? bits : hi;
+          UST(q, un);
+        }
+        const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
+        if (__ballot(fail) != 0) {
+          row_update = true;
+          skip_row = true;
+          break;
+        }
+      }
+      skip_row = false;
+      // ---- column half-step: v_c = d_c / sum_i u_i Kt_ic --------------------------------
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      float x[CPL], x2[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) x[c] = x2[c] = 0.f;
+      float4 ua = *reinterpret_cast<const float4*>(ul + 4 * h);
+#pragma unroll
+      for (int q = 0; q < MC; ++q) {
+        if (q >= c8) break;
+        float4 na = ua;  // the next chunk's scalings (past c8: unused)
+        if (q + 1 < MC) na = *reinterpret_cast<const float4*>(ul + 8 * (q + 1) + 4 * h);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          x[c] = __builtin_fmaf(ua.x, K[4 * q][c], x[c]);
+          x2[c] = __builtin_fmaf(ua.y, K[4 * q + 1][c], x2[c]);
+          x[c] = __builtin_fmaf(ua.z, K[4 * q + 2][c], x[c]);
+          x2[c] = __builtin_fmaf(ua.w, K[4 * q + 3][c], x2[c]);
+        }
+        ua = na;
+      }
+      // fold: register c of half 0 gets column c, of half 1 column c + P
+      float xf[P];
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        float a = x[c] + x2[c];
+        float b = c + P < CPL ? x[c + P] + x2[c + P] : 0.f;
+        swap32(a, b);
+        xf[c] = a + b;
+      }
+      float sB[P];
+      demands(sB);
+      uint32_t clo = 0xFFFFFFFFu, chi = 0u;
+#pragma unroll
+      for (int c = 0; c < P; ++c) {
+        const float vn = sB[c] * frcp(FV(c) ? xf[c] : 1.f);
+        const uint32_t bits = __float_as_uint(vn);
+        clo = bits < clo ? bits : clo;
+        chi = bits > chi ? bits : chi;
+        float a, b;
+        halves_both(vn, a, b);
+        v[c] = a;
+        if (c + P < CPL) v[c + P] = b;
+      }
+      col_fail = __ballot(!(clo >= __float_as_uint(kLo) && chi <= __float_as_uint(kHi))) != 0;
+      done = it == p.iters;
+      if (!done) ++it;
+      if (col_fail || done) break;
+    }
+    if (col_fail) {
+      // exact log-domain update of every column (both halves alike), absorbed
+      // into G; Kt is rebuilt at the top of the loop, or below after the last
+      // iteration
+      psync<1>();
+      float mx[CPL], sum[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) { mx[c] = -INFINITY; sum[c] = 0.f; }
+      for (int32_t i = 0; i < nh; ++i) {
+        const float fi = Fl[i] + flog2(ul[i]);
+        const float* crow = Cb + (int64_t)hidx[i] * R;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          if (HV(c)) {
+            const float t = fi - crow[HJ(c)] * kappa;
+            const float m2 = fmaxf(mx[c], t);
+            sum[c] = sum[c] * fexp2(mx[c] - m2) + fexp2(t - m2);
+            mx[c] = m2;
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        GL(c) = HV(c) ? flog2(bd[HJ(c)]) - (mx[c] + flog2(sum[c])) : 0.f;
+        v[c] = HV(c) ? 1.f : 0.f;
+      }
+      psync<1>();
+      if (done) {
+        build(false);
+        break;
+      }
+      continue;
+    }
+    if (done) break;
+  }
+
+  // ---- plan, column cap, outputs -------------------------------------------------
+  psync<1>();
+  const bool colcap = !(p.flags & TAOT_SK_NO_COLCAP);
+  float fac[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) fac[c] = 1.f;
+  if (colcap) {
+    float cs[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) cs[c] = 0.f;
+#pragma unroll
+    for (int q = 0; q < MC; ++q) {
+      if (q >= c8) break;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float ui = ul[HR(q, r)];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) cs[c] += ui * K[4 * q + r][c] * v[c];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      float a, b;
+      halves_both(cs[c], a, b);
+      const float tot = a + b;
+      fac[c] = HV(c) ? fminf(1.f, bd[HJ(c)] / (tot + 1e-12f)) : 1.f;
+    }
+  }
+  if (p.T) {
+    float* Tb = p.T + pb * R * R;
+    for (int32_t i = 0; i < R; ++i) {
+      const bool hot = hpos[i] >= 0;
+      for (int32_t j = lane; j < R; j += kWave)
+        if (!hot || cpos[j] < 0) Tb[(int64_t)i * R + j] = 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < MC; ++q) {
+      if (q >= c8) break;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int gi = HR(q, r);
+        if (gi < nh) {
+          const float ui = ul[gi];
+          float* trow = Tb + (int64_t)hidx[gi] * R;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c)
+            if (HV(c)) trow[HJ(c)] = ui * K[4 * q + r][c] * (v[c] * fac[c]);
+        }
+      }
+    }
+  }
+  const float to_nat = p.eps * kLn2;
+  for (int32_t i = lane; i < R; i += kWave) {
+    const int32_t ih = hpos[i];
+    if (p.f) p.f[pb * R + i] = ih >= 0 ? (Fl[ih] + flog2(ul[ih])) * to_nat : -INFINITY;
+    if (p.g && cpos[i] < 0) p.g[pb * R + i] = -INFINITY;
+  }
+  if (p.g && h == 0) {
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+      if (HV(c)) p.g[pb * R + HJ(c)] = (GL(c) + flog2(v[c])) * to_nat;
+  }
+  if (lane == 0 && p.status) p.status[pb] = 0u;
+#undef UST
+#undef GL
+#undef HR
+#undef RV
+#undef FV
+#undef HJ
+#undef HV
+}
+
 // The solver instance of wave wv (uniform over the wave).
 template <int CPL, int C8W, int NW>
 __device__ __forceinline__ void solve_on_wave(int wv, const SkParams& p, int64_t pb, int32_t nh, int32_t nc,
@@ -923,9 +1277,27 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
     if (gt == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
     return;
   }
-  const int cpl = nc <= 64 ? 1 : nc <= 128 ? 2 : 4;
-  const int c8w = ((nh + 7) / 8 + NW - 1) / NW;
-  switch (cpl * 16 + c8w) {
+  if constexpr (NW == 1 && W == 2) {
+    // one wave alone: the folded layout (every single class of the two-wave
+    // kernel fits it)
+    const int cph = (nc + 31) / 32, c8 = (nh + 7) / 8;
+    switch (cph) {
+#define TAOT_HALF_CASE(CPL_)                                                                          \
+  case CPL_:                                                                                          \
+    if (c8 >= 1 && c8 <= half_max_c8(CPL_)) {                                                         \
+      half_solve<CPL_>(p, pb, nh, nc, c8, cpos, hpos, cidx, hidx, sAl, Fl, ul, Gall, Sall, kappa);    \
+      return;                                                                                         \
+    }                                                                                                 \
+    break;
+      TAOT_HALF_CASE(1) TAOT_HALF_CASE(2) TAOT_HALF_CASE(3) TAOT_HALF_CASE(4)
+      TAOT_HALF_CASE(5) TAOT_HALF_CASE(6) TAOT_HALF_CASE(7) TAOT_HALF_CASE(8)
+#undef TAOT_HALF_CASE
+      default: break;
+    }
+  } else {
+    const int cpl = nc <= 64 ? 1 : nc <= 128 ? 2 : 4;
+    const int c8w = ((nh + 7) / 8 + NW - 1) / NW;
+    switch (cpl * 16 + c8w) {
 #define TAOT_WAVE_CASE(CPL_, C8W_)                                                                    \
   case CPL_ * 16 + C8W_:                                                                              \
     if constexpr (shape_ok(W, NW, CPL_, C8W_))                                                        \
@@ -935,10 +1307,11 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
 #define TAOT_WAVE_CPL(CPL_)                                                                           \
   TAOT_WAVE_CASE(CPL_, 1) TAOT_WAVE_CASE(CPL_, 2) TAOT_WAVE_CASE(CPL_, 3) TAOT_WAVE_CASE(CPL_, 4)      \
   TAOT_WAVE_CASE(CPL_, 5) TAOT_WAVE_CASE(CPL_, 6) TAOT_WAVE_CASE(CPL_, 7) TAOT_WAVE_CASE(CPL_, 8)
-    TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2) TAOT_WAVE_CPL(4)
+      TAOT_WAVE_CPL(1) TAOT_WAVE_CPL(2) TAOT_WAVE_CPL(4)
 #undef TAOT_WAVE_CPL
 #undef TAOT_WAVE_CASE
-    default: break;
+      default: break;
+    }
   }
 }
 
