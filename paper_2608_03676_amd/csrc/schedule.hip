@@ -767,17 +767,27 @@ __device__ __forceinline__ void list_append(bool flag, int32_t item, int32_t* li
   const uint64_t m = __ballot(flag);
   int32_t base = 0;
   if (lane == 0 && m) base = atomicAdd(count, __popcll(m));
-  base = __shfl(base, 0, kWave);
+  base = __builtin_amdgcn_readlane(base, 0);
   if (flag) list[base + __popcll(m & ((1ull << lane) - 1ull))] = item;
 }
 
+template <int CTRL>
+__device__ __forceinline__ int32_t dpp_i32(int32_t x) {
+  // every lane has a source lane for the patterns used here
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xf, 0xf, true);
+}
+// Max over the 64 lanes without LDS round trips: DPP steps within each
+// 16-lane row, then the permlane16 and permlane32 swaps across rows.  All
+// lanes must call it.
 __device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const int32_t u = __shfl_xor(v, o, kWave);
-    v = u > v ? u : v;
-  }
-  return v;
+  v = max(v, dpp_i32<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp_i32<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp_i32<0x141>(v));  // row_half_mirror
+  v = max(v, dpp_i32<0x140>(v));  // row_mirror
+  const auto r16 = __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+  v = max((int32_t)r16[0], (int32_t)r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false);
+  return max((int32_t)r32[0], (int32_t)r32[1]);
 }
 
 // One problem per workgroup of CF::kT threads; thread i bids for list entries
