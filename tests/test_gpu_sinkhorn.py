@@ -221,6 +221,33 @@ def test_two_wave_rows(nh, nc, gpu):
         _check_against_oracle(a, b, C, eps, iters)
 
 
+def test_folded_shapes(gpu):
+    """Every one-wave shape of the two-wave kernel (SK_WAVES_1), whose single
+    problems fold their columns over the half-waves: 1..8 columns per lane
+    (cold ranks up to 32 per column, exact multiples and ragged), every
+    chunk count the layout holds (ragged hot ranks), and past it the
+    two-wave problems (more than 48 hot and 128 cold ranks)."""
+    rng = np.random.default_rng(23)
+    R = 320
+    shapes = []
+    for cpl in range(1, 9):
+        for c8 in range(1, 9):
+            nc = 32 * cpl - (int(rng.integers(1, 31)) if c8 % 2 else 0)
+            nh = 8 * c8 - int(rng.integers(0, 8))
+            shapes.append((nh, nc))
+    B = len(shapes)
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p, (nh, nc) in enumerate(shapes):
+        perm = rng.permutation(R)
+        a[p, perm[:nh]] = rng.integers(1, 4000, size=nh)
+        b[p, perm[nh:nh + nc]] = rng.multinomial(int(a[p].sum()), np.full(nc, 1.0 / nc)) + 1
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32))
+    for eps, iters in ((0.08, 200), (0.02, 120)):
+        print(f"[sinkhorn parity] folded shapes eps={eps}", flush=True)
+        _check_against_oracle(a, b, C, eps, iters, taot.SK_WAVES_1)
+
+
 @pytest.mark.parametrize("flags", [0, taot.SK_WAVES_1])
 def test_register_shapes(flags, gpu):
     """One problem of every register class (1, 2 or 4 columns per lane x 1..8
