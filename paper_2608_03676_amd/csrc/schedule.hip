@@ -454,7 +454,8 @@ struct LdsSmall {
   static constexpr int kDC = 64;     // distinct slot experts per problem
   static constexpr int kPL = 11;     // count bit-planes: counts <= R*K <= 1024
   static constexpr int kMaxS = 1024; // R*K
-  static constexpr int kNEC = 256;   // candidate experts (spill > 0) in LDS
+  static constexpr int kNEC = 128;   // candidate experts (spill > 0) in LDS
+  static constexpr int kWavesPerEU = 8;  // large batches: eight problems per compute unit (20 KB of LDS each at R = 256, K = 2)
 };
 struct LdsLarge {
   static constexpr int kT = 1024;
@@ -464,6 +465,7 @@ struct LdsLarge {
   static constexpr int kPL = 13;     // counts <= R*K <= 4096
   static constexpr int kMaxS = 4096;
   static constexpr int kNEC = 1024;
+  static constexpr int kWavesPerEU = 1;  // one problem per compute unit in any case
 };
 // list entries pack (slot, slot-expert index, host structure): 12 + 7 + 7 bits
 constexpr int kItemSlotBits = 12, kItemExpertBits = 7;
@@ -646,7 +648,7 @@ auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restr
 template <class CF>
 struct LdsState {
   // both phases
-  int32_t* slot_ec;   // [S] candidate index of the slot's expert or -1
+  int16_t* slot_ec;   // [S] candidate index of the slot's expert or -1
   int32_t* amt;       // [S] slot amounts (Phase 2), tokens still planned (Phase 3)
   int32_t* ce;        // [NEC] candidate experts (spill > 0), ascending
   // Phase 2
@@ -655,7 +657,7 @@ struct LdsState {
   // Phase 3 (aliases the Phase-2 region)
   double* price; uint32_t* rkey; int32_t* work;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
-  int32_t* cn; double* cv; int32_t* cvr; uint32_t* cw; uint64_t* cm;
+  int8_t* cn; double* cv; int32_t* cvr; uint32_t* cw; uint64_t* cm;
   size_t bytes;
 };
 
@@ -670,7 +672,7 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
     off = (off + bytes + 15) & ~(size_t)15;
     return q;
   };
-  w.slot_ec = (int32_t*)take(4 * S1);
+  w.slot_ec = (int16_t*)take(2 * S1);
   w.amt = (int32_t*)take(4 * S1);
   w.ce = (int32_t*)take(4 * N_);
   const size_t split = off;
@@ -681,11 +683,11 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   const size_t end2 = off;
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
-  w.work = (int32_t*)take(2 * 4 * S1);
+  w.work = (int32_t*)take(4 * S1);
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(4 * DC);
   w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
   w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * CF::kPL * TW);
-  w.cn = (int32_t*)take(4 * SC);
+  w.cn = (int8_t*)take(SC);
   w.cv = (double*)take(8 * SC * kTierMax); w.cvr = (int32_t*)take(4 * SC * kTierMax);
   w.cw = (uint32_t*)take(4 * SC * kTierMax);
   w.cm = (uint64_t*)take(8 * SC * kTierMax * TW);
@@ -791,9 +793,11 @@ __device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
 }
 
 // One problem per workgroup of CF::kT threads; thread i bids for list entries
-// i, i + kT, ... (SPL of them).
-template <class CF, int SPL>
-__global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
+// i, i + kT, ... (SPL of them).  WPE waves per SIMD bound the registers: a
+// batch that fills the chip needs all its problems resident at once, a
+// smaller one is better served without the register cap.
+template <class CF, int SPL, int WPE>
+__global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp) {
   constexpr int NT = CF::kT, NW = NT / kWave, TW = CF::kTW;
   extern __shared__ __attribute__((aligned(16))) char lds_dyn[];
   __shared__ int32_t wave_cnt[NW];
@@ -963,7 +967,7 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
           L.prop_e[w] = -1;  // matched ranks stop proposing
           L.assigned[w * K + k] = ec;
           const int32_t s = L.cr[w] * K + k;
-          L.slot_ec[s] = ec;
+          L.slot_ec[s] = (int16_t)ec;
           L.amt[s] += g;
           se[s] = L.ce[ec];
         }
@@ -1027,7 +1031,7 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
     const bool f = ec >= 0 && L.amt[s] > 0;
     const int32_t item =
         f ? s | (L.dmap[ec] << kItemSlotBits) | (wp.sidx[s / K] << (kItemSlotBits + kItemExpertBits)) : 0;
-    list_append(f, item, L.work + S, &sh_nw[1]);  // the list of round 1 (odd)
+    list_append(f, item, L.work, &sh_nw[1]);  // the list of round 1 (odd)
   }
   for (int32_t r = tid; r < R; r += NT) {
     L.price[r] = 0.0;
@@ -1037,7 +1041,7 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
   }
   for (int32_t q = tid; q < CF::kPL * TW; q += NT) L.planes[q] = 0ull;
   const int32_t ns = wp.hdr[0];
-  for (int32_t q = tid; q < ns; q += NT) L.cn[q] = wp.cn[q];
+  for (int32_t q = tid; q < ns; q += NT) L.cn[q] = (int8_t)wp.cn[q];
   for (int32_t q = tid; q < ns * kTierMax; q += NT) {
     L.cv[q] = wp.cv[q];
     L.cvr[q] = wp.cvr[q];
@@ -1062,7 +1066,9 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
   // Every bid names a rank, which then serves its best bidder with a positive
   // amount; so every open slot with a valid rank bids again in every round,
   // and the auction keeps a list of them.  A round is two steps, one barrier
-  // each, with the list and the rank keys in two buffers by round parity:
+  // each, with the rank keys in two buffers by round parity and the list in
+  // one (every thread has read its items before the barrier that precedes
+  // the rewrite):
   //   X: each listed slot bids and posts its key to the rank it bid for;
   //   Y: the same thread moves tokens if its slot won, and keeps the slot on
   //      next round's list while it still plans tokens.
@@ -1074,7 +1080,7 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
   for (int64_t t = 1; t <= tmax; ++t) {
     const int cur = (int)(t & 1), prv = cur ^ 1;
     uint32_t* rk = L.rkey + cur * R;
-    const int32_t* list = L.work + cur * S;
+    const int32_t* list = L.work;
     const int32_t nw = sh_nw[cur];
     const int32_t maxc = sh_maxc;
     const int32_t nplanes = maxc > 0 ? 32 - __builtin_clz((uint32_t)maxc) : 0;
@@ -1243,7 +1249,7 @@ __global__ void __launch_bounds__(CF::kT) schedule_lds_kernel(LdsParams wp) {
         }
         keep = a > 0;
       }
-      list_append(keep, item[i], L.work + prv * S, &sh_nw[prv]);
+      list_append(keep, item[i], L.work, &sh_nw[prv]);
     }
     newmax = wave_max_i32(newmax);
     if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
@@ -1315,12 +1321,12 @@ SchWs carve_sched(void* ws, int32_t B, int32_t R, int32_t E, int32_t K) {
   return w;
 }
 
-template <class CF, int SPL>
+template <class CF, int SPL, int WPE>
 taot_status launch_lds_kernel(const LdsParams& wp, int32_t B, size_t lds, hipStream_t stream) {
-  if (lds > 65536 && hipFuncSetAttribute((const void*)schedule_lds_kernel<CF, SPL>,
+  if (lds > 65536 && hipFuncSetAttribute((const void*)schedule_lds_kernel<CF, SPL, WPE>,
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL((schedule_lds_kernel<CF, SPL>), dim3((unsigned)B), dim3(CF::kT), lds, stream, wp);
+  hipLaunchKernelGGL((schedule_lds_kernel<CF, SPL, WPE>), dim3((unsigned)B), dim3(CF::kT), lds, stream, wp);
   return hipGetLastError() == hipSuccess ? TAOT_OK : TAOT_ERR_LAUNCH;
 }
 
@@ -1356,9 +1362,22 @@ taot_status launch_lds_path(const SchParams& p, const SchWs& w, int32_t B, int32
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   const LdsParams wp{p, w.sidx, w.cn, w.cv, w.cvr, w.cw, w.cm, w.hdr, w.fallback, w.nprime, NEC};
   taot_status st;
-  if (S <= CF::kT) st = launch_lds_kernel<CF, 1>(wp, B, slds, stream);
-  else if (S <= 2 * CF::kT) st = launch_lds_kernel<CF, 2>(wp, B, slds, stream);
-  else st = launch_lds_kernel<CF, 4>(wp, B, slds, stream);
+  // a batch of more problems than fit six to a compute unit takes the
+  // register-capped build, which can hold CF::kWavesPerEU per SIMD
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return TAOT_ERR_LAUNCH;
+  const bool cap = (int64_t)B > (int64_t)6 * cus;
+  if (S <= CF::kT)
+    st = cap ? launch_lds_kernel<CF, 1, CF::kWavesPerEU>(wp, B, slds, stream)
+             : launch_lds_kernel<CF, 1, 1>(wp, B, slds, stream);
+  else if (S <= 2 * CF::kT)
+    st = cap ? launch_lds_kernel<CF, 2, CF::kWavesPerEU>(wp, B, slds, stream)
+             : launch_lds_kernel<CF, 2, 1>(wp, B, slds, stream);
+  else
+    st = cap ? launch_lds_kernel<CF, 4, CF::kWavesPerEU>(wp, B, slds, stream)
+             : launch_lds_kernel<CF, 4, 1>(wp, B, slds, stream);
   launched = st == TAOT_OK;
   return st;
 }
