@@ -654,6 +654,7 @@ struct LdsState {
   // Phase 2
   int32_t* hce; double* den; int32_t* cr; int32_t* spare_p; int32_t* matched; int32_t* prop_e;
   double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
+  int32_t* qbest;  // [R] q = min(spill, spare) of each cold rank's standing proposal
   // Phase 3 (aliases the Phase-2 region)
   double* price; uint32_t* rkey; int32_t* work;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
@@ -680,6 +681,7 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   w.spare_p = (int32_t*)take(4 * R_); w.matched = (int32_t*)take(4 * R_); w.prop_e = (int32_t*)take(4 * R_);
   w.prop_s = (double*)take(8 * R_); w.assigned = (int32_t*)take(4 * S1);
   w.spill_p = (int32_t*)take(4 * N_); w.ekey = (uint64_t*)take(8 * N_); w.ewin = (int32_t*)take(4 * N_);
+  w.qbest = (int32_t*)take(4 * R_);
   const size_t end2 = off;
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
@@ -900,9 +902,22 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       bool proposed = false;
       for (int32_t rc = tid; rc < nc; rc += NT) {
         if (L.matched[rc]) continue;
-        int32_t best = -1;
-        double bs = -INFINITY;
         const int32_t sp = L.spare_p[rc];
+        // A losing proposal stands while its expert's q = min(spill, spare) is
+        // unchanged: within a round of k no score rises (spill only falls; an
+        // unmatched rank's spare, its taken set and the other terms are
+        // fixed), so that expert is still the best, and still the lowest
+        // index among the best.  Otherwise the rank scans again.
+        const int32_t pe = L.prop_e[rc];
+        if (pe >= 0) {
+          const int32_t sl = L.spill_p[pe];
+          if ((sl < sp ? sl : sp) == L.qbest[rc]) {
+            proposed = true;
+            continue;
+          }
+        }
+        int32_t best = -1, bq = 0;
+        double bs = -INFINITY;
         if (sp > 0) {
           const int32_t r = L.cr[rc];
           const int32_t* asg = L.assigned + rc * K;
@@ -937,12 +952,13 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
               const double tn = (double)tt[u] / L.den[hh[u]];
               const double t2 = a2 * tn;
               const double score = (q + t1) + t2;
-              if (score > bs) { bs = score; best = ec; }
+              if (score > bs) { bs = score; best = ec; bq = sl[u] < sp ? sl[u] : sp; }
             }
           }
         }
         L.prop_e[rc] = best;
         L.prop_s[rc] = bs;
+        L.qbest[rc] = bq;
         proposed |= best >= 0;
       }
       if (!block_or<NT>(proposed, flagbuf, parity)) break;  // nothing can change any more
