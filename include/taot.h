@@ -63,6 +63,11 @@ typedef enum {
                                      default small batches spread a problem over
                                      up to four waves)                              */
 
+/* round_schedule flags: ablations of the Phase-2 score (Sec. A.3 discusses
+ * the contribution of each term).  Phase 3 is unaffected. */
+#define TAOT_SCH_NO_TOPO 0x1u  /* drop the topology term alpha * Bpref (score q + 0.1 alpha Tn) */
+#define TAOT_SCH_NO_FLOW 0x2u  /* drop the flow-hint term 0.1 * alpha * Tn (score q + alpha Bpref) */
+
 /* Returns a static description of a status code (host, never NULL). */
 const char* taot_status_string(taot_status s);
 
@@ -156,6 +161,8 @@ taot_status taot_sinkhorn_batched(const float* a, const float* b, int32_t B, int
  *   K       0..TAOT_MAX_SLOTS_PER_RANK guest slots per rank.
  *   price_step  finite, the auction's price increment.
  *   t_max   maximum auction rounds; <= 0 selects R*K*(R+1).
+ *   flags   TAOT_SCH_* (0 for the method as published): a dropped term
+ *           enters the score as +0 in the same evaluation order.
  * Outputs:
  *   slot_expert [B][R*K] int32   expert placed in slot s, -1 if empty.
  *   slot_amount [B][R*K] int64   tokens planned for slot s (A).
@@ -171,7 +178,7 @@ taot_status taot_round_schedule(const int32_t* n, const int64_t* spill, const in
                                 const int64_t* excess, const double* alpha, const int32_t* home,
                                 const float* T, const double* Bpref, const double* Bauct,
                                 int32_t B, int32_t R, int32_t E, int32_t K, double price_step,
-                                int64_t t_max, int32_t* slot_expert, int64_t* slot_amount,
+                                int64_t t_max, uint32_t flags, int32_t* slot_expert, int64_t* slot_amount,
                                 int32_t* X, int64_t* unfilled, int32_t* rounds_used,
                                 uint32_t* status, void* ws, size_t ws_bytes, void* stream);
 

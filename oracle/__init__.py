@@ -34,7 +34,7 @@ def lib():
                                       _P, _P, _P, _P, _P]
         L.oracle_topology_pref.argtypes = [_P, _I32, _P, _P]
         L.oracle_max_threads.argtypes = []
-        L.oracle_phase2.argtypes = [_P] * 7 + [_I32] * 4 + [_P] * 3
+        L.oracle_phase2.argtypes = [_P] * 7 + [_I32] * 4 + [ctypes.c_uint32] + [_P] * 3
         L.oracle_phase3.argtypes = [_P] * 4 + [_I32] * 4 + [_F64, _I64] + [_P] * 4
         L.oracle_metrics.argtypes = [_P] * 4 + [_I32] * 5 + [_F64] + [_P] * 5
         for f in (L.oracle_plan_loads, L.oracle_sinkhorn, L.oracle_topology_pref, L.oracle_phase2,
@@ -127,7 +127,10 @@ def topology_pref(C):
     return Bp, Ba
 
 
-def phase2(spill, spare, excess, alpha, home, T32, Bpref, K: int):
+SCH_NO_TOPO, SCH_NO_FLOW = 0x1, 0x2  # Phase-2 score ablations
+
+
+def phase2(spill, spare, excess, alpha, home, T32, Bpref, K: int, flags: int = 0):
     spill = _c(spill, np.int64)
     if spill.ndim == 1:
         spill, spare, excess = spill[None], _c(spare, np.int64)[None], _c(excess, np.int64)[None]
@@ -144,7 +147,7 @@ def phase2(spill, spare, excess, alpha, home, T32, Bpref, K: int):
     sa = np.empty((B, R * K), np.int64)
     used = np.empty(B, np.int32)
     rc = lib().oracle_phase2(spill.ctypes.data, spare.ctypes.data, excess.ctypes.data, alpha.ctypes.data,
-                             home.ctypes.data, T32.ctypes.data, Bpref.ctypes.data, B, R, E, K,
+                             home.ctypes.data, T32.ctypes.data, Bpref.ctypes.data, B, R, E, K, flags,
                              se.ctypes.data, sa.ctypes.data, used.ctypes.data)
     _check(rc, "oracle_phase2")
     return se, sa, used

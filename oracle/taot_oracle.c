@@ -315,8 +315,8 @@ int oracle_topology_pref(const float* C, int32_t R, double* Bpref, double* Bauct
 
 static void phase2_one(const int64_t* spill, const int64_t* spare, const int64_t* excess,
                        double alpha, const int32_t* home, const float* T, const double* Bpref,
-                       int32_t R, int32_t E, int32_t K, int32_t* slot_expert, int64_t* slot_amount,
-                       int32_t* inner_used) {
+                       int32_t R, int32_t E, int32_t K, uint32_t flags, int32_t* slot_expert,
+                       int64_t* slot_amount, int32_t* inner_used) {
   int64_t* spill_p = (int64_t*)malloc(sizeof(int64_t) * (size_t)E);
   int64_t* spare_p = (int64_t*)malloc(sizeof(int64_t) * (size_t)R);
   unsigned char* U = (unsigned char*)calloc((size_t)E * (size_t)R, 1);
@@ -348,10 +348,11 @@ static void phase2_one(const int64_t* spill, const int64_t* spare, const int64_t
           int32_t h = home[e];
           if (h == r || U[(int64_t)e * R + r] || spill_p[e] <= 0) continue;
           double q = (double)(spill_p[e] < spare_p[r] ? spill_p[e] : spare_p[r]);
-          double t1 = alpha * Bpref[(int64_t)h * R + r];
+          /* an ablated term (flags) is the literal 0 in the same sum */
+          double t1 = (flags & ORACLE_SCH_NO_TOPO) ? 0.0 : alpha * Bpref[(int64_t)h * R + r];
           double ex = (double)excess[h];
           double tn = (double)T[(int64_t)h * R + r] / (ex > ORACLE_EPS0 ? ex : ORACLE_EPS0);
-          double t2 = a2 * tn;
+          double t2 = (flags & ORACLE_SCH_NO_FLOW) ? 0.0 : a2 * tn;
           double score = (q + t1) + t2;
           if (score > best_s[r]) { /* strict: lowest e wins ties */
             best_s[r] = score;
@@ -401,17 +402,18 @@ static void phase2_one(const int64_t* spill, const int64_t* spare, const int64_t
 
 int oracle_phase2(const int64_t* spill, const int64_t* spare, const int64_t* excess,
                   const double* alpha, const int32_t* home, const float* T, const double* Bpref,
-                  int32_t B, int32_t R, int32_t E, int32_t K, int32_t* slot_expert,
+                  int32_t B, int32_t R, int32_t E, int32_t K, uint32_t flags, int32_t* slot_expert,
                   int64_t* slot_amount, int32_t* inner_used) {
   if (!spill || !spare || !excess || !alpha || !home || !T || !Bpref || !slot_expert ||
-      !slot_amount || !inner_used || B < 0 || R <= 0 || E <= 0 || K < 0)
+      !slot_amount || !inner_used || B < 0 || R <= 0 || E <= 0 || K < 0 ||
+      (flags & ~(uint32_t)(ORACLE_SCH_NO_TOPO | ORACLE_SCH_NO_FLOW)))
     return -1;
   for (int32_t e = 0; e < E; ++e)
     if (home[e] < 0 || home[e] >= R) return -1;
 #pragma omp parallel for schedule(dynamic)
   for (int32_t b = 0; b < B; ++b)
     phase2_one(spill + (int64_t)b * E, spare + (int64_t)b * R, excess + (int64_t)b * R, alpha[b],
-               home, T + (int64_t)b * R * R, Bpref, R, E, K, slot_expert + (int64_t)b * R * K,
+               home, T + (int64_t)b * R * R, Bpref, R, E, K, flags, slot_expert + (int64_t)b * R * K,
                slot_amount + (int64_t)b * R * K, inner_used + b);
   return 0;
 }

@@ -18,6 +18,9 @@
 #include <stdint.h>
 
 #define ORACLE_EPS0 1e-12
+/* Phase-2 score ablations: drop alpha * Bpref, or drop 0.1 * alpha * Tn */
+#define ORACLE_SCH_NO_TOPO 0x1u
+#define ORACLE_SCH_NO_FLOW 0x2u
 
 #define ORACLE_ST_BAD_ID 1u
 #define ORACLE_ST_BAD_INPUT 2u
@@ -65,11 +68,12 @@ int oracle_topology_pref(const float* C, int32_t R, double* Bpref, double* Bauct
 
 /* Alg. 2 (Phase 2, column-priority matching) for B problems.
  *   T [B][R][R] is the Phase-1 plan in fp32 (promoted to fp64 inside).
+ *   flags: ORACLE_SCH_* ablations of the score (0 for the method as published).
  * outputs: slot_expert [B][R*K] (-1 empty), slot_amount [B][R*K],
  *   inner_used [B] (inner iterations executed, summed over rounds). */
 int oracle_phase2(const int64_t* spill, const int64_t* spare, const int64_t* excess,
                   const double* alpha, const int32_t* home, const float* T, const double* Bpref,
-                  int32_t B, int32_t R, int32_t E, int32_t K, int32_t* slot_expert,
+                  int32_t B, int32_t R, int32_t E, int32_t K, uint32_t flags, int32_t* slot_expert,
                   int64_t* slot_amount, int32_t* inner_used);
 
 /* Alg. 3 (Phase 3, Lagrangian auction) for B problems.

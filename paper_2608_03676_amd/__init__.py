@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(HERE, "libtaot.so")
 
 ST_BAD_ID, ST_BAD_INPUT, ST_ZERO_MASS, ST_UNFILLED, ST_STREAMED = 0x1, 0x2, 0x4, 0x8, 0x10
 SK_NO_COLCAP, SK_FORCE_STREAM, SK_NO_REGISTER, SK_WAVES_1 = 0x1, 0x2, 0x4, 0x8
+SCH_NO_TOPO, SCH_NO_FLOW = 0x1, 0x2  # Phase-2 score ablations (round_schedule flags)
 STATUS_NAMES = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace", 4: "launch"}
 
 _lib = None
@@ -59,7 +60,7 @@ def lib():
         L.taot_round_schedule_workspace_size.restype = _SZ
         L.taot_round_schedule_workspace_size.argtypes = [_I32, _I32, _I32, _I32]
         L.taot_round_schedule.restype = ctypes.c_int
-        L.taot_round_schedule.argtypes = [_P] * 9 + [_I32] * 4 + [_F64, _I64] + [_P] * 6 + [_P, _SZ, _P]
+        L.taot_round_schedule.argtypes = [_P] * 9 + [_I32] * 4 + [_F64, _I64, _U32] + [_P] * 6 + [_P, _SZ, _P]
         L.taot_topology_pref.restype = ctypes.c_int
         L.taot_topology_pref.argtypes = [_P, _I32, _P, _P]
         _lib = L
@@ -180,8 +181,9 @@ class Schedule:
 
 def round_schedule(n, spill, spare, excess, alpha, home, T, Bpref, Bauct, K: int,
                    price_step: float = 2.0 ** -6, t_max: int = 0, out: Optional[Schedule] = None,
-                   workspace: Optional[torch.Tensor] = None, stream=None) -> Schedule:
-    """Steps 4-5: Phase-2 matching and Phase-3 auction (taot_round_schedule)."""
+                   workspace: Optional[torch.Tensor] = None, stream=None, flags: int = 0) -> Schedule:
+    """Steps 4-5: Phase-2 matching and Phase-3 auction (taot_round_schedule).
+    flags: SCH_NO_TOPO / SCH_NO_FLOW drop a Phase-2 score term (ablations)."""
     _dev(n, "n", torch.int32)
     for name, t in (("spill", spill), ("spare", spare), ("excess", excess)):
         _dev(t, name, torch.int64)
@@ -205,7 +207,7 @@ def round_schedule(n, spill, spare, excess, alpha, home, T, Bpref, Bauct, K: int
     _check("taot_round_schedule", lib().taot_round_schedule(
         n.data_ptr(), spill.data_ptr(), spare.data_ptr(), excess.data_ptr(), alpha.data_ptr(),
         home.data_ptr(), T.data_ptr(), Bpref.data_ptr(), Bauct.data_ptr(), B, R, E, K, float(price_step),
-        int(t_max), _ptr(out.slot_expert), _ptr(out.slot_amount), _ptr(out.X), _ptr(out.unfilled),
+        int(t_max), int(flags), _ptr(out.slot_expert), _ptr(out.slot_amount), _ptr(out.X), _ptr(out.unfilled),
         _ptr(out.rounds_used), _ptr(out.status), ws.data_ptr(), ws.numel(), _stream(stream)))
     return out
 

@@ -76,10 +76,11 @@ taot_status taot_round_schedule(const int32_t* n, const int64_t* spill, const in
                                 const int64_t* excess, const double* alpha, const int32_t* home,
                                 const float* T, const double* Bpref, const double* Bauct,
                                 int32_t B, int32_t R, int32_t E, int32_t K, double price_step,
-                                int64_t t_max, int32_t* slot_expert, int64_t* slot_amount,
+                                int64_t t_max, uint32_t flags, int32_t* slot_expert, int64_t* slot_amount,
                                 int32_t* X, int64_t* unfilled, int32_t* rounds_used,
                                 uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
   if (bad_dims(B, R) || E <= 0 || K < 0 || !isfinite(price_step)) return TAOT_ERR_INVALID_ARG;
+  if (flags & ~(TAOT_SCH_NO_TOPO | TAOT_SCH_NO_FLOW)) return TAOT_ERR_INVALID_ARG;
   if (R > TAOT_MAX_RANKS || E > TAOT_MAX_EXPERTS || K > TAOT_MAX_SLOTS_PER_RANK)
     return TAOT_ERR_UNSUPPORTED;
   if (B == 0) return TAOT_OK;
@@ -89,7 +90,7 @@ taot_status taot_round_schedule(const int32_t* n, const int64_t* spill, const in
   if ((int64_t)R * K * R > 0x7fffffffLL * 8) return TAOT_ERR_UNSUPPORTED;
   if (!ws || ws_bytes < schedule_ws(B, R, E, K)) return TAOT_ERR_WORKSPACE;
   return launch_schedule(n, spill, spare, excess, alpha, home, T, Bpref, Bauct, B, R, E, K,
-                         price_step, t_max, slot_expert, slot_amount, X, unfilled, rounds_used,
+                         price_step, t_max, flags, slot_expert, slot_amount, X, unfilled, rounds_used,
                          status, ws, static_cast<hipStream_t>(stream));
 }
 

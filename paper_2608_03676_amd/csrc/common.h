@@ -81,7 +81,7 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
                             const int64_t* excess, const double* alpha, const int32_t* home,
                             const float* T, const double* Bpref, const double* Bauct, int32_t B,
                             int32_t R, int32_t E, int32_t K, double price_step, int64_t t_max,
-                            int32_t* slot_expert, int64_t* slot_amount, int32_t* X,
+                            uint32_t flags, int32_t* slot_expert, int64_t* slot_amount, int32_t* X,
                             int64_t* unfilled, int32_t* rounds_used, uint32_t* status, void* ws,
                             hipStream_t stream);
 size_t schedule_ws(int32_t B, int32_t R, int32_t E, int32_t K);

@@ -56,7 +56,18 @@ struct SchParams {
   char* slab;
   int64_t slab_bytes;
   const int32_t* fallback;  // [B] 1 = the LDS-resident kernel left this problem to us (nullable)
+  uint32_t flags;           // TAOT_SCH_*
 };
+
+// Weights of the Phase-2 score terms: alpha for alpha * Bpref and 0.1 * alpha
+// for the flow hint, or 0 for a term the flags drop (it then enters the sum
+// as +0, in the same evaluation order).
+__device__ __forceinline__ double topo_weight(uint32_t flags, double alpha) {
+  return (flags & TAOT_SCH_NO_TOPO) ? 0.0 : alpha;
+}
+__device__ __forceinline__ double flow_weight(uint32_t flags, double alpha) {
+  return (flags & TAOT_SCH_NO_FLOW) ? 0.0 : 0.1 * alpha;
+}
 
 struct Slab {
   // Phase 2
@@ -168,8 +179,8 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
     int32_t* se = p.slot_expert + b * S;
     int64_t* sa = p.slot_amount + b * S;
     int32_t* Xb = p.X + b * (int64_t)R * S;
-    const double alpha = p.alpha[b];
-    const double a2 = 0.1 * alpha;  // weight of the OT hint
+    const double alpha = topo_weight(p.flags, p.alpha[b]);
+    const double a2 = flow_weight(p.flags, p.alpha[b]);  // weight of the OT hint
 
     // ---- validation and setup -----------------------------------------------
     if (tid == 0) sh_flag = 0;
@@ -825,8 +836,8 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   int32_t* se = p.slot_expert + b * S;
   int64_t* sa = p.slot_amount + b * S;
   int32_t* Xb = p.X + b * (int64_t)R * S;
-  const double alpha = p.alpha[b];
-  const double a2 = 0.1 * alpha;
+  const double alpha = topo_weight(p.flags, p.alpha[b]);
+  const double a2 = flow_weight(p.flags, p.alpha[b]);
 
   // ---- validation, candidates, cold ranks ------------------------------------------
   bool badh = false;
@@ -1406,13 +1417,14 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
                             const int64_t* excess, const double* alpha, const int32_t* home,
                             const float* T, const double* Bpref, const double* Bauct, int32_t B,
                             int32_t R, int32_t E, int32_t K, double price_step, int64_t t_max,
-                            int32_t* slot_expert, int64_t* slot_amount, int32_t* X,
+                            uint32_t flags, int32_t* slot_expert, int64_t* slot_amount, int32_t* X,
                             int64_t* unfilled, int32_t* rounds_used, uint32_t* status, void* ws,
                             hipStream_t stream) {
   if (B == 0) return TAOT_OK;
   SchWs w = carve_sched(ws, B, R, E, K);
   SchParams p{n, spill, spare, excess, alpha, home, T, Bpref, Bauct, B, R, E, K, price_step, t_max,
-              slot_expert, slot_amount, X, unfilled, rounds_used, status, w.slab, w.slab_bytes, w.fallback};
+              slot_expert, slot_amount, X, unfilled, rounds_used, status, w.slab, w.slab_bytes, w.fallback,
+              flags};
   bool launched = false;
   taot_status st = launch_lds_path<LdsSmall>(p, w, B, R, E, K, price_step, stream, launched);
   if (st == TAOT_OK && !launched) st = launch_lds_path<LdsLarge>(p, w, B, R, E, K, price_step, stream, launched);

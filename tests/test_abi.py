@@ -86,10 +86,11 @@ def test_host_validation_sinkhorn():
 def test_host_validation_round_schedule():
     L = taot.lib()
     P = _fake()
-    call = lambda B=1, R=4, E=4, K=2, step=1.0 / 64, ws=P, wsb=1 << 40: L.taot_round_schedule(
-        P, P, P, P, P, P, P, P, P, B, R, E, K, step, 0, P, P, P, P, None, None, ws, wsb, None)
+    call = lambda B=1, R=4, E=4, K=2, step=1.0 / 64, flags=0, ws=P, wsb=1 << 40: L.taot_round_schedule(
+        P, P, P, P, P, P, P, P, P, B, R, E, K, step, 0, flags, P, P, P, P, None, None, ws, wsb, None)
     assert call(K=-1) == 1
     assert call(step=float("inf")) == 1
+    assert call(flags=0x4) == 1          # unknown ablation flag
     assert call(K=65) == 2
     assert call(ws=None) == 3
     assert call(wsb=16) == 3

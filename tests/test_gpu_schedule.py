@@ -17,11 +17,11 @@ def _to(x, dt=None):
     return torch.from_numpy(np.ascontiguousarray(x if dt is None else x.astype(dt))).to("cuda:0")
 
 
-def _compare(L, home, T32, Bp, Ba, K, t_max=0, eta=2.0 ** -6, label=""):
-    se, sa, used = O.phase2(L.spill, L.spare, L.excess, L.alpha, home, T32, Bp, K)
+def _compare(L, home, T32, Bp, Ba, K, t_max=0, eta=2.0 ** -6, label="", flags=0):
+    se, sa, used = O.phase2(L.spill, L.spare, L.excess, L.alpha, home, T32, Bp, K, flags=flags)
     X, unfilled, rounds, status = O.phase3(L.n, se, sa, Ba, K, eta, t_max)
     s = taot.round_schedule(_to(L.n), _to(L.spill), _to(L.spare), _to(L.excess), _to(L.alpha),
-                            _to(home, np.int32), _to(T32), _to(Bp), _to(Ba), K, eta, t_max)
+                            _to(home, np.int32), _to(T32), _to(Bp), _to(Ba), K, eta, t_max, flags=flags)
     torch.cuda.synchronize()
     assert np.array_equal(s.slot_expert.cpu().numpy(), se), f"{label} slot experts"
     assert np.array_equal(s.slot_amount.cpu().numpy(), sa), f"{label} slot amounts"
@@ -46,6 +46,21 @@ def test_workloads(cfg, problems, K, gpu):
     Bp, Ba = O.topology_pref(C)
     se, sa, X, unfilled = _compare(L, W.home_map(w), P.T.astype(np.float32), Bp, Ba, K, label=f"cfg{cfg}")
     assert np.all(unfilled == 0)
+
+
+@pytest.mark.parametrize("flags", [taot.SCH_NO_TOPO, taot.SCH_NO_FLOW, taot.SCH_NO_TOPO | taot.SCH_NO_FLOW])
+@pytest.mark.parametrize("cfg,problems", [(1, list(range(0, 58, 8))), (3, [0, 977])])
+def test_score_ablations(cfg, problems, flags, gpu):
+    """The Phase-2 score ablations, bit-exact against the oracle with the
+    same flags."""
+    w = W.WORKLOADS[cfg]
+    print(f"[schedule parity] workload {cfg} problems {problems} flags {flags}", flush=True)
+    _, L = oracle_inputs(w, problems)
+    C = W.cost_matrix(w)
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), w.eps, w.iters)
+    Bp, Ba = O.topology_pref(C)
+    _compare(L, W.home_map(w), P.T.astype(np.float32), Bp, Ba, w.K, label=f"cfg{cfg} flags {flags}",
+             flags=flags)
 
 
 def _random_instance(seed):

@@ -89,6 +89,34 @@ def test_phase2_micro_ot_hint_breaks_tie():
     assert se[0].tolist() == [-1, -1, 0, 0] and sa[0].tolist() == [0, 0, 3, 2]
 
 
+def test_phase2_micro_ablations():
+    """The intra-node case with expert 0 spilling only 3 (excess still 5).
+    Full score: rank 1 (6.1, intra-node) takes 1, then ranks 2 and 3 tie at
+    min(2,2) + 1.25 + 0.2 = 3.45 and rank 2 takes the last 2.
+    Without the topology term the scores are min(spill, spare) + 0.5 T/5:
+    ranks 2 and 3 tie at 2 + 0.2 and rank 2 takes 2; then rank 1 has
+    min(1,1) + 0.1 = 1.1 against rank 3's min(1,2) + 0.2 = 1.2, so rank 3
+    takes the last token.  In the OT-hint case, dropping the flow term gives
+    the same split as the uninformative hint (rank 2 first, 3 / 2)."""
+    C = np.array([[0, 1, 4, 4], [1, 0, 4, 4], [4, 4, 0, 1], [4, 4, 1, 0]], np.float32)
+    Bp, _ = O.topology_pref(C)
+    T = np.zeros((4, 4), np.float32)
+    T[0] = [0, 1, 2, 2]
+    args = ([3, 0, 0, 0], [0, 1, 2, 2], [5, 0, 0, 0], 5.0, np.arange(4), T, Bp)
+    se, sa, used = O.phase2(*args, K=1)
+    assert se[0].tolist() == [-1, 0, 0, -1] and sa[0].tolist() == [0, 1, 2, 0] and used[0] == 2
+    se, sa, used = O.phase2(*args, K=1, flags=O.SCH_NO_TOPO)
+    assert se[0].tolist() == [-1, -1, 0, 0] and sa[0].tolist() == [0, 0, 2, 1] and used[0] == 2
+    T2 = np.zeros((4, 4), np.float32)
+    T2[0] = [0, 0, 1, 4]
+    args2 = ([5, 0, 0, 0], [0, 0, 3, 3], [5, 0, 0, 0], 5.0, np.arange(4), T2, Bp)
+    for flags in (O.SCH_NO_FLOW, O.SCH_NO_TOPO | O.SCH_NO_FLOW):
+        se, sa, _ = O.phase2(*args2, K=1, flags=flags)
+        assert se[0].tolist() == [-1, -1, 0, 0] and sa[0].tolist() == [0, 0, 3, 2]
+    with pytest.raises(ValueError):
+        O.phase2(*args, K=1, flags=0x4)
+
+
 def test_phase3_micro():
     """Continues the intra-node micro-case: slots 1, 2, 3 (hosts 1, 2, 3) hold
     expert 0 for 3, 1, 1 tokens; ranks hold n[:,0] = (4, 3, 2, 1); bonus 1
