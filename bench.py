@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--other-steps", type=int, default=3,
                     help="timed steps for the planner latency of workloads 1-4 other than --workload (0: skip)")
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--quality", action="store_true",
+                    help="print the plan-quality table of the Phase-2 score ablations on --workload "
+                         "(every problem of the batch, no timing) instead of benchmarking")
     return ap.parse_args()
 
 
@@ -165,6 +168,50 @@ def run_workload(w, K, steps, warmup, dev):
                 loads_ms=loads_ms, sk_ms=sk_ms, sch_ms=sch_ms, ms_step=ms_step)
 
 
+def plan_quality_table(w, K, dev):
+    """Plan quality of the full score and of its ablations (round_schedule
+    flags) on one batch: rho before and after the planned moves, replicas
+    inside / across nodes (node = rank // 8) and the weighted cost intra +
+    3 inter, mean and standard deviation over the batch's problems."""
+    import numpy as np
+    import torch
+
+    import paper_2608_03676_amd as taot
+    import workloads as W
+    B, R, E, N = w.B, w.R, w.E, w.N
+    thr, seeds = W.tables(w)
+    ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
+    W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
+                     B, E, R, w.tokens, w.k, ids)
+    home = torch.from_numpy(W.home_map(w)).to(dev)
+    C_np = W.cost_matrix(w)
+    Bp_np, Ba_np = taot.topology_pref(C_np)
+    C, Bp, Ba = (torch.from_numpy(x).to(dev) for x in (C_np, Bp_np, Ba_np))
+    loads = taot.plan_loads(ids, home, E)
+    flow = taot.sinkhorn_batched(loads.supply, loads.demand, C, w.eps, w.iters)
+    del ids
+    rho0 = loads.rho.cpu().numpy()
+    rows = []
+    for name, flags in (("full score", 0), ("no topology term", taot.SCH_NO_TOPO),
+                        ("no flow-hint term", taot.SCH_NO_FLOW),
+                        ("spill/spare only", taot.SCH_NO_TOPO | taot.SCH_NO_FLOW)):
+        sched = taot.round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T,
+                                    Bp, Ba, K, w.price_step, 0, flags=flags)
+        q = taot.plan_quality(loads.load_r, home, sched, K, ranks_per_node=8, w_inter=3.0)
+        torch.cuda.synchronize()
+        ra, ni, no, wt = (x.cpu().numpy().astype(float) for x in (q.rho_after, q.intra, q.inter, q.weighted))
+        rows.append(dict(variant=name, flags=flags, rho_before=[rho0.mean(), rho0.std()],
+                         rho_after=[ra.mean(), ra.std()], intra=[ni.mean(), ni.std()], inter=[no.mean(), no.std()],
+                         weighted=[wt.mean(), wt.std()], unfilled=int(sched.unfilled.sum().item())))
+    print(f"plan quality, workload {w.index}: {B} problems, R = {R}, K = {K} (mean +- std over problems)")
+    print(f"{'variant':<20} {'rho before':>16} {'rho after':>16} {'intra':>14} {'inter':>14} {'intra+3inter':>16} unfilled")
+    for r in rows:
+        f = lambda v, d=4: f"{v[0]:.{d}f} +- {v[1]:.{d}f}"
+        print(f"{r['variant']:<20} {f(r['rho_before']):>16} {f(r['rho_after']):>16} {f(r['intra'], 1):>14} "
+              f"{f(r['inter'], 1):>14} {f(r['weighted'], 1):>16} {r['unfilled']}")
+    print(json.dumps({"plan_quality": rows, "workload": w.index, "K": K}), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -184,6 +231,9 @@ def main():
     w = W.WORKLOADS[args.workload]
     K = w.K if args.K is None else args.K
     B, R, E, N = w.B, w.R, w.E, w.N
+    if args.quality:
+        plan_quality_table(w, K, dev)
+        return
     log(f"[bench] workload {w.index}: {w.name}; B={B} R={R} E={E} N={N} iters={w.iters} K={K}")
     run = run_workload(w, K, args.steps, args.warmup, dev)
     loads, flow, sched = run["loads"], run["flow"], run["sched"]

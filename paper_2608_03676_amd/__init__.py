@@ -237,7 +237,7 @@ class Plan:
 
 
 def plan_step(ids, home, C, E: int, eps: float, iters: int, K: int, Bpref=None, Bauct=None,
-              price_step: float = 2.0 ** -6, t_max: int = 0, stream=None) -> Plan:
+              price_step: float = 2.0 ** -6, t_max: int = 0, stream=None, flags: int = 0) -> Plan:
     """One full planner step over all B problems (three enqueued calls, no sync)."""
     if Bpref is None or Bauct is None:
         Bp, Ba = topology_pref(C.detach().cpu().numpy() if isinstance(C, torch.Tensor) else C)
@@ -246,5 +246,42 @@ def plan_step(ids, home, C, E: int, eps: float, iters: int, K: int, Bpref=None, 
     loads = plan_loads(ids, home, E, stream=stream)
     flow = sinkhorn_batched(loads.supply, loads.demand, C, eps, iters, stream=stream)
     sched = round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T,
-                           Bpref, Bauct, K, price_step, t_max, stream=stream)
+                           Bpref, Bauct, K, price_step, t_max, stream=stream, flags=flags)
     return Plan(loads, flow, sched)
+
+
+@dataclasses.dataclass
+class Quality:
+    load_after: torch.Tensor  # [B][R] int64 rank loads once the planned tokens moved
+    rho_after: torch.Tensor   # [B] float64 (R * max load - L) / L, 0 if L = 0
+    intra: torch.Tensor       # [B] int64 replicas hosted in their expert's home node
+    inter: torch.Tensor       # [B] int64 replicas hosted in another node
+    weighted: torch.Tensor    # [B] float64 intra + w_inter * inter
+
+
+def plan_quality(load_r: torch.Tensor, home: torch.Tensor, sched: Schedule, K: int,
+                 ranks_per_node: int = 8, w_inter: float = 3.0) -> Quality:
+    """Plan-quality metrics of one schedule per problem (Sec. 4.1): the
+    imbalance left after the planned tokens move from each expert's home rank
+    to the ranks hosting its replicas, and the replicas placed inside and
+    across nodes (node = rank // ranks_per_node), weighted intra + w_inter *
+    inter.  Evaluation of a plan, not a planner step: plain tensor ops on the
+    schedule's device."""
+    se = sched.slot_expert.long()
+    B, S = se.shape
+    R = load_r.shape[1]
+    valid = se >= 0
+    moved = sched.X.sum(dim=1, dtype=torch.int64) * valid           # [B][S]
+    host = (torch.arange(S, device=se.device) // K).expand(B, S)      # [B][S]
+    h = home.long()[se.clamp(min=0)]                                  # [B][S]
+    la = load_r.to(torch.int64).clone()
+    la.scatter_add_(1, h, -moved)
+    la.scatter_add_(1, host, moved)
+    L = load_r.to(torch.int64).sum(1)
+    lmax = la.max(1).values
+    rho = torch.where(L > 0, (R * lmax - L).double() / L.clamp(min=1).double(),
+                      torch.zeros_like(L, dtype=torch.float64))
+    same = (h // ranks_per_node) == (host // ranks_per_node)
+    intra = (valid & same).sum(1)
+    inter = (valid & ~same).sum(1)
+    return Quality(la, rho, intra, inter, intra.double() + w_inter * inter.double())
