@@ -169,8 +169,8 @@ def run_workload(w, K, steps, warmup, dev):
 
 
 def plan_quality_table(w, K, dev):
-    """Plan quality of the full score and of its ablations (round_schedule
-    flags) on one batch: rho before and after the planned moves, replicas
+    """Plan quality of the full score, of its ablations and of row-priority
+    matching (round_schedule flags) on one batch: rho before and after the planned moves, replicas
     inside / across nodes (node = rank // 8) and the weighted cost intra +
     3 inter, mean and standard deviation over the batch's problems."""
     import numpy as np
@@ -194,7 +194,8 @@ def plan_quality_table(w, K, dev):
     rows = []
     for name, flags in (("full score", 0), ("no topology term", taot.SCH_NO_TOPO),
                         ("no flow-hint term", taot.SCH_NO_FLOW),
-                        ("spill/spare only", taot.SCH_NO_TOPO | taot.SCH_NO_FLOW)):
+                        ("spill/spare only", taot.SCH_NO_TOPO | taot.SCH_NO_FLOW),
+                        ("row priority", taot.SCH_ROW_PRIORITY)):
         sched = taot.round_schedule(loads.n, loads.spill, loads.spare, loads.excess, loads.alpha, home, flow.T,
                                     Bp, Ba, K, w.price_step, 0, flags=flags)
         q = taot.plan_quality(loads.load_r, home, sched, K, ranks_per_node=8, w_inter=3.0)

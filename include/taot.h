@@ -67,6 +67,13 @@ typedef enum {
  * the contribution of each term).  Phase 3 is unaffected. */
 #define TAOT_SCH_NO_TOPO 0x1u  /* drop the topology term alpha * Bpref (score q + 0.1 alpha Tn) */
 #define TAOT_SCH_NO_FLOW 0x2u  /* drop the flow-hint term 0.1 * alpha * Tn (score q + alpha Bpref) */
+#define TAOT_SCH_ROW_PRIORITY 0x4u /* Phase 2 from the experts' side (the greedy Sec. A.3 sets
+                                      Alg. 2 against): each slot round takes the experts with
+                                      spill left by spill at the round's start (largest first,
+                                      lower id on ties), and each takes its best-scoring ranks
+                                      with spare left and the slot free, one at a time (lowest
+                                      rank on ties), until its spill is gone; rounds_used[b][0]
+                                      then counts placements */
 
 /* Returns a static description of a status code (host, never NULL). */
 const char* taot_status_string(taot_status s);

@@ -127,7 +127,7 @@ def topology_pref(C):
     return Bp, Ba
 
 
-SCH_NO_TOPO, SCH_NO_FLOW = 0x1, 0x2  # Phase-2 score ablations
+SCH_NO_TOPO, SCH_NO_FLOW, SCH_ROW_PRIORITY = 0x1, 0x2, 0x4  # Phase-2 ablations
 
 
 def phase2(spill, spare, excess, alpha, home, T32, Bpref, K: int, flags: int = 0):

@@ -400,16 +400,99 @@ static void phase2_one(const int64_t* spill, const int64_t* spare, const int64_t
   free(win_s);
 }
 
+/* Row priority (the experts-outer reading of the greedy that Sec. A.3 sets
+ * Alg. 2 against): in each slot round k, the experts with spill left are
+ * taken in order of their spill at the round's start (largest first, lower
+ * id on ties); each in turn takes ranks one at a time, the best-scoring rank
+ * with spare left, slot k free and not already holding the expert (same
+ * score as Alg. 2, lowest rank on ties), moving min(spill, spare), until its
+ * spill is gone or no rank qualifies. */
+static const int64_t* g_order_spill; /* sort key of order_cmp */
+static int order_cmp(const void* a, const void* b) {
+  const int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+  if (g_order_spill[x] != g_order_spill[y]) return g_order_spill[x] > g_order_spill[y] ? -1 : 1;
+  return x < y ? -1 : (x > y);
+}
+static void phase2_row_one(const int64_t* spill, const int64_t* spare, const int64_t* excess,
+                           double alpha, const int32_t* home, const float* T, const double* Bpref,
+                           int32_t R, int32_t E, int32_t K, uint32_t flags, int32_t* slot_expert,
+                           int64_t* slot_amount, int32_t* used_out) {
+  int64_t* spill_p = (int64_t*)malloc(sizeof(int64_t) * (size_t)E);
+  int64_t* spare_p = (int64_t*)malloc(sizeof(int64_t) * (size_t)R);
+  int64_t* key = (int64_t*)malloc(sizeof(int64_t) * (size_t)E);
+  int32_t* order = (int32_t*)malloc(sizeof(int32_t) * (size_t)E);
+  unsigned char* U = (unsigned char*)calloc((size_t)E * (size_t)R, 1);
+  memcpy(spill_p, spill, sizeof(int64_t) * (size_t)E);
+  memcpy(spare_p, spare, sizeof(int64_t) * (size_t)R);
+  for (int32_t s = 0; s < R * K; ++s) {
+    slot_expert[s] = -1;
+    slot_amount[s] = 0;
+  }
+  const double a2 = 0.1 * alpha;
+  int32_t used = 0;
+  for (int32_t k = 0; k < K; ++k) {
+    int32_t n = 0;
+    for (int32_t e = 0; e < E; ++e) {
+      key[e] = spill_p[e];
+      if (spill_p[e] > 0) order[n++] = e;
+    }
+    g_order_spill = key;
+    qsort(order, (size_t)n, sizeof(int32_t), order_cmp);
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t e = order[i], h = home[e];
+      while (spill_p[e] > 0) {
+        int32_t best = -1;
+        double bs = -INFINITY;
+        for (int32_t r = 0; r < R; ++r) {
+          if (spare_p[r] <= 0 || slot_expert[r * K + k] >= 0 || h == r || U[(int64_t)e * R + r]) continue;
+          double q = (double)(spill_p[e] < spare_p[r] ? spill_p[e] : spare_p[r]);
+          double t1 = (flags & ORACLE_SCH_NO_TOPO) ? 0.0 : alpha * Bpref[(int64_t)h * R + r];
+          double ex = (double)excess[h];
+          double tn = (double)T[(int64_t)h * R + r] / (ex > ORACLE_EPS0 ? ex : ORACLE_EPS0);
+          double t2 = (flags & ORACLE_SCH_NO_FLOW) ? 0.0 : a2 * tn;
+          double score = (q + t1) + t2;
+          if (score > bs) { /* strict: lowest r wins ties */
+            bs = score;
+            best = r;
+          }
+        }
+        if (best < 0) break;
+        int64_t g = spill_p[e] < spare_p[best] ? spill_p[e] : spare_p[best];
+        spill_p[e] -= g;
+        spare_p[best] -= g;
+        U[(int64_t)e * R + best] = 1;
+        slot_expert[best * K + k] = e;
+        slot_amount[best * K + k] += g;
+        ++used;
+      }
+    }
+  }
+  *used_out = used;
+  free(spill_p);
+  free(spare_p);
+  free(key);
+  free(order);
+  free(U);
+}
+
 int oracle_phase2(const int64_t* spill, const int64_t* spare, const int64_t* excess,
                   const double* alpha, const int32_t* home, const float* T, const double* Bpref,
                   int32_t B, int32_t R, int32_t E, int32_t K, uint32_t flags, int32_t* slot_expert,
                   int64_t* slot_amount, int32_t* inner_used) {
   if (!spill || !spare || !excess || !alpha || !home || !T || !Bpref || !slot_expert ||
       !slot_amount || !inner_used || B < 0 || R <= 0 || E <= 0 || K < 0 ||
-      (flags & ~(uint32_t)(ORACLE_SCH_NO_TOPO | ORACLE_SCH_NO_FLOW)))
+      (flags & ~(uint32_t)(ORACLE_SCH_NO_TOPO | ORACLE_SCH_NO_FLOW | ORACLE_SCH_ROW_PRIORITY)))
     return -1;
   for (int32_t e = 0; e < E; ++e)
     if (home[e] < 0 || home[e] >= R) return -1;
+  if (flags & ORACLE_SCH_ROW_PRIORITY) {
+    /* serial over problems: the qsort key is a file-scope pointer */
+    for (int32_t b = 0; b < B; ++b)
+      phase2_row_one(spill + (int64_t)b * E, spare + (int64_t)b * R, excess + (int64_t)b * R, alpha[b],
+                     home, T + (int64_t)b * R * R, Bpref, R, E, K, flags, slot_expert + (int64_t)b * R * K,
+                     slot_amount + (int64_t)b * R * K, inner_used + b);
+    return 0;
+  }
 #pragma omp parallel for schedule(dynamic)
   for (int32_t b = 0; b < B; ++b)
     phase2_one(spill + (int64_t)b * E, spare + (int64_t)b * R, excess + (int64_t)b * R, alpha[b],

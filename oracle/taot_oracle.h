@@ -21,6 +21,8 @@
 /* Phase-2 score ablations: drop alpha * Bpref, or drop 0.1 * alpha * Tn */
 #define ORACLE_SCH_NO_TOPO 0x1u
 #define ORACLE_SCH_NO_FLOW 0x2u
+/* Phase-2 matching from the experts' side (row priority) instead of Alg. 2 */
+#define ORACLE_SCH_ROW_PRIORITY 0x4u
 
 #define ORACLE_ST_BAD_ID 1u
 #define ORACLE_ST_BAD_INPUT 2u
@@ -68,7 +70,9 @@ int oracle_topology_pref(const float* C, int32_t R, double* Bpref, double* Bauct
 
 /* Alg. 2 (Phase 2, column-priority matching) for B problems.
  *   T [B][R][R] is the Phase-1 plan in fp32 (promoted to fp64 inside).
- *   flags: ORACLE_SCH_* ablations of the score (0 for the method as published).
+ *   flags: ORACLE_SCH_* ablations of the score (0 for the method as published);
+ *   ORACLE_SCH_ROW_PRIORITY replaces Alg. 2 by the experts-outer greedy that
+ *   Sec. A.3 contrasts it with (inner_used then counts placements).
  * outputs: slot_expert [B][R*K] (-1 empty), slot_amount [B][R*K],
  *   inner_used [B] (inner iterations executed, summed over rounds). */
 int oracle_phase2(const int64_t* spill, const int64_t* spare, const int64_t* excess,

@@ -25,7 +25,7 @@ LIB_PATH = os.path.join(HERE, "libtaot.so")
 
 ST_BAD_ID, ST_BAD_INPUT, ST_ZERO_MASS, ST_UNFILLED, ST_STREAMED = 0x1, 0x2, 0x4, 0x8, 0x10
 SK_NO_COLCAP, SK_FORCE_STREAM, SK_NO_REGISTER, SK_WAVES_1 = 0x1, 0x2, 0x4, 0x8
-SCH_NO_TOPO, SCH_NO_FLOW = 0x1, 0x2  # Phase-2 score ablations (round_schedule flags)
+SCH_NO_TOPO, SCH_NO_FLOW, SCH_ROW_PRIORITY = 0x1, 0x2, 0x4  # Phase-2 ablations (round_schedule flags)
 STATUS_NAMES = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace", 4: "launch"}
 
 _lib = None
@@ -183,7 +183,8 @@ def round_schedule(n, spill, spare, excess, alpha, home, T, Bpref, Bauct, K: int
                    price_step: float = 2.0 ** -6, t_max: int = 0, out: Optional[Schedule] = None,
                    workspace: Optional[torch.Tensor] = None, stream=None, flags: int = 0) -> Schedule:
     """Steps 4-5: Phase-2 matching and Phase-3 auction (taot_round_schedule).
-    flags: SCH_NO_TOPO / SCH_NO_FLOW drop a Phase-2 score term (ablations)."""
+    flags: SCH_NO_TOPO / SCH_NO_FLOW drop a Phase-2 score term, SCH_ROW_PRIORITY matches
+    from the experts' side (ablations)."""
     _dev(n, "n", torch.int32)
     for name, t in (("spill", spill), ("spare", spare), ("excess", excess)):
         _dev(t, name, torch.int64)

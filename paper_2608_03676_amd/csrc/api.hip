@@ -80,7 +80,7 @@ taot_status taot_round_schedule(const int32_t* n, const int64_t* spill, const in
                                 int32_t* X, int64_t* unfilled, int32_t* rounds_used,
                                 uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
   if (bad_dims(B, R) || E <= 0 || K < 0 || !isfinite(price_step)) return TAOT_ERR_INVALID_ARG;
-  if (flags & ~(TAOT_SCH_NO_TOPO | TAOT_SCH_NO_FLOW)) return TAOT_ERR_INVALID_ARG;
+  if (flags & ~(TAOT_SCH_NO_TOPO | TAOT_SCH_NO_FLOW | TAOT_SCH_ROW_PRIORITY)) return TAOT_ERR_INVALID_ARG;
   if (R > TAOT_MAX_RANKS || E > TAOT_MAX_EXPERTS || K > TAOT_MAX_SLOTS_PER_RANK)
     return TAOT_ERR_UNSUPPORTED;
   if (B == 0) return TAOT_OK;

@@ -159,6 +159,8 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
   extern __shared__ char lds_raw[];
   __shared__ int32_t wave_cnt[kSchWaves];
   __shared__ int32_t sh_flag;
+  __shared__ double sh_rbs[kSchWaves];  // row-priority argmax, per wave
+  __shared__ int32_t sh_rbi[kSchWaves];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
   const int32_t R = p.R, E = p.E, K = p.K;
   const int64_t S = (int64_t)R * K;
@@ -225,6 +227,85 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 
     // ---- Phase 2: column-priority iterative matching --------------------------
     int32_t used2 = 0;
+    if (p.flags & TAOT_SCH_ROW_PRIORITY) {
+      // the experts-outer greedy (ablation): per slot round, the experts with
+      // spill left in order of spill (largest first, lower index on ties), each
+      // taking its best ranks one at a time until its spill is gone
+      for (int32_t k = 0; k < K; ++k) {
+        int32_t nord = 0;
+        for (int32_t base = 0; base < ne; base += kSchThreads) {
+          const int32_t ec = base + tid;
+          const int64_t v = ec < ne ? sl.spill_p[ec] : 0;
+          int32_t tot;
+          compact_pos(v > 0, wave_cnt, tot);
+          if (v > 0) {
+            int32_t pos = 0;
+            for (int32_t o = 0; o < ne; ++o) {
+              const int64_t u = sl.spill_p[o];
+              pos += u > v || (u == v && o < ec);
+            }
+            sl.win[pos] = ec;
+          }
+          nord += tot;
+        }
+        __syncthreads();
+        for (int32_t i = 0; i < nord; ++i) {
+          const int32_t ec = sl.win[i];
+          const int32_t h = p.home[sl.ce[ec]];
+          for (;;) {
+            const int64_t spl = sl.spill_p[ec];
+            if (spl <= 0) break;
+            double bs = -INFINITY;
+            int32_t best = INT_MAX;
+            for (int32_t rc = tid; rc < nc; rc += kSchThreads) {
+              const int64_t sp = sl.spare_p[rc];
+              const int32_t r = sl.cr[rc];
+              if (sp <= 0 || r == h || sl.assigned[(int64_t)rc * K + k] >= 0) continue;
+              bool taken = false;
+              for (int32_t kk = 0; kk < k; ++kk) taken |= sl.assigned[(int64_t)rc * K + kk] == ec;
+              if (taken) continue;
+              const double q = (double)(spl < sp ? spl : sp);
+              const double t1 = alpha * p.Bpref[(int64_t)h * R + r];
+              const double ex = (double)excess[h];
+              const double tn = (double)Tb[(int64_t)h * R + r] / (ex > kEps0 ? ex : kEps0);
+              const double t2 = a2 * tn;
+              const double score = (q + t1) + t2;
+              if (score > bs) { bs = score; best = rc; }  // rc ascends within a thread
+            }
+            // block argmax: max score, then lowest cold-rank index (= lowest rank)
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) {
+              const double os = __shfl_xor(bs, o, kWave);
+              const int32_t oi = __shfl_xor(best, o, kWave);
+              if (os > bs || (os == bs && oi < best)) { bs = os; best = oi; }
+            }
+            if (lane == 0) { sh_rbs[wid] = bs; sh_rbi[wid] = best; }
+            __syncthreads();
+            if (tid == 0) {
+              double b2 = sh_rbs[0];
+              int32_t i2 = sh_rbi[0];
+              for (int w2 = 1; w2 < kSchWaves; ++w2)
+                if (sh_rbs[w2] > b2 || (sh_rbs[w2] == b2 && sh_rbi[w2] < i2)) { b2 = sh_rbs[w2]; i2 = sh_rbi[w2]; }
+              if (i2 != INT_MAX) {
+                const int64_t g = spl < sl.spare_p[i2] ? spl : sl.spare_p[i2];
+                sl.spill_p[ec] -= g;
+                sl.spare_p[i2] -= g;
+                sl.assigned[(int64_t)i2 * K + k] = ec;
+                const int64_t s = (int64_t)sl.cr[i2] * K + k;
+                se[s] = sl.ce[ec];
+                sa[s] += g;
+              }
+              sh_flag = i2 != INT_MAX;
+            }
+            __syncthreads();
+            const bool placed = sh_flag != 0;
+            __syncthreads();
+            if (!placed) break;
+            ++used2;
+          }
+        }
+      }
+    } else
     for (int32_t k = 0; k < K; ++k) {
       for (int32_t rc = tid; rc < nc; rc += kSchThreads) sl.matched[rc] = 0;
       __syncthreads();
@@ -1426,8 +1507,12 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
               slot_expert, slot_amount, X, unfilled, rounds_used, status, w.slab, w.slab_bytes, w.fallback,
               flags};
   bool launched = false;
-  taot_status st = launch_lds_path<LdsSmall>(p, w, B, R, E, K, price_step, stream, launched);
-  if (st == TAOT_OK && !launched) st = launch_lds_path<LdsLarge>(p, w, B, R, E, K, price_step, stream, launched);
+  taot_status st = TAOT_OK;
+  // the row-priority ablation lives in the general kernel only
+  if (!(flags & TAOT_SCH_ROW_PRIORITY)) {
+    st = launch_lds_path<LdsSmall>(p, w, B, R, E, K, price_step, stream, launched);
+    if (st == TAOT_OK && !launched) st = launch_lds_path<LdsLarge>(p, w, B, R, E, K, price_step, stream, launched);
+  }
   if (st != TAOT_OK) return st;
   if (!launched) p.fallback = nullptr;  // the general kernel takes every problem
   const size_t lds = (size_t)R * (sizeof(double) + sizeof(uint64_t) + 2 * sizeof(int32_t));

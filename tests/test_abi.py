@@ -90,7 +90,7 @@ def test_host_validation_round_schedule():
         P, P, P, P, P, P, P, P, P, B, R, E, K, step, 0, flags, P, P, P, P, None, None, ws, wsb, None)
     assert call(K=-1) == 1
     assert call(step=float("inf")) == 1
-    assert call(flags=0x4) == 1          # unknown ablation flag
+    assert call(flags=0x8) == 1          # unknown flag
     assert call(K=65) == 2
     assert call(ws=None) == 3
     assert call(wsb=16) == 3

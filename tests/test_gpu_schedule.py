@@ -48,11 +48,12 @@ def test_workloads(cfg, problems, K, gpu):
     assert np.all(unfilled == 0)
 
 
-@pytest.mark.parametrize("flags", [taot.SCH_NO_TOPO, taot.SCH_NO_FLOW, taot.SCH_NO_TOPO | taot.SCH_NO_FLOW])
+@pytest.mark.parametrize("flags", [taot.SCH_NO_TOPO, taot.SCH_NO_FLOW, taot.SCH_NO_TOPO | taot.SCH_NO_FLOW,
+                                   taot.SCH_ROW_PRIORITY, taot.SCH_ROW_PRIORITY | taot.SCH_NO_TOPO])
 @pytest.mark.parametrize("cfg,problems", [(1, list(range(0, 58, 8))), (3, [0, 977])])
 def test_score_ablations(cfg, problems, flags, gpu):
-    """The Phase-2 score ablations, bit-exact against the oracle with the
-    same flags."""
+    """The Phase-2 ablations (score terms dropped, row-priority matching),
+    bit-exact against the oracle with the same flags."""
     w = W.WORKLOADS[cfg]
     print(f"[schedule parity] workload {cfg} problems {problems} flags {flags}", flush=True)
     _, L = oracle_inputs(w, problems)

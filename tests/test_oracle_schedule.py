@@ -114,7 +114,27 @@ def test_phase2_micro_ablations():
         se, sa, _ = O.phase2(*args2, K=1, flags=flags)
         assert se[0].tolist() == [-1, -1, 0, 0] and sa[0].tolist() == [0, 0, 3, 2]
     with pytest.raises(ValueError):
-        O.phase2(*args, K=1, flags=0x4)
+        O.phase2(*args, K=1, flags=0x8)
+
+
+def test_phase2_micro_row_priority():
+    """R = 4, nodes {0,1} and {2,3}, alpha = 5, K = 1, no flow hint.  Expert 0
+    (home 0) spills 6, expert 1 (home 2) spills 2; ranks 1 and 3 have spare 3.
+    Scores: rank 1: expert 0 min(6,3) + 5 = 8, expert 1 2 + 1.25 = 3.25;
+    rank 3: expert 0 3 + 1.25 = 4.25, expert 1 2 + 5 = 7.
+    Column priority: each rank takes its own best, 0 on rank 1 (3 tokens) and
+    1 on rank 3 (2 tokens), in one inner iteration.  Row priority: expert 0
+    (largest spill) goes first and takes rank 1 (8), then rank 3 (4.25), 3
+    tokens each, leaving expert 1 no slot."""
+    C = np.array([[0, 1, 4, 4], [1, 0, 4, 4], [4, 4, 0, 1], [4, 4, 1, 0]], np.float32)
+    Bp, _ = O.topology_pref(C)
+    T = np.zeros((4, 4), np.float32)
+    home = np.array([0, 2], np.int32)
+    args = ([6, 2], [0, 3, 0, 3], [6, 0, 2, 0], 5.0, home, T, Bp)
+    se, sa, used = O.phase2(*args, K=1)
+    assert se[0].tolist() == [-1, 0, -1, 1] and sa[0].tolist() == [0, 3, 0, 2] and used[0] == 1
+    se, sa, used = O.phase2(*args, K=1, flags=O.SCH_ROW_PRIORITY)
+    assert se[0].tolist() == [-1, 0, -1, 0] and sa[0].tolist() == [0, 3, 0, 3] and used[0] == 2
 
 
 def test_phase3_micro():
