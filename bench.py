@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--other-steps", type=int, default=3,
                     help="timed steps for the planner latency of workloads 1-4 other than --workload (0: skip)")
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--report", default=None, metavar="P1,P2,...",
+                    help="plan --workload once and print the planner's four-part report for these "
+                         "problems (layers) instead of benchmarking")
+    ap.add_argument("--report-file", default=None, help="write the --report text here instead of stdout")
     ap.add_argument("--quality", action="store_true",
                     help="print the plan-quality table of the Phase-2 score ablations on --workload "
                          "(every problem of the batch, no timing) instead of benchmarking")
@@ -234,6 +238,22 @@ def main():
     B, R, E, N = w.B, w.R, w.E, w.N
     if args.quality:
         plan_quality_table(w, K, dev)
+        return
+    if args.report is not None:
+        thr, seeds = W.tables(w)
+        ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
+        W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev),
+                         torch.from_numpy(seeds.view(np.int64)).to(dev), B, E, R, w.tokens, w.k, ids)
+        home = torch.from_numpy(W.home_map(w)).to(dev)
+        plan = taot.plan_step(ids, home, torch.from_numpy(W.cost_matrix(w)).to(dev), E, w.eps, w.iters, K,
+                              price_step=w.price_step)
+        torch.cuda.synchronize()
+        text = taot.plan_report(plan, home, K, problems=[int(x) for x in args.report.split(",") if x.strip()])
+        if args.report_file:
+            with open(args.report_file, "w") as fh:
+                fh.write(text)
+        else:
+            sys.stdout.write(text)
         return
     log(f"[bench] workload {w.index}: {w.name}; B={B} R={R} E={E} N={N} iters={w.iters} K={K}")
     run = run_workload(w, K, args.steps, args.warmup, dev)

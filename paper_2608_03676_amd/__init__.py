@@ -286,3 +286,62 @@ def plan_quality(load_r: torch.Tensor, home: torch.Tensor, sched: Schedule, K: i
     intra = (valid & same).sum(1)
     inter = (valid & ~same).sum(1)
     return Quality(la, rho, intra, inter, intra.double() + w_inter * inter.double())
+
+
+def plan_report(plan: Plan, home: torch.Tensor, K: int, problems=None, ranks_per_node: int = 8,
+                w_inter: float = 3.0) -> str:
+    """The planner's per-invocation report for the given problems (layers):
+    (1) per-rank and per-expert load before routing, hot ranks and hot
+    experts marked; (2) the cloning plan, each cloned expert's slot, whether
+    the copy is intra- or inter-node and the tokens it takes, then the copy
+    counts and weighted cost; (3) the projected per-rank load; (4) imbalance
+    before and after, the peak-load reduction, the fraction of tokens
+    rerouted and the final copy counts and cost (Sec. 4 / appendix report).
+    Host-side formatting of a finished plan."""
+    L, sched = plan.loads, plan.schedule
+    q = plan_quality(L.load_r, home, sched, K, ranks_per_node, w_inter)
+    load_r, load_e = L.load_r.cpu().numpy(), L.load_e.cpu().numpy()
+    excess, spill = L.excess.cpu().numpy(), L.spill.cpu().numpy()
+    rho0, la, rho1 = L.rho.cpu().numpy(), q.load_after.cpu().numpy(), q.rho_after.cpu().numpy()
+    se, X = sched.slot_expert.cpu().numpy(), sched.X.cpu().numpy()
+    hm = home.cpu().numpy()
+    B, R = load_r.shape
+    problems = range(B) if problems is None else problems
+    out = []
+
+    def ranks(vals, marks=None):
+        cells = [f"{r:4d}:{int(v):>9d}{'*' if marks is not None and marks[r] else ' '}" for r, v in enumerate(vals)]
+        return ["   " + " ".join(cells[i:i + 8]) for i in range(0, len(cells), 8)]
+
+    for b in problems:
+        tot = int(load_r[b].sum())
+        mean = tot / R if R else 0.0
+        out.append(f"== plan report, problem {b}: R = {R}, E = {hm.shape[0]}, K = {K}, "
+                   f"L = {tot}, mean {mean:.1f} ==")
+        out.append("[1] load before routing (* hot rank: load above the integer mean)")
+        out += ranks(load_r[b], excess[b] > 0)
+        hot = np.nonzero(spill[b] > 0)[0]
+        out.append(f"    hot experts (spill > 0): {len(hot)}")
+        for e in hot:
+            out.append(f"      expert {e:5d} on rank {hm[e]:4d}: load {int(load_e[b, e])}, spill {int(spill[b, e])}")
+        out.append("[2] cloning plan")
+        moved_tot, ni, no = 0, 0, 0
+        for s_ in np.nonzero(se[b] >= 0)[0]:
+            e, host = int(se[b, s_]), int(s_) // K
+            moved = int(X[b, :, s_].sum())
+            moved_tot += moved
+            intra = hm[e] // ranks_per_node == host // ranks_per_node
+            ni, no = ni + intra, no + (not intra)
+            out.append(f"      expert {e:5d} (rank {hm[e]:4d}) -> slot {s_ % K} of rank {host:4d}: "
+                       f"{'intra' if intra else 'inter'}-node, {moved} tokens")
+        out.append(f"    topology: {ni} intra-node, {no} inter-node copies; weighted cost "
+                   f"{ni + w_inter * no:.1f} (intra + {w_inter:g} x inter)")
+        out.append("[3] projected load after routing")
+        out += ranks(la[b])
+        pk0, pk1 = int(load_r[b].max()), int(la[b].max())
+        out.append("[4] summary")
+        out.append(f"    imbalance rho {rho0[b]:.4f} -> {rho1[b]:.4f}; peak load {pk0} -> {pk1} "
+                   f"({100.0 * (pk0 - pk1) / pk0 if pk0 else 0.0:.1f} % lower); rerouted {moved_tot} of "
+                   f"{tot} tokens ({100.0 * moved_tot / tot if tot else 0.0:.2f} %); "
+                   f"copies {ni} intra / {no} inter, weighted cost {ni + w_inter * no:.1f}")
+    return "\n".join(out) + "\n"
