@@ -48,6 +48,10 @@ def parse():
     ap.add_argument("--quality", action="store_true",
                     help="print the plan-quality table of the Phase-2 score ablations on --workload "
                          "(every problem of the batch, no timing) instead of benchmarking")
+    ap.add_argument("--hot-rank", action="store_true",
+                    help="sweep the hot-rank workloads of the paper's scalability study (EP degree, hot "
+                         "fraction, guest slots): plan quality and planner latency per point, instead of "
+                         "benchmarking --workload")
     return ap.parse_args()
 
 
@@ -102,17 +106,13 @@ def copy_calibration(mib):
 def run_workload(w, K, steps, warmup, dev):
     """Device-generated inputs, preallocated outputs, `warmup` untimed steps,
     then `steps` timed steps (HIP events on the launch stream)."""
-    import numpy as np
     import torch
 
     import paper_2608_03676_amd as taot
     import workloads as W
     B, R, E, N = w.B, w.R, w.E, w.N
     t0 = time.time()
-    thr, seeds = W.tables(w)
-    ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
-    W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
-                     B, E, R, w.tokens, w.k, ids)
+    ids = W.workload_ids_device(w, dev)
     home_np = W.home_map(w)
     C_np = W.cost_matrix(w)
     Bp_np, Ba_np = taot.topology_pref(C_np)
@@ -177,16 +177,12 @@ def plan_quality_table(w, K, dev):
     matching (round_schedule flags) on one batch: rho before and after the planned moves, replicas
     inside / across nodes (node = rank // 8) and the weighted cost intra +
     3 inter, mean and standard deviation over the batch's problems."""
-    import numpy as np
     import torch
 
     import paper_2608_03676_amd as taot
     import workloads as W
     B, R, E, N = w.B, w.R, w.E, w.N
-    thr, seeds = W.tables(w)
-    ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
-    W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
-                     B, E, R, w.tokens, w.k, ids)
+    ids = W.workload_ids_device(w, dev)
     home = torch.from_numpy(W.home_map(w)).to(dev)
     C_np = W.cost_matrix(w)
     Bp_np, Ba_np = taot.topology_pref(C_np)
@@ -217,6 +213,65 @@ def plan_quality_table(w, K, dev):
     print(json.dumps({"plan_quality": rows, "workload": w.index, "K": K}), flush=True)
 
 
+HOT_RANK_PANELS = (
+    ("EP degree (hot fraction 0.5, K = 2)", [(ep, 0.5, 2) for ep in (4, 8, 16, 32)]),
+    ("hot fraction (EP16, K = 2)", [(16, f, 2) for f in (0.3, 0.5, 0.7, 0.9)]),
+    ("guest slots per rank (EP16, hot fraction 0.5)", [(16, 0.5, K) for K in (1, 2, 4, 8, 16)]),
+)
+
+
+def hot_rank_sweep(dev, steps, warmup):
+    """The three sweeps of the paper's scalability study (Sec. 4.4) on the
+    hot-rank workloads, 48 problems per point: the hottest rank's share of
+    the load, rho before and after the planned moves, replicas inside and
+    across nodes and the weighted cost intra + 3 inter for the full score,
+    the weighted cost and rho after without the topology term, and the
+    planner latency per step (all 48 problems) from HIP events."""
+    import torch
+
+    import paper_2608_03676_amd as taot
+    import workloads as W
+    out = []
+    for title, points in HOT_RANK_PANELS:
+        rows = []
+        for ep, frac, K in points:
+            w = W.llep_workload(ep, frac, K)
+            log(f"[hot rank] EP{ep} frac {frac} K={K}")
+            run = run_workload(w, K, steps, warmup, dev)
+            L, F = run["loads"], run["flow"]
+            home = torch.from_numpy(run["home_np"]).to(dev)
+            Bp, Ba = (torch.from_numpy(run[x]).to(dev) for x in ("Bp_np", "Ba_np"))
+            load = L.load_r.double()
+            share = (load.max(1).values / load.sum(1)).cpu().numpy()
+            res = dict(ep=ep, frac=frac, K=K, hot_share=float(share.mean()),
+                       rho_before=float(L.rho.mean()), ms_per_step=run["ms_step"],
+                       us_per_problem=1e3 * run["ms_step"] / w.B)
+            for tag, flags in (("", 0), ("_no_topo", taot.SCH_NO_TOPO)):
+                s = taot.round_schedule(L.n, L.spill, L.spare, L.excess, L.alpha, home, F.T, Bp, Ba, K,
+                                        w.price_step, 0, flags=flags)
+                q = taot.plan_quality(L.load_r, home, s, K, ranks_per_node=8, w_inter=3.0)
+                res["rho_after" + tag] = float(q.rho_after.mean())
+                res["intra" + tag] = float(q.intra.double().mean())
+                res["inter" + tag] = float(q.inter.double().mean())
+                res["weighted" + tag] = float(q.weighted.mean())
+                res["unfilled" + tag] = int(s.unfilled.sum())
+            rows.append(res)
+            del run
+            torch.cuda.empty_cache()
+        out.append(dict(panel=title, rows=rows))
+        print(f"hot-rank sweep, {title}: 48 problems per point, means over the problems")
+        print(f"{'EP':>4} {'frac':>5} {'K':>3} {'hot share':>9} {'rho before':>10} {'rho after':>9} {'intra':>6} "
+              f"{'inter':>6} {'weighted':>8} | {'no topology: rho after':>22} {'weighted':>8} | "
+              f"{'planner ms':>10} {'us/problem':>10}")
+        for r in rows:
+            print(f"{r['ep']:>4} {r['frac']:>5.1f} {r['K']:>3} {r['hot_share']:>9.4f} {r['rho_before']:>10.4f} "
+                  f"{r['rho_after']:>9.4f} {r['intra']:>6.1f} {r['inter']:>6.1f} {r['weighted']:>8.1f} | "
+                  f"{r['rho_after_no_topo']:>22.4f} {r['weighted_no_topo']:>8.1f} | {r['ms_per_step']:>10.3f} "
+                  f"{r['us_per_problem']:>10.1f}")
+        print(flush=True)
+    print(json.dumps({"hot_rank_sweep": out}), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -233,6 +288,9 @@ def main():
     import workloads as W
 
     dev = torch.device("cuda:0")
+    if args.hot_rank:
+        hot_rank_sweep(dev, args.steps, args.warmup)
+        return
     w = W.WORKLOADS[args.workload]
     K = w.K if args.K is None else args.K
     B, R, E, N = w.B, w.R, w.E, w.N
@@ -240,10 +298,7 @@ def main():
         plan_quality_table(w, K, dev)
         return
     if args.report is not None:
-        thr, seeds = W.tables(w)
-        ids = torch.empty((B, R, N), dtype=torch.int32, device=dev)
-        W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev),
-                         torch.from_numpy(seeds.view(np.int64)).to(dev), B, E, R, w.tokens, w.k, ids)
+        ids = W.workload_ids_device(w, dev)
         home = torch.from_numpy(W.home_map(w)).to(dev)
         plan = taot.plan_step(ids, home, torch.from_numpy(W.cost_matrix(w)).to(dev), E, w.eps, w.iters, K,
                               price_step=w.price_step)

@@ -26,10 +26,7 @@ def full(gpu):
     w = W.WORKLOADS[3]
     B, R, E, N = w.B, w.R, w.E, w.N
     print(f"[fullsize] workload 3: B={B} R={R} E={E} N={N}", flush=True)
-    thr, seeds = W.tables(w)
-    ids = torch.empty((B, R, N), dtype=torch.int32, device=gpu)
-    W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(gpu), torch.from_numpy(seeds.view(np.int64)).to(gpu),
-                     B, E, R, w.tokens, w.k, ids)
+    ids = W.workload_ids_device(w, gpu)
     home_np = W.home_map(w)
     C_np = W.cost_matrix(w)
     Bp_np, Ba_np = taot.topology_pref(C_np)

@@ -102,17 +102,17 @@ def test_deterministic(gpu):
 def test_device_generator_matches_host_twin(gpu):
     """The device twin of the input generator reproduces the host ids bit for bit."""
     dev = torch.device("cuda:0")
-    for cfg, problems in ((0, [0]), (3, [5, 1900]), (4, [1])):
-        w = W.WORKLOADS[cfg]
+    for w, problems in ((W.WORKLOADS[0], [0]), (W.WORKLOADS[3], [5, 1900]), (W.WORKLOADS[4], [1]),
+                        (W.llep_workload(32, 0.7), [0, 47])):
         thr, seeds = W.tables(w, problems)
         B = len(problems)
         ids = torch.empty((B, w.R, w.N), dtype=torch.int32, device=dev)
         W.gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
-                         B, w.E, w.R, w.tokens, w.k, ids)
+                         B, w.E, w.R, *w.draw_shape, ids)
         torch.cuda.synchronize()
         got = ids.cpu().numpy()
         for q, b in enumerate(problems):
             rows = [0, w.R // 2, w.R - 1]
             for r in rows:
-                ref = W.gen_ids_host(thr[q], int(seeds[q]), w.R, w.tokens, w.k, r, r + 1)[0]
-                assert np.array_equal(got[q, r], ref), (cfg, b, r)
+                ref = W.gen_ids_host(thr[q], int(seeds[q]), w.R, *w.draw_shape, r, r + 1)[0]
+                assert np.array_equal(got[q, r], ref), (w.name, b, r)

@@ -272,3 +272,22 @@ def test_supply_scaling_and_column_cap():
     np.testing.assert_allclose(T.sum(), b.sum(), rtol=1e-9)
     # rows sum to gamma * a with gamma = 9/12
     np.testing.assert_allclose(T.sum(1), a * 9.0 / 12.0, rtol=1e-6)
+
+
+@pytest.mark.parametrize("eps,gamma", [(3.0, 1.0), (0.08, 1.0), (3.0, 0.8)])
+def test_single_overloaded_rank(eps, gamma):
+    """One supply row (one overloaded rank, as in the hot-rank workloads of
+    Sec. 4.4): the column marginals alone fix the plan, T[h] = d, whatever
+    the costs and eps; with supply above demand gamma scales it back."""
+    rng = np.random.default_rng(11)
+    R = 16
+    C = W.cost_matrix_for(R, ("two_tier", 1.0, 3.0)).astype(np.float64)
+    h = 5
+    b = rng.integers(1, 900, size=R).astype(float)
+    b[h] = 0
+    a = np.zeros(R)
+    a[h] = b.sum() / gamma
+    P = O.sinkhorn(a, b, C, eps=eps, iters=3)
+    T = P.T[0]
+    np.testing.assert_allclose(T[h], b, rtol=1e-12, atol=0)
+    assert np.all(np.delete(T, h, axis=0) == 0)

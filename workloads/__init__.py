@@ -11,9 +11,16 @@ per token as k = 8 distinct experts by successive sampling without
 replacement from a Zipf law over a seeded permutation of the experts (see
 gen_ids.h for the exact counter-based definition).
 
+A second family, `llep_workload(ep, frac, K)`, follows the imbalance
+construction of the paper's scalability study (Sec. 4.4): in every problem a
+seeded hot rank receives a fraction `frac` of the routing choices and the
+rest go to uniformly random experts, on a Qwen3-30B-A3B-shaped layer (128
+experts, top-8, 48 layers) at EP 4-32, with the paper's two-tier cost
+(1 inside a node, lambda = 3 across nodes) and eps = lambda.
+
 The paper's own routing came from Qwen3-30B-A3B on the Pile test split
-(Sec. 4.1); neither is available here, so these skewed synthetic loads stand
-in for it.
+(Sec. 4.1); neither is available here, so these synthetic loads stand in
+for it.
 """
 from __future__ import annotations
 
@@ -50,7 +57,7 @@ class Workload:
     tokens: int            # tokens per source rank
     k: int                 # top-k
     home: str              # "block" (e // (E/R)), "identity" (e), "roundrobin" (e mod R)
-    zipf: tuple            # ("fixed", s) or ("uniform", lo, hi)
+    zipf: tuple            # ("fixed", s) | ("uniform", lo, hi) | ("hot_rank", frac)
     spike: Optional[tuple]  # (fraction of experts, factor) or None
     cost: tuple            # ("two_tier", intra, inter) | ("three_tier", node, rack, far, rack_ranks)
                            # | ("fat_tree", node, leaf, far, leaf_ranks)
@@ -58,6 +65,8 @@ class Workload:
     iters: int             # Sinkhorn iterations
     K: int = 2             # guest slots per rank
     price_step: float = 2.0 ** -6
+    distinct: bool = True  # a token's k choices are distinct experts (else drawn independently)
+    seed: Optional[int] = None  # master seed (default 20260801 + index)
 
     @property
     def N(self) -> int:
@@ -65,8 +74,14 @@ class Workload:
         return self.tokens * self.k
 
     @property
+    def draw_shape(self):
+        """(tokens, choices per token) as passed to the generator: independent
+        choices are k draws of one choice each, so no choice is ever redrawn."""
+        return (self.tokens, self.k) if self.distinct else (self.tokens * self.k, 1)
+
+    @property
     def master_seed(self) -> int:
-        return 20260801 + self.index
+        return 20260801 + self.index if self.seed is None else self.seed
 
 
 WORKLOADS = [
@@ -86,6 +101,34 @@ WORKLOADS = [
              B=64, R=1024, E=4096, tokens=8192, k=8, home="block", zipf=("fixed", 1.5), spike=None,
              cost=("fat_tree", 1.0, 4.0, 16.0, 64), eps=0.08, iters=2000),
 ]
+
+
+LLEP_EP = (4, 8, 16, 32)
+LLEP_FRAC = (0.3, 0.5, 0.7, 0.9)
+LLEP_K = (1, 2, 4, 8, 16)
+
+
+def llep_workload(ep: int, frac: float, K: int = 2) -> Workload:
+    """Hot-rank workload of the paper's scalability study (Sec. 4.4) at EP
+    degree `ep` and hot fraction `frac`: 48 problems (one per MoE layer of a
+    Qwen3-30B-A3B-shaped model: 128 experts in blocks of 128 / ep per rank,
+    top-8), 8192 tokens per rank (a 32768-token sequence over 4-way tensor
+    parallelism, Sec. 4.1), cost 1 inside a node of 8 ranks and lambda = 3
+    across nodes (Sec. A.1), eps = lambda (Sec. A.2), 200 iterations."""
+    if ep < 1 or 128 % ep or not 0.0 <= frac <= 1.0:
+        raise ValueError(f"llep_workload: ep must divide 128 and 0 <= frac <= 1 (got {ep}, {frac})")
+    return Workload(100 + ep, f"LLEP-style hot rank: EP{ep}, {round(100 * frac)}% to one rank, K={K}",
+                    B=48, R=ep, E=128, tokens=8192, k=8, home="block", zipf=("hot_rank", float(frac)),
+                    spike=None, cost=("two_tier", 1.0, 3.0), eps=3.0, iters=200, K=K, distinct=False,
+                    seed=20260901 + 1000 * ep + round(1000 * frac))
+
+
+def hot_rank(w: Workload, b: int) -> int:
+    """The overloaded rank of problem b of a hot-rank workload."""
+    if w.zipf[0] != "hot_rank":
+        raise ValueError("hot_rank: not a hot-rank workload")
+    rng = np.random.Generator(np.random.PCG64([w.master_seed, b]))
+    return int(rng.integers(w.R))
 
 
 def home_map(w: Workload) -> np.ndarray:
@@ -129,7 +172,16 @@ def problem_seed(w: Workload, b: int) -> int:
 
 
 def expert_weights(w: Workload, b: int) -> np.ndarray:
-    """Unnormalised routing weight of each expert for problem b (fp64)."""
+    """Unnormalised routing weight of each expert for problem b (fp64).
+
+    Hot-rank law: a choice goes with probability frac to a uniformly chosen
+    expert of the hot rank and otherwise to a uniformly chosen expert of all
+    E, so the hot rank's expected share of the choices is
+    frac + (1 - frac) / R when every rank homes E / R experts."""
+    if w.zipf[0] == "hot_rank":
+        frac = w.zipf[1]
+        hot = home_map(w) == hot_rank(w, b)
+        return np.full(w.E, (1.0 - frac) / w.E) + np.where(hot, frac / hot.sum(), 0.0)
     rng = np.random.Generator(np.random.PCG64([w.master_seed, b]))
     perm = rng.permutation(w.E)
     if w.zipf[0] == "fixed":
@@ -197,7 +249,7 @@ def gen_ids_host(thr: np.ndarray, seed: int, R: int, T: int, k: int, r0: int = 0
 
 def problem_ids_host(w: Workload, b: int, r0: int = 0, r1: Optional[int] = None) -> np.ndarray:
     thr, seeds = tables(w, [b])
-    return gen_ids_host(thr[0], int(seeds[0]), w.R, w.tokens, w.k, r0, r1)
+    return gen_ids_host(thr[0], int(seeds[0]), w.R, *w.draw_shape, r0, r1)
 
 
 def _dev():
@@ -212,6 +264,18 @@ def _dev():
                                        ctypes.c_void_p]
         _dev_lib = lib
     return _dev_lib
+
+
+def workload_ids_device(w: Workload, dev, problems=None):
+    """ids [P][R][N] int32 on `dev` for the given problems (all by default),
+    made by the device twin."""
+    import torch
+    thr, seeds = tables(w, problems)
+    P = len(seeds)
+    ids = torch.empty((P, w.R, w.N), dtype=torch.int32, device=dev)
+    gen_ids_device(torch.from_numpy(thr.view(np.int64)).to(dev), torch.from_numpy(seeds.view(np.int64)).to(dev),
+                   P, w.E, w.R, *w.draw_shape, ids)
+    return ids
 
 
 def gen_ids_device(thr_dev, seeds_dev, B: int, E: int, R: int, T: int, k: int, ids_dev, stream=None):
