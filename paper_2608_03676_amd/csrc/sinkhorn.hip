@@ -853,6 +853,22 @@ __device__ __forceinline__ float reduce4(float (&p)[4], int lane) {
   y = y + dpp<0xB1>(y);               // quad_perm [1,0,3,2]
   return y;
 }
+// Sums 8 per-lane values over the 32 lanes of each half-wave; lane l ends
+// with the total of value 4 b4 + 2 b2 + b3 of its half (bk = bit k of l).
+// The steps pair lanes l ^ 16 (permlane16 swap: values 0-3 stay in the lower
+// row, 4-7 go to the upper), l <-> 15 - l (row_mirror, two independent
+// chains), l <-> 7 - l (row_half_mirror), l ^ 2 and l ^ 1 (quad_perm).
+__device__ __forceinline__ float reduce8h(float (&p)[8], int lane) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) { swap16(p[k], p[k + 4]); p[k] = p[k] + p[k + 4]; }
+  const bool b3 = lane & 8, b2 = lane & 4;
+  const float y0 = (b3 ? p[1] : p[0]) + dpp<0x140>(b3 ? p[0] : p[1]);  // value 4 b4 + b3
+  const float y1 = (b3 ? p[3] : p[2]) + dpp<0x140>(b3 ? p[2] : p[3]);  // value 4 b4 + 2 + b3
+  float z = (b2 ? y1 : y0) + dpp<0x141>(b2 ? y0 : y1);
+  z = z + dpp<0x4E>(z);  // quad_perm [2,3,0,1]
+  z = z + dpp<0xB1>(z);  // quad_perm [1,0,3,2]
+  return z;
+}
 // Max and sum over the 32 lanes of each half-wave (bitwise the same in every
 // lane of the half).
 __device__ __forceinline__ float half_max(float x) {
@@ -970,9 +986,14 @@ __device__ __forceinline__ void half_solve(const SkParams& p, int64_t pb, int32_
 #pragma unroll
   for (int q = 0; q < MC; ++q)
     if (q < c8) UST(q, RV(q) ? 1.f : 0.f);
-  float sAq[MC];
+  // Row half-steps take chunks in pairs (q, q + 1): reduce8h leaves the total
+  // of row PR(q) in lane l; an odd last chunk goes through reduce4.
+#define PR(q) (8 * ((q) + ((lane >> 4) & 1)) + 4 * h + 2 * ((lane >> 2) & 1) + ((lane >> 3) & 1))
+  float sAp[MC / 2];
 #pragma unroll
-  for (int q = 0; q < MC; ++q) sAq[q] = RV(q) ? sAl[8 * q + (lane >> 3)] : 1.f;
+  for (int q = 0; q < MC; q += 2) sAp[q / 2] = PR(q) < nh ? sAl[PR(q)] : 1.f;
+  const int qt = c8 - 1;  // the odd last chunk, when c8 is odd
+  const float sAt = (c8 & 1) && RV(qt) ? sAl[8 * qt + (lane >> 3)] : 1.f;
 
   int32_t it = 1;
   bool skip_row = true;
@@ -991,22 +1012,39 @@ __device__ __forceinline__ void half_solve(const SkParams& p, int64_t pb, int32_
         // ---- row half-step: u_i = s~_i / sum_c Kt_ic v_c ----------------------------
         uint32_t lo = 0xFFFFFFFFu, hi = 0u;
 #pragma unroll
-        for (int q = 0; q < MC; ++q) {
+        for (int q = 0; q < MC; q += 2) {
           if (q >= c8) break;
-          float pp[4];
+          if (q + 1 < c8) {
+            float pp[8];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float acc = K[4 * q + r][0] * v[0];
+            for (int r = 0; r < 8; ++r) {
+              float acc = K[4 * q + r][0] * v[0];
 #pragma unroll
-            for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[4 * q + r][c], v[c], acc);
-            pp[r] = acc;
+              for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[4 * q + r][c], v[c], acc);
+              pp[r] = acc;
+            }
+            const float y = reduce8h(pp, lane);  // all lanes take part
+            const float un = sAp[q / 2] * frcp(PR(q) < nh ? y : 1.f);
+            const uint32_t bits = __float_as_uint(un);
+            lo = bits < lo ? bits : lo;
+            hi = bits > hi ? bits : hi;
+            if ((lane & 3) == 0) ul[PR(q)] = un;
+          } else {
+            float pp[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              float acc = K[4 * q + r][0] * v[0];
+#pragma unroll
+              for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[4 * q + r][c], v[c], acc);
+              pp[r] = acc;
+            }
+            const float y = reduce4(pp, lane);
+            const float un = sAt * frcp(RV(q) ? y : 1.f);
+            const uint32_t bits = __float_as_uint(un);
+            lo = bits < lo ? bits : lo;
+            hi = bits > hi ? bits : hi;
+            UST(q, un);
           }
-          const float y = reduce4(pp, lane);  // all lanes take part
-          const float un = sAq[q] * frcp(RV(q) ? y : 1.f);
-          const uint32_t bits = __float_as_uint(un);
-          lo = bits < lo ? bits : lo;
-          hi = bits > hi ? bits : hi;
-          UST(q, un);
         }
         const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
         if (__ballot(fail) != 0) {
@@ -1164,6 +1202,7 @@ __device__ __forceinline__ void half_solve(const SkParams& p, int64_t pb, int32_
   }
   if (lane == 0 && p.status) p.status[pb] = 0u;
 #undef UST
+#undef PR
 #undef GL
 #undef HR
 #undef RV
