@@ -68,3 +68,40 @@ def test_hot_rank_batch(ep, frac, K, gpu):
     assert np.array_equal(q.intra.cpu().numpy(), m["intra"]) and np.array_equal(q.inter.cpu().numpy(), m["inter"])
     if ep <= 8:  # one node: every replica stays inside it
         assert not m["inter"].any()
+
+
+@pytest.mark.parametrize("ep,frac,K", [(16, 0.0, 2), (16, 1.0, 2), (8, 1.0, 16)])
+def test_hot_rank_extremes(ep, frac, K, gpu):
+    """frac = 0 (uniform routing: small random imbalance, several overloaded
+    ranks or none) and frac = 1 (every choice on the hot rank's experts, the
+    other ranks idle): loads bit-exact, plan within tolerance, schedule
+    bit-exact, on a slice of the batch."""
+    w = W.llep_workload(ep, frac, K)
+    problems = [0, 17, 47]
+    print(f"[hot rank] EP{ep} frac {frac} K={K}: problems {problems}", flush=True)
+    home_np, C_np = W.home_map(w), W.cost_matrix(w)
+    Bp_np, Ba_np = taot.topology_pref(C_np)
+    home, C, Bp, Ba = (torch.from_numpy(x).to(gpu) for x in (home_np, C_np, Bp_np, Ba_np))
+    ids = W.workload_ids_device(w, gpu, problems)
+    L = taot.plan_loads(ids, home, w.E)
+    F = taot.sinkhorn_batched(L.supply, L.demand, C, w.eps, w.iters)
+    torch.cuda.synchronize()
+    ref = O.plan_loads(np.stack([W.problem_ids_host(w, b) for b in problems]), home_np, w.E)
+    for name, rname in (("n", "n"), ("excess", "excess"), ("spare", "spare"), ("spill", "spill")):
+        assert np.array_equal(getattr(L, name).cpu().numpy(), getattr(ref, rname)), name
+    if frac == 1.0:  # only the hot rank holds load
+        for q, b in enumerate(problems):
+            assert np.flatnonzero(ref.load[q]).tolist() == [W.hot_rank(w, b)]
+    a, d = ref.excess.astype(float), ref.spare.astype(float)
+    plan = O.sinkhorn(a, d, C_np.astype(float), w.eps, w.iters)
+    sinkhorn_check(F.T.cpu().numpy(), plan.T, a, d)
+    T32 = plan.T.astype(np.float32)
+    s = taot.round_schedule(L.n, L.spill, L.spare, L.excess, L.alpha, home, torch.from_numpy(T32).to(gpu), Bp, Ba,
+                            K, w.price_step, 0)
+    torch.cuda.synchronize()
+    se, sa, used = O.phase2(ref.spill, ref.spare, ref.excess, ref.alpha, home_np, T32, Bp_np, K)
+    X, unfilled, rounds, status = O.phase3(ref.n, se, sa, Ba_np, K, w.price_step)
+    assert np.array_equal(s.slot_expert.cpu().numpy(), se)
+    assert np.array_equal(s.slot_amount.cpu().numpy(), sa)
+    assert np.array_equal(s.X.cpu().numpy(), X)
+    assert np.array_equal(s.unfilled.cpu().numpy(), unfilled)
