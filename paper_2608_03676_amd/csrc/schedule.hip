@@ -549,6 +549,16 @@ struct LdsSmall {
   static constexpr int kNEC = 128;   // candidate experts (spill > 0) in LDS
   static constexpr int kWavesPerEU = 8;  // large batches: eight problems per compute unit (20 KB of LDS each at R = 256, K = 2)
 };
+struct LdsTiny {
+  static constexpr int kT = 64;      // one wave per problem: its barriers cost next to nothing
+  static constexpr int kTW = 1;      // R <= 64
+  static constexpr int kSC = 64;
+  static constexpr int kDC = 64;
+  static constexpr int kPL = 9;      // counts <= R*K <= 256
+  static constexpr int kMaxS = 256;
+  static constexpr int kNEC = 128;
+  static constexpr int kWavesPerEU = 8;
+};
 struct LdsLarge {
   static constexpr int kT = 1024;
   static constexpr int kTW = 16;     // R <= 1024
@@ -1405,7 +1415,7 @@ struct SchWs {
   size_t bytes;
 };
 
-// The tables are sized for the larger configuration, which either may use.
+// The tables are sized for the largest configuration, which any of them may use.
 SchWs carve_sched(void* ws, int32_t B, int32_t R, int32_t E, int32_t K) {
   Carver c{static_cast<char*>(ws)};
   SchWs w;
@@ -1510,7 +1520,8 @@ taot_status launch_schedule(const int32_t* n, const int64_t* spill, const int64_
   taot_status st = TAOT_OK;
   // the row-priority ablation lives in the general kernel only
   if (!(flags & TAOT_SCH_ROW_PRIORITY)) {
-    st = launch_lds_path<LdsSmall>(p, w, B, R, E, K, price_step, stream, launched);
+    st = launch_lds_path<LdsTiny>(p, w, B, R, E, K, price_step, stream, launched);
+    if (st == TAOT_OK && !launched) st = launch_lds_path<LdsSmall>(p, w, B, R, E, K, price_step, stream, launched);
     if (st == TAOT_OK && !launched) st = launch_lds_path<LdsLarge>(p, w, B, R, E, K, price_step, stream, launched);
   }
   if (st != TAOT_OK) return st;
