@@ -279,7 +279,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: the planner's problems are independent and "
-              f"this build has no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
+              f"the library has no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
