@@ -113,7 +113,7 @@ def llep_workload(ep: int, frac: float, K: int = 2) -> Workload:
     degree `ep` and hot fraction `frac`: 48 problems (one per MoE layer of a
     Qwen3-30B-A3B-shaped model: 128 experts in blocks of 128 / ep per rank,
     top-8), 8192 tokens per rank (a 32768-token sequence over 4-way tensor
-    parallelism, Sec. 4.1), cost 1 inside a node of 8 ranks and lambda = 3
+    parallelism, Appendix B), cost 1 inside a node of 8 ranks and lambda = 3
     across nodes (Sec. A.1), eps = lambda (Sec. A.2), 200 iterations."""
     if ep < 1 or 128 % ep or not 0.0 <= frac <= 1.0:
         raise ValueError(f"llep_workload: ep must divide 128 and 0 <= frac <= 1 (got {ep}, {frac})")
