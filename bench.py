@@ -225,8 +225,9 @@ def hot_rank_sweep(dev, steps, warmup):
     hot-rank workloads, 48 problems per point: the hottest rank's share of
     the load, rho before and after the planned moves, replicas inside and
     across nodes and the weighted cost intra + 3 inter for the full score,
-    the weighted cost and rho after without the topology term, and the
-    planner latency per step (all 48 problems) from HIP events."""
+    the weighted cost and rho after without the topology term, rho after
+    with row-priority matching, and the planner latency per step (all 48
+    problems) from HIP events."""
     import torch
 
     import paper_2608_03676_amd as taot
@@ -246,7 +247,7 @@ def hot_rank_sweep(dev, steps, warmup):
             res = dict(ep=ep, frac=frac, K=K, hot_share=float(share.mean()),
                        rho_before=float(L.rho.mean()), ms_per_step=run["ms_step"],
                        us_per_problem=1e3 * run["ms_step"] / w.B)
-            for tag, flags in (("", 0), ("_no_topo", taot.SCH_NO_TOPO)):
+            for tag, flags in (("", 0), ("_no_topo", taot.SCH_NO_TOPO), ("_row", taot.SCH_ROW_PRIORITY)):
                 s = taot.round_schedule(L.n, L.spill, L.spare, L.excess, L.alpha, home, F.T, Bp, Ba, K,
                                         w.price_step, 0, flags=flags)
                 q = taot.plan_quality(L.load_r, home, s, K, ranks_per_node=8, w_inter=3.0)
@@ -262,12 +263,12 @@ def hot_rank_sweep(dev, steps, warmup):
         print(f"hot-rank sweep, {title}: 48 problems per point, means over the problems")
         print(f"{'EP':>4} {'frac':>5} {'K':>3} {'hot share':>9} {'rho before':>10} {'rho after':>9} {'intra':>6} "
               f"{'inter':>6} {'weighted':>8} | {'no topology: rho after':>22} {'weighted':>8} | "
-              f"{'planner ms':>10} {'us/problem':>10}")
+              f"{'row priority: rho after':>23} | {'planner ms':>10} {'us/problem':>10}")
         for r in rows:
             print(f"{r['ep']:>4} {r['frac']:>5.1f} {r['K']:>3} {r['hot_share']:>9.4f} {r['rho_before']:>10.4f} "
                   f"{r['rho_after']:>9.4f} {r['intra']:>6.1f} {r['inter']:>6.1f} {r['weighted']:>8.1f} | "
-                  f"{r['rho_after_no_topo']:>22.4f} {r['weighted_no_topo']:>8.1f} | {r['ms_per_step']:>10.3f} "
-                  f"{r['us_per_problem']:>10.1f}")
+                  f"{r['rho_after_no_topo']:>22.4f} {r['weighted_no_topo']:>8.1f} | {r['rho_after_row']:>23.4f} | "
+                  f"{r['ms_per_step']:>10.3f} {r['us_per_problem']:>10.1f}")
         print(flush=True)
     print(json.dumps({"hot_rank_sweep": out}), flush=True)
 
