@@ -33,11 +33,13 @@ def lib():
         L.oracle_sinkhorn.argtypes = [_P, _P, _I32, _I32, _P, _I64, _F64, _I32, _I32, _F64, _I32,
                                       _P, _P, _P, _P, _P]
         L.oracle_topology_pref.argtypes = [_P, _I32, _P, _P]
+        L.oracle_column_cap.argtypes = [_P, _P, _I32, _I32]
         L.oracle_max_threads.argtypes = []
         L.oracle_phase2.argtypes = [_P] * 7 + [_I32] * 4 + [ctypes.c_uint32] + [_P] * 3
         L.oracle_phase3.argtypes = [_P] * 4 + [_I32] * 4 + [_F64, _I64] + [_P] * 4
         L.oracle_metrics.argtypes = [_P] * 4 + [_I32] * 5 + [_F64] + [_P] * 5
-        for f in (L.oracle_plan_loads, L.oracle_sinkhorn, L.oracle_topology_pref, L.oracle_phase2,
+        for f in (L.oracle_plan_loads, L.oracle_sinkhorn, L.oracle_topology_pref, L.oracle_column_cap,
+                  L.oracle_phase2,
                   L.oracle_phase3, L.oracle_metrics, L.oracle_max_threads):
             f.restype = ctypes.c_int
         _lib = L
@@ -111,6 +113,17 @@ def sinkhorn(a, b, C, eps: float, iters: int, domain: str = "log", tol: float = 
                                out.status.ctypes.data)
     _check(rc, "oracle_sinkhorn")
     return out
+
+
+def column_cap(T, b) -> np.ndarray:
+    """The column-cap step alone (Sec. A.2) on a copy of the plans T [B][R][R]."""
+    T = np.array(T, dtype=np.float64, copy=True)
+    b = _c(b, np.float64)
+    if T.ndim == 2:
+        T, b = T[None], b[None]
+    B, R = b.shape
+    _check(lib().oracle_column_cap(T.ctypes.data, b.ctypes.data, B, R), "oracle_column_cap")
+    return T
 
 
 def max_threads() -> int:

@@ -146,6 +146,18 @@ static double row_residual(const double* s, int32_t R, const double* C, double e
   return res;
 }
 
+/* Column cap (Sec. A.2): scale every column whose mass exceeds its demand
+ * back to the demand; columns at or below it are left alone. */
+static void column_cap_one(double* T, const double* b, int32_t R) {
+  for (int32_t j = 0; j < R; ++j) {
+    double c = 0.0;
+    for (int32_t i = 0; i < R; ++i) c += T[(int64_t)i * R + j];
+    double fac = b[j] / (c + ORACLE_EPS0);
+    if (fac > 1.0) fac = 1.0;
+    for (int32_t i = 0; i < R; ++i) T[(int64_t)i * R + j] *= fac;
+  }
+}
+
 static void sinkhorn_one(const double* a, const double* b, int32_t R, const double* C, double eps,
                          int32_t iters, int32_t domain, double tol, int32_t colcap, double* T,
                          double* f, double* g, int32_t* used, uint32_t* status) {
@@ -251,16 +263,8 @@ static void sinkhorn_one(const double* a, const double* b, int32_t R, const doub
     }
   }
 
-  if (colcap) {
-    /* column cap: T_ij <- T_ij * min(1, d_j / (sum_i T_ij + eps0)) */
-    for (int32_t j = 0; j < R; ++j) {
-      double c = 0.0;
-      for (int32_t i = 0; i < R; ++i) c += T[(int64_t)i * R + j];
-      double fac = b[j] / (c + ORACLE_EPS0);
-      if (fac > 1.0) fac = 1.0;
-      for (int32_t i = 0; i < R; ++i) T[(int64_t)i * R + j] *= fac;
-    }
-  }
+  /* column cap, once, on the final plan */
+  if (colcap) column_cap_one(T, b, R);
   free(s);
   free(t);
 }
@@ -278,6 +282,12 @@ int oracle_sinkhorn(const double* a, const double* b, int32_t B, int32_t R, cons
     sinkhorn_one(a + (int64_t)p * R, b + (int64_t)p * R, R, C + (int64_t)p * C_stride, eps, iters,
                  domain, tol, colcap, T + (int64_t)p * R * R, f + (int64_t)p * R,
                  g + (int64_t)p * R, used + p, status + p);
+  return 0;
+}
+
+int oracle_column_cap(double* T, const double* b, int32_t B, int32_t R) {
+  if (!T || !b || B < 0 || R <= 0) return -1;
+  for (int32_t p = 0; p < B; ++p) column_cap_one(T + (int64_t)p * R * R, b + (int64_t)p * R, R);
   return 0;
 }
 

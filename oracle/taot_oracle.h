@@ -66,6 +66,12 @@ int oracle_sinkhorn(const double* a, const double* b, int32_t B, int32_t R, cons
 /* Topology-preference matrices derived from C (fp32 input, fp64 output):
  *   Bpref[i][j] = cmin / C[i][j] for i != j (cmin = smallest off-diagonal cost), 0 on i == j;
  *   Bauct[i][j] = Bpref[i][j] for i != j, 1 on i == j. */
+/* The column-cap safeguard of Sec. A.2 on its own, in place on B plans
+ * T [B][R][R] with demands b [B][R]: c_j = sum_i T_ij, then
+ * T_ij <- T_ij * min(1, b_j / (c_j + eps0)).  oracle_sinkhorn applies this
+ * same step to its final plan when colcap != 0. */
+int oracle_column_cap(double* T, const double* b, int32_t B, int32_t R);
+
 int oracle_topology_pref(const float* C, int32_t R, double* Bpref, double* Bauct);
 
 /* Alg. 2 (Phase 2, column-priority matching) for B problems.

@@ -274,6 +274,46 @@ def test_supply_scaling_and_column_cap():
     np.testing.assert_allclose(T.sum(1), a * 9.0 / 12.0, rtol=1e-6)
 
 
+def test_column_cap_where_it_binds():
+    """The cap step alone (Sec. A.2) on hand-made plans whose columns exceed
+    their demand: such a column is scaled down to d_j / (c_j + eps0) of
+    itself; a column at or below its demand, or empty, is left as it is
+    (the factor is capped at 1, never scaled up); rows are not touched."""
+    T = np.array([[2.0, 1.0, 0.0, 3.0],
+                  [2.0, 1.0, 0.0, 1.0],
+                  [4.0, 0.0, 0.0, 0.0]])
+    T4 = np.zeros((4, 4))
+    T4[:3] = T
+    b = np.array([2.0, 5.0, 1.0, 4.0])   # column sums 8, 2, 0, 4
+    out = O.column_cap(T4, b)[0]
+    f0 = 2.0 / (8.0 + O.EPS0)             # binds: 8 -> 2
+    f3 = min(1.0, 4.0 / (4.0 + O.EPS0))   # at its demand: 1 - 2.5e-13
+    expect = T4.copy()
+    expect[:, 0] *= f0
+    expect[:, 3] *= f3
+    np.testing.assert_array_equal(out, expect)
+    np.testing.assert_allclose(out.sum(0), [2.0, 2.0, 0.0, 4.0], rtol=1e-12)
+    assert out[0, 1] == 1.0 and out[1, 1] == 1.0  # under its demand: not scaled up
+
+
+def test_column_cap_applies_once_to_the_final_plan():
+    """sinkhorn(colcap) equals the cap step applied to sinkhorn(no colcap),
+    bit for bit: the cap runs once, after the last iteration, on the final
+    plan (reading R8), at several iteration counts and with gamma < 1."""
+    rng = np.random.default_rng(5)
+    R = 9
+    C = rng.uniform(0.0, 3.0, (R, R))
+    a = np.zeros((2, R))
+    b = np.zeros((2, R))
+    a[0, :3], b[0, 3:] = rng.integers(1, 40, 3), rng.integers(1, 40, 6)
+    a[1, :4], b[1, 4:] = rng.integers(30, 90, 4), rng.integers(1, 20, 5)  # supply above demand
+    for iters in (1, 2, 7, 40):
+        P1 = O.sinkhorn(a, b, C, eps=0.3, iters=iters, colcap=True)
+        P0 = O.sinkhorn(a, b, C, eps=0.3, iters=iters, colcap=False)
+        assert P1.T.tobytes() == O.column_cap(P0.T, b).tobytes()
+        assert np.all(P1.T.sum(1) <= P0.T.sum(1) * (1 + 1e-15))
+
+
 @pytest.mark.parametrize("eps,gamma", [(3.0, 1.0), (0.08, 1.0), (3.0, 0.8)])
 def test_single_overloaded_rank(eps, gamma):
     """One supply row (one overloaded rank, as in the hot-rank workloads of
