@@ -39,8 +39,10 @@ typedef enum {
 
 /* Per-problem status bits (uint32_t status[B]). */
 #define TAOT_ST_BAD_ID 0x1u    /* plan_loads: routing ids outside [0, E) were skipped   */
-#define TAOT_ST_BAD_INPUT 0x2u /* a home rank outside [0, R), or a / b / C negative or
-                                  non-finite; the problem's outputs are zero        */
+#define TAOT_ST_BAD_INPUT 0x2u /* plan_loads: a home rank outside [0, R); sinkhorn: an
+                                  entry of a or b negative or non-finite, or any of
+                                  the R*R entries of the problem's C non-finite; the
+                                  problem's outputs are zero (f, g = -inf)          */
 #define TAOT_ST_ZERO_MASS 0x4u /* sinkhorn: total supply or demand is zero; T = 0      */
 #define TAOT_ST_UNFILLED 0x8u  /* round_schedule: the auction stopped at t_max with
                                   planned tokens left unassigned (`unfilled` > 0)   */
@@ -126,7 +128,9 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
  *
  *   a, b    [B][R] float   supply and demand (non-negative, finite).
  *   C       [R][R] float   cost; C_batch_stride = 0 shares one matrix, R*R gives
- *                          one per problem.  Finite.
+ *                          one per problem.  Any real values; every entry is
+ *                          checked, and a NaN or infinity anywhere in a
+ *                          problem's matrix marks that problem BAD_INPUT.
  *   eps     > 0            absolute entropic regulariser.
  *   iters   >= 1           Sinkhorn iterations (one iteration = u then v update).
  *   flags   TAOT_SK_*.

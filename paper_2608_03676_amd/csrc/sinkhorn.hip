@@ -101,7 +101,43 @@ struct SkParams {
   int64_t kt_stride;
   int32_t lds_kt_cap;    // Kt capacity (floats) of the LDS kernel
   int32_t all_streamed;  // every problem goes to the streamed kernel
+  const int32_t* cbad;   // [matrices][cchunks] 1 = the chunk of C holds a non-finite entry
+  int32_t cchunks;       // chunks of kScanChunk entries per cost matrix
 };
+
+// Cost validation.  Every entry of a problem's C is checked (not only those
+// the iterate reads): cost_scan_kernel marks each chunk of kScanChunk
+// entries that holds a NaN or an infinity, once per call for a shared C and
+// once per problem for per-problem costs; the class prepass and the LDS and
+// streamed kernels OR the chunk marks of their problem's matrix.
+constexpr int64_t kScanChunk = 65536;
+constexpr int kScanThreads = 256;
+__host__ __device__ constexpr int32_t scan_chunks(int32_t R) {
+  return (int32_t)(((int64_t)R * R + kScanChunk - 1) / kScanChunk);
+}
+
+__global__ void __launch_bounds__(kScanThreads)
+cost_scan_kernel(const float* __restrict__ C, int64_t R2, int32_t chunks, int32_t* __restrict__ cbad) {
+  const int64_t mat = blockIdx.x / chunks, ch = blockIdx.x % chunks;
+  const float* c = C + mat * R2;
+  const int64_t lo = ch * kScanChunk, hi = lo + kScanChunk < R2 ? lo + kScanChunk : R2;
+  int bad = 0;
+  for (int64_t q = lo + threadIdx.x; q < hi; q += kScanThreads) {
+    const float x = c[q];
+    bad |= !(x - x == 0.f);  // NaN or +-inf
+  }
+  bad = __syncthreads_or(bad);
+  if (threadIdx.x == 0) cbad[blockIdx.x] = bad ? 1 : 0;
+}
+
+// Whether problem pb's cost matrix holds a non-finite entry; the chunk marks
+// are read by lane (uniform result over the wave).
+__device__ __forceinline__ bool cost_bad_wave(const SkParams& p, int64_t pb) {
+  const int64_t base = (p.C_stride ? pb : 0) * p.cchunks;
+  bool bad = false;
+  for (int32_t k = threadIdx.x & (kWave - 1); k < p.cchunks; k += kWave) bad |= p.cbad[base + k] != 0;
+  return __ballot(bad) != 0;
+}
 
 // Block-wide exclusive compaction position of `flag` within an NT-thread chunk.
 template <int NT = kSkThreads>
@@ -157,6 +193,7 @@ __global__ void __launch_bounds__(NT) sinkhorn_kernel(SkParams p) {
   // ---- supply/demand: validation, mass, compaction of H and C ----------------
   if (tid == 0) sh_bad = 0;
   __syncthreads();
+  if (wid == 0 && cost_bad_wave(p, pb) && lane == 0) sh_bad = 1;
   double sa = 0.0, sd = 0.0;
   for (int32_t i = tid; i < R; i += NT) {
     const float ai = a[i], bi = bd[i];
@@ -210,13 +247,7 @@ __global__ void __launch_bounds__(NT) sinkhorn_kernel(SkParams p) {
     for (int32_t ii = wid; ii < nh; ii += NW) {
       const float* crow = Cb + (int64_t)hidx[ii] * R;
       float mx = -INFINITY;
-      bool badc = false;
-      for (int32_t j = lane; j < R; j += kWave) {
-        const float c = crow[j];
-        badc |= !(c == c) || c == INFINITY || c == -INFINITY;
-        mx = fmaxf(mx, -c * kappa);
-      }
-      if (badc) sh_bad = 1;
+      for (int32_t j = lane; j < R; j += kWave) mx = fmaxf(mx, -crow[j] * kappa);
       mx = wave_max(mx);
       float s = 0.f;
       for (int32_t j = lane; j < R; j += kWave) s += fexp2(-crow[j] * kappa - mx);
@@ -1238,7 +1269,6 @@ template <int NW, int W>
 __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int32_t* wl) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = NW == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform
-  const int gt = NW == 1 ? lane : (int)threadIdx.x;  // thread index within the problem's waves
   const int32_t R = p.R;
   // float arrays first: ul is read 16 bytes at a time
   float* sAl = reinterpret_cast<float*>(wl);  // [64] scaled supply
@@ -1248,8 +1278,7 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
   float* Sall = Gall + NW * 4 * kWave;        // [NW][64][4] column demands
   float* xbuf = Sall + NW * 4 * kWave;        // [2][NW][4][64] column exchange (NW > 1)
   int32_t* iw = reinterpret_cast<int32_t*>(reinterpret_cast<float*>(wl) + wave_lds_floats(NW));
-  int32_t* flag = iw;            // [4]: bad cost entry seen
-  int32_t* cpos = iw + 4;        // [R] compact column, -1 if not cold
+  int32_t* cpos = iw + 4;        // [R] compact column, -1 if not cold (iw[0..3] unused)
   int32_t* hpos = cpos + R;      // [R] compact row of rank i, -1 if not hot
   int32_t* cidx = hpos + R;      // [256]
   int32_t* hidx = cidx + 256;    // [64]
@@ -1283,39 +1312,23 @@ __device__ __forceinline__ void wave_problem(const SkParams& p, int64_t pb, int3
   double gamma = __shfl(sd, 0, kWave) / fmax(__shfl(sa, 0, kWave), kEps0);
   gamma = gamma < 1.0 ? gamma : 1.0;
   sAl[lane] = lane < nh ? (float)(gamma * (double)a[hidx[lane]]) : 0.f;  // zero padding to 64 rows
-  if (gt == 0) flag[0] = 0;
   psync<NW>();
   const float kappa = kLog2e / p.eps;
 
   // ---- first row update over all R columns (v = 1): F_i = log2 s~_i - LSE2_j(-C'_ij),
-  // rows dealt out over the waves
-  bool badc = false;
+  // rows dealt out over the waves (the class prepass has left problems with
+  // a non-finite cost to the LDS or streamed kernel)
   for (int32_t i = wv; i < nh; i += NW) {
     const float* crow = Cb + (int64_t)hidx[i] * R;
     float mx = -INFINITY;
-    for (int32_t j = lane; j < R; j += kWave) {
-      const float c = crow[j];
-      badc |= !(c == c) || c == INFINITY || c == -INFINITY;
-      mx = fmaxf(mx, -c * kappa);
-    }
+    for (int32_t j = lane; j < R; j += kWave) mx = fmaxf(mx, -crow[j] * kappa);
     mx = lanes_max(mx);
     float sum = 0.f;
     for (int32_t j = lane; j < R; j += kWave) sum += fexp2(-crow[j] * kappa - mx);
     sum = lanes_sum(sum);
     if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
   }
-  if (__ballot(badc) != 0 && lane == 0) flag[0] = 1;
   psync<NW>();
-  if (flag[0] != 0) {
-    if (p.T)
-      for (int64_t q = gt; q < (int64_t)R * R; q += NW * kWave) p.T[pb * R * R + q] = 0.f;
-    for (int32_t i = gt; i < R; i += NW * kWave) {
-      if (p.f) p.f[pb * R + i] = -INFINITY;
-      if (p.g) p.g[pb * R + i] = -INFINITY;
-    }
-    if (gt == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
-    return;
-  }
   if constexpr (NW == 1 && W == 2) {
     // one wave alone: the folded layout (every single class of the two-wave
     // kernel fits it)
@@ -1430,8 +1443,10 @@ __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* 
     nh += __popcll(__ballot(in && ai > 0.f));
     nc += __popcll(__ballot(in && bi > 0.f));
   }
-  int c = __ballot(bad) != 0 ? 0 : classify(nh, nc, p.flags);
-  if (c == 0 && __ballot(bad) == 0) c = wide_class(nh, nc, p.flags);
+  // invalid supplies, demands or costs: the LDS or streamed kernel reports them
+  const bool any_bad = __ballot(bad) != 0 || cost_bad_wave(p, pb);
+  int c = any_bad ? 0 : classify(nh, nc, p.flags);
+  if (c == 0 && !any_bad) c = wide_class(nh, nc, p.flags);
   if (lane == 0) cls[pb] = c;
 }
 
@@ -1785,7 +1800,7 @@ __device__ __forceinline__ void wide_problem(const SkParams& p, int64_t pb, int3
   float* vsh = part + kWideWaves * kWave * kWideMaxCpl;  // [16][64]
   float* gsh = vsh + kWave * kWideMaxCpl;           // [16][64]
   int32_t* iw = reinterpret_cast<int32_t*>(reinterpret_cast<float*>(wl) + wide_lds_floats());
-  int32_t* flag = iw;        // [4]: bad cost entry; column failure by parity
+  int32_t* flag = iw;        // [4]: flag[1 + parity] column failure of an iteration
   int32_t* cnt = iw + 4;     // [4]: nh, nc
   int32_t* cpos = iw + 8;    // [R]
   int32_t* hpos = cpos + R;  // [R]
@@ -1833,34 +1848,19 @@ __device__ __forceinline__ void wide_problem(const SkParams& p, int64_t pb, int3
   const int32_t nh = cnt[0], nc = cnt[1];
   const float kappa = kLog2e / p.eps;
 
-  // ---- first row update over all R columns (v = 1), rows dealt out over the waves
-  bool badc = false;
+  // ---- first row update over all R columns (v = 1), rows dealt out over the
+  // waves (problems with a non-finite cost never reach this kernel)
   for (int32_t i = wv; i < nh; i += kWideWaves) {
     const float* crow = Cb + (int64_t)hidx[i] * R;
     float mx = -INFINITY;
-    for (int32_t j = lane; j < R; j += kWave) {
-      const float c = crow[j];
-      badc |= !(c == c) || c == INFINITY || c == -INFINITY;
-      mx = fmaxf(mx, -c * kappa);
-    }
+    for (int32_t j = lane; j < R; j += kWave) mx = fmaxf(mx, -crow[j] * kappa);
     mx = lanes_max(mx);
     float sum = 0.f;
     for (int32_t j = lane; j < R; j += kWave) sum += fexp2(-crow[j] * kappa - mx);
     sum = lanes_sum(sum);
     if (lane == 0) Fl[i] = flog2(sAl[i]) - (mx + flog2(sum));
   }
-  if (__ballot(badc) != 0 && lane == 0) atomicOr(&flag[0], 1);
   __syncthreads();
-  if (flag[0] != 0) {
-    if (p.T)
-      for (int64_t q = threadIdx.x; q < (int64_t)R * R; q += kWideThreads) p.T[pb * R * R + q] = 0.f;
-    for (int32_t i = threadIdx.x; i < R; i += kWideThreads) {
-      if (p.f) p.f[pb * R + i] = -INFINITY;
-      if (p.g) p.g[pb * R + i] = -INFINITY;
-    }
-    if (threadIdx.x == 0 && p.status) p.status[pb] = TAOT_ST_BAD_INPUT;
-    return;
-  }
   switch (wide_cpl(nc)) {
 #define TAOT_WIDE_CASE(CPL_)                                                                          \
   case CPL_:                                                                                          \
@@ -1941,6 +1941,7 @@ struct SkWs {
   int32_t* cls;     // [B] register class
   int32_t* lists;   // [3][B] register problems: multi, single, wide
   int32_t* counts;  // [3]
+  int32_t* cbad;    // [B or 1][scan_chunks(R)] chunk marks of the cost scan
   float* kt;
   int64_t kt_stride;
   size_t bytes;
@@ -1953,6 +1954,7 @@ SkWs carve(void* ws, int32_t B, int32_t R) {
   w.cls = c.take<int32_t>((size_t)B);
   w.lists = c.take<int32_t>((size_t)3 * B);
   w.counts = c.take<int32_t>(3);
+  w.cbad = c.take<int32_t>((size_t)B * scan_chunks(R));
   w.kt_stride = round_up((int64_t)R * R, 64);
   w.kt = c.take<float>((size_t)B * w.kt_stride);
   w.bytes = c.off;
@@ -1968,7 +1970,14 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
                             float* f, float* g, uint32_t* status, void* ws, hipStream_t stream) {
   if (B == 0) return TAOT_OK;
   SkWs w = carve(ws, B, R);
-  SkParams p{a, b, B, R, C, C_stride, eps, iters, flags, T, f, g, status, w.flag, w.kt, w.kt_stride, 0, 0};
+  SkParams p{a, b, B, R, C, C_stride, eps, iters, flags, T, f, g, status, w.flag, w.kt, w.kt_stride, 0, 0,
+             w.cbad, scan_chunks(R)};
+  {
+    const int64_t mats = C_stride ? B : 1;
+    hipLaunchKernelGGL(cost_scan_kernel, dim3((unsigned)(mats * p.cchunks)), dim3(kScanThreads), 0, stream, C,
+                       (int64_t)R * R, p.cchunks, w.cbad);
+    if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  }
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
   if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {

@@ -8,7 +8,7 @@ import torch
 import oracle as O
 import paper_2608_03676_amd as taot
 import workloads as W
-from helpers import oracle_inputs, sinkhorn_check
+from helpers import oracle_inputs, potentials_check, sinkhorn_check
 
 pytestmark = pytest.mark.gpu
 
@@ -30,11 +30,8 @@ def _check_against_oracle(a32, b32, C32, eps, iters, flags=0):
     T, f, g, st = _gpu_sinkhorn(a32, b32, C32, eps, iters, flags)
     ref = O.sinkhorn(a, b, C32.astype(np.float64), eps, iters, colcap=not (flags & taot.SK_NO_COLCAP))
     rels = sinkhorn_check(T, ref.T, a, b)
-    # potentials agree where finite (the plan pins them up to a shared constant:
-    # compare f_i + g_j on the support instead of f and g separately)
-    for p in range(a.shape[0]):
-        hot, cold = ref.f[p] > -np.inf, ref.g[p] > -np.inf
-        assert np.array_equal(hot, f[p] > -np.inf) and np.array_equal(cold, g[p] > -np.inf)
+    worst = potentials_check(f, g, ref.f, ref.g, eps, iters)
+    print(f"  potentials: max |d(f+g)| {worst[0]:.2e} eps, max |df|, |dg| {worst[1]:.2e} eps", flush=True)
     return T, st, rels
 
 
@@ -189,6 +186,48 @@ def test_degenerate(gpu):
     Cb[0, 5] = np.inf
     _, _, _, st = _gpu_sinkhorn(a[3:], b[3:], Cb, 0.5, 10)
     assert st[0] == taot.ST_BAD_INPUT
+
+
+@pytest.mark.parametrize("R,where", [(8, (5, 1)), (8, (3, 3)), (300, (299, 7)), (1100, (1099, 1098))])
+@pytest.mark.parametrize("bad", [np.nan, np.inf, -np.inf])
+def test_nonfinite_cost_anywhere(R, where, bad, gpu):
+    """A NaN or infinity in any entry of C marks the problem BAD_INPUT with a
+    zero plan and -inf potentials, as in the oracle, also in a row or column
+    the iterate never reads (here the entry's row is not hot, or it is the
+    diagonal).  With per-problem costs only the problem whose matrix holds it
+    is marked; the others are planned as usual (register, wide and streamed
+    classes at R = 8 / 300 / 1100)."""
+    rng = np.random.default_rng(R)
+    B = 3
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p in range(B):
+        a[p, :2] = rng.integers(5000, 20000, size=2)    # hot ranks 0 and 1
+        # cold ranks 2 .. R-2, demand about the supply; the last rank is neither
+        b[p, 2:R - 1] = rng.multinomial(int(a[p].sum()), np.full(R - 3, 1.0 / (R - 3))) + 1
+    C = W.cost_matrix_for(R, ("three_tier", 1.0, 3.0, 8.0, 32)) if R > 8 else \
+        rng.uniform(0.5, 2.0, (R, R)).astype(np.float32)
+    i, j = where
+    assert a[0, i] == 0  # a row the iterate does not read
+    Cs = C.copy()
+    Cs[i, j] = bad
+    eps, iters = 0.1, 20
+    T, f, g, st = _gpu_sinkhorn(a, b, Cs, eps, iters)
+    ref = O.sinkhorn(a.astype(float), b.astype(float), Cs.astype(float), eps, iters)
+    assert np.all(ref.status == O.ST_BAD_INPUT)
+    assert np.all(st == taot.ST_BAD_INPUT), st
+    assert not T.any() and np.all(np.isneginf(f)) and np.all(np.isneginf(g))
+    # per-problem costs: only problem 1's matrix holds the bad entry
+    Cp = np.stack([C, C, C])
+    Cp[1, i, j] = bad
+    T, f, g, st = _gpu_sinkhorn(a, b, Cp, eps, iters)
+    ref = O.sinkhorn(a.astype(float), b.astype(float), Cp.astype(float), eps, iters)
+    assert list(ref.status) == [0, O.ST_BAD_INPUT, 0]
+    assert st[1] == taot.ST_BAD_INPUT and st[0] & taot.ST_BAD_INPUT == 0 and st[2] & taot.ST_BAD_INPUT == 0, st
+    assert not T[1].any() and np.all(np.isneginf(f[1])) and np.all(np.isneginf(g[1]))
+    keep = [0, 2]
+    sinkhorn_check(T[keep], ref.T[keep], a[keep].astype(float), b[keep].astype(float))
+    potentials_check(f[keep], g[keep], ref.f[keep], ref.g[keep], eps, iters)
 
 
 def test_deterministic(gpu):
