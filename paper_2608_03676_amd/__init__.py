@@ -290,14 +290,17 @@ def plan_quality(load_r: torch.Tensor, home: torch.Tensor, sched: Schedule, K: i
 
 def plan_report(plan: Plan, home: torch.Tensor, K: int, problems=None, ranks_per_node: int = 8,
                 w_inter: float = 3.0) -> str:
-    """The planner's per-invocation report for the given problems (layers):
-    (1) per-rank and per-expert load before routing, hot ranks and hot
-    experts marked; (2) the cloning plan, each cloned expert's slot, whether
-    the copy is intra- or inter-node and the tokens it takes, then the copy
-    counts and weighted cost; (3) the projected per-rank load; (4) imbalance
-    before and after, the peak-load reduction, the fraction of tokens
-    rerouted and the final copy counts and cost (Sec. 4 / appendix report).
-    Host-side formatting of a finished plan."""
+    """Text report of a finished plan, one block per chosen problem (layer),
+    in the four parts of the planner log described in Appendix B.3:
+    [1] every rank's load, ranks above the integer mean starred, and each
+        expert that spills, with its home rank, load and spill;
+    [2] one line per filled guest slot (expert, its home rank, the hosting
+        rank and slot, same node or not, tokens the slot receives), then the
+        copy counts and their weighted cost;
+    [3] every rank's load once the planned tokens have moved;
+    [4] rho and the largest rank load before and after, the share of all
+        tokens sent to a replica, and the copy counts and cost.
+    Formats on the host what the plan already holds."""
     L, sched = plan.loads, plan.schedule
     q = plan_quality(L.load_r, home, sched, K, ranks_per_node, w_inter)
     load_r, load_e = L.load_r.cpu().numpy(), L.load_e.cpu().numpy()
