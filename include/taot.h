@@ -6,7 +6,8 @@
  * Conventions for every entry point
  *   - Arrays are contiguous, row-major DEVICE pointers unless marked "host".
  *   - The caller owns every input, output and workspace buffer.  The library
- *     never allocates, frees or keeps pointers and has no mutable global state;
+ *     never allocates, frees or keeps pointers and has no mutable global state
+ *     (one exception: the fixed device scratch of taot_plan_loads_noalloc);
  *     calls on different streams may run concurrently.
  *   - Each call only enqueues work on `stream` (a hipStream_t; 0 = the null
  *     stream) and returns without synchronising.  Every output is fully
@@ -35,6 +36,8 @@ typedef enum {
   TAOT_ERR_UNSUPPORTED = 2, /* shape beyond the limits below                    */
   TAOT_ERR_WORKSPACE = 3,   /* ws == NULL or ws_bytes < the required size      */
   TAOT_ERR_LAUNCH = 4,      /* the HIP runtime rejected a kernel launch        */
+  TAOT_ERR_SCRATCH = 5,     /* taot_plan_loads_noalloc: the shape needs more than
+                               its fixed scratch (see there)                   */
 } taot_status;
 
 /* Per-problem status bits (uint32_t status[B]). */
@@ -112,6 +115,29 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
                             int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                             float* demand, double* rho, double* alpha, int64_t* bad_ids,
                             uint32_t* status, void* ws, size_t ws_bytes, void* stream);
+
+/* Allocation-free variant of taot_plan_loads, for callers that cannot
+ * allocate device memory or pass a workspace (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments,
+ * outputs and status bits as taot_plan_loads without ws / ws_bytes; the
+ * enqueued kernels are the same.  Its workspace is a fixed 1 MiB array in
+ * device memory of the library, one per GPU, set up on the first call on
+ * each device and kept until the process ends; no call allocates or frees
+ * memory.  Every call on one GPU uses the same array (its contents are
+ * rebuilt by each call), so calls that overlap on one GPU, on different
+ * streams or host threads, race: serialise them.
+ * Returns TAOT_ERR_SCRATCH, enqueuing nothing, when the shape's workspace
+ * exceeds the array: B above taot_plan_loads_noalloc_max_problems(R, E)
+ * (about 1.1e5 problems at R = 2048, E = 32768), TAOT_ERR_LAUNCH if the
+ * array's device address cannot be obtained. */
+taot_status taot_plan_loads_noalloc(const int32_t* ids, int32_t B, int32_t R, int64_t N, int32_t E,
+                                    const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
+                                    int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
+                                    float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                                    uint32_t* status, void* stream);
+/* Largest B taot_plan_loads_noalloc accepts for R ranks and E experts (0 for
+ * an invalid or unsupported R or E). */
+size_t taot_plan_loads_noalloc_max_problems(int32_t R, int32_t E);
 
 /* ------------------------------------------------------------------------ */
 /* Step 3: batched Phase-1 Sinkhorn-Knopp flow planning (Sec. 3.2 "Phase 1";

@@ -21,6 +21,7 @@ const char* taot_status_string(taot_status s) {
     case TAOT_ERR_UNSUPPORTED: return "unsupported shape";
     case TAOT_ERR_WORKSPACE: return "workspace missing or too small";
     case TAOT_ERR_LAUNCH: return "kernel launch failed";
+    case TAOT_ERR_SCRATCH: return "needs more than the fixed scratch of the allocation-free entry point";
   }
   return "unknown status";
 }
@@ -44,6 +45,35 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
   if (!ws || ws_bytes < plan_loads_ws(B, R, E)) return TAOT_ERR_WORKSPACE;
   return launch_plan_loads(ids, B, R, N, E, home, n, load_e, load_r, excess, spare, spill, supply,
                            demand, rho, alpha, bad_ids, status, ws, static_cast<hipStream_t>(stream));
+}
+
+taot_status taot_plan_loads_noalloc(const int32_t* ids, int32_t B, int32_t R, int64_t N, int32_t E,
+                                    const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
+                                    int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
+                                    float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                                    uint32_t* status, void* stream) {
+  if (bad_dims(B, R) || E <= 0 || N < 0) return TAOT_ERR_INVALID_ARG;
+  if (R > TAOT_MAX_RANKS || E > TAOT_MAX_EXPERTS) return TAOT_ERR_UNSUPPORTED;
+  if (B == 0) return TAOT_OK;
+  if ((N > 0 && !ids) || !home || !n || !load_e || !load_r || !excess || !spare || !spill || !alpha)
+    return TAOT_ERR_INVALID_ARG;
+  if ((int64_t)B * R > 0x7fffffffLL || N > 0x7fffffffLL) return TAOT_ERR_UNSUPPORTED;
+  if (plan_loads_ws(B, R, E) > plan_loads_scratch_limit()) return TAOT_ERR_SCRATCH;
+  void* ws = plan_loads_scratch();
+  if (!ws) return TAOT_ERR_LAUNCH;
+  return launch_plan_loads(ids, B, R, N, E, home, n, load_e, load_r, excess, spare, spill, supply,
+                           demand, rho, alpha, bad_ids, status, ws, static_cast<hipStream_t>(stream));
+}
+
+size_t taot_plan_loads_noalloc_max_problems(int32_t R, int32_t E) {
+  if (R <= 0 || E <= 0 || R > TAOT_MAX_RANKS || E > TAOT_MAX_EXPERTS) return 0;
+  size_t lo = 0, hi = (size_t)1 << 31;  // largest B whose workspace fits the scratch
+  while (lo + 1 < hi) {
+    const size_t mid = (lo + hi) / 2;
+    if (plan_loads_ws((int32_t)(mid > 0x7fffffff ? 0x7fffffff : mid), R, E) <= plan_loads_scratch_limit()) lo = mid;
+    else hi = mid;
+  }
+  return lo;
 }
 
 size_t taot_sinkhorn_workspace_size(int32_t B, int32_t R) {

@@ -71,6 +71,8 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
                               float* demand, double* rho, double* alpha, int64_t* bad_ids,
                               uint32_t* status, void* ws, hipStream_t stream);
 size_t plan_loads_ws(int32_t B, int32_t R, int32_t E);
+size_t plan_loads_scratch_limit();
+void* plan_loads_scratch();
 
 taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R, const float* C,
                             int64_t C_stride, float eps, int32_t iters, uint32_t flags, float* T,

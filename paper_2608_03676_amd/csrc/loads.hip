@@ -13,6 +13,8 @@
 //                                     counters privatised per lane group.
 //   marginals_kernel   (B blocks)     reads n once; loads, mean, excess/spare,
 //                                     rho, alpha, spill.
+#include <mutex>
+
 #include "common.h"
 
 namespace taot {
@@ -279,9 +281,36 @@ LoadsWs carve(void* ws, int32_t B, int32_t R, int32_t E) {
   return w;
 }
 
+// Fixed scratch of the allocation-free entry point: the same workspace
+// layout as above, in a file-scope device array (one copy per GPU, held until
+// the process ends).  Host code never uses the array's name as an address:
+// its device address is looked up once per device with hipGetSymbolAddress.
+constexpr size_t kScratchBytes = (size_t)1 << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
 }  // namespace
 
 size_t plan_loads_ws(int32_t B, int32_t R, int32_t E) { return carve(nullptr, B, R, E).bytes; }
+
+size_t plan_loads_scratch_limit() { return kScratchBytes; }
+
+// Device address of this device's scratch array (looked up on the first call
+// per device), or nullptr if the runtime cannot give it.
+void* plan_loads_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    scratch_ptr[dev] = ptr;
+  }
+  return scratch_ptr[dev];
+}
 
 taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N, int32_t E,
                               const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
