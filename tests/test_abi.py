@@ -115,3 +115,27 @@ def test_topology_pref_rejects_bad_costs():
     C[1, 2] = 0.0
     with pytest.raises(taot.TaotError):
         taot.topology_pref(C)
+
+
+def test_noalloc_limits_on_host():
+    """The allocation-free plan_loads refuses on the host, before any HIP
+    call: invalid arguments, and batches whose workspace exceeds its fixed
+    scratch (TAOT_ERR_SCRATCH); the limit shrinks with R and E."""
+    L = taot.lib()
+    L.taot_plan_loads_noalloc.restype = ctypes.c_int
+    L.taot_plan_loads_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                          ctypes.c_int32] + [ctypes.c_void_p] * 14
+    L.taot_plan_loads_noalloc_max_problems.restype = ctypes.c_size_t
+    L.taot_plan_loads_noalloc_max_problems.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    cap16 = L.taot_plan_loads_noalloc_max_problems(16, 64)
+    cap_big = L.taot_plan_loads_noalloc_max_problems(2048, 32768)
+    assert cap16 > cap_big > 100000
+    assert L.taot_plan_loads_noalloc_max_problems(0, 64) == 0
+    assert L.taot_plan_loads_noalloc_max_problems(16, 32769) == 0
+    # the workspace of cap16 problems fits 1 MiB, one more does not
+    assert L.taot_plan_loads_workspace_size(cap16, 16, 64) <= 1 << 20 < L.taot_plan_loads_workspace_size(cap16 + 1, 16, 64)
+    p = [_fake()] * 13
+    assert L.taot_plan_loads_noalloc(_fake(), cap16 + 1, 16, 8, 64, *p, None) == 5
+    assert L.taot_status_string(5).startswith(b"needs more than the fixed scratch")
+    assert L.taot_plan_loads_noalloc(None, 1, 16, 8, 64, *p, None) == 1  # ids NULL with N > 0
+    assert L.taot_plan_loads_noalloc(_fake(), 1, 4096, 8, 64, *p, None) == 2  # R beyond the limit
