@@ -538,6 +538,9 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 // slot-expert counts exceed the LDS layout.
 
 constexpr int kTierMax = 4;  // distinct bonus values per host column
+// The count window of the R = 1024 layout: the ranks with base + k services,
+// k < kLvl (base = the fewest services of any rank), as one rank set per k.
+constexpr int kLvl = 4;
 
 struct LdsSmall {
   static constexpr int kT = 256;     // threads per problem
@@ -569,6 +572,10 @@ struct LdsLarge {
   static constexpr int kNEC = 1024;
   static constexpr int kWavesPerEU = 1;  // one problem per compute unit in any case
 };
+// The count window's rebuild takes rank r on thread r (wave w builds word w).
+static_assert(LdsSmall::kT == LdsSmall::kTW * kWave && LdsTiny::kT == LdsTiny::kTW * kWave &&
+                  LdsLarge::kT == LdsLarge::kTW * kWave,
+              "one thread per rank of the largest R of each configuration");
 // list entries pack (slot, slot-expert index, host structure): 12 + 7 + 7 bits
 constexpr int kItemSlotBits = 12, kItemExpertBits = 7;
 
@@ -760,6 +767,9 @@ struct LdsState {
   // Phase 3 (aliases the Phase-2 region)
   double* price; uint32_t* rkey; int32_t* work;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
+  // count window (TW > 4 only): [kLvl][TW] rank sets; lvl_base: base,
+  // minimum (rebase scratch), level-0 word emptied, by round parity (2)
+  uint64_t* lvl; int32_t* lvl_base;
   int8_t* cn; double* cv; int32_t* cvr; uint32_t* cw; uint64_t* cm;
   size_t bytes;
 };
@@ -788,9 +798,11 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
   w.work = (int32_t*)take(4 * S1);
-  w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(4 * DC);
+  // the word lists guide the per-word search of sets wider than 4 words only
+  w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
   w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
   w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * CF::kPL * TW);
+  w.lvl = (uint64_t*)take(TW > 4 ? 8 * kLvl * TW : 0); w.lvl_base = (int32_t*)take(TW > 4 ? 4 * 4 : 0);
   w.cn = (int8_t*)take(SC);
   w.cv = (double*)take(8 * SC * kTierMax); w.cvr = (int32_t*)take(4 * SC * kTierMax);
   w.cw = (uint32_t*)take(4 * SC * kTierMax);
@@ -1125,7 +1137,8 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   // and the words of each set that hold ranks
   int32_t* np = wp.nprime + b * (int64_t)CF::kDC * R;
   const int32_t* nb = p.n + b * (int64_t)R * E;
-  for (int32_t d = tid; d < D; d += NT) L.vwords[d] = 0u;
+  if constexpr (TW > 4)
+    for (int32_t d = tid; d < D; d += NT) L.vwords[d] = 0u;
   __syncthreads();
   for (int32_t d = 0; d < D; ++d) {
     const int32_t e = L.dexp[d];
@@ -1136,7 +1149,8 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       const uint64_t m = __ballot(v > 0);
       if (lane == 0) {
         L.vmask[d * TW + w] = m;
-        if (m) atomicOr(&L.vwords[d], 1u << w);
+        if constexpr (TW > 4)
+          if (m) atomicOr(&L.vwords[d], 1u << w);
       }
     }
   }
@@ -1158,6 +1172,14 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     L.cnt[r] = 0;
   }
   for (int32_t q = tid; q < CF::kPL * TW; q += NT) L.planes[q] = 0ull;
+  if constexpr (TW > 4) {
+    // count window: every rank starts with 0 services (level 0 of base 0)
+    for (int32_t q = tid; q < kLvl * TW; q += NT) {
+      const int32_t lo = (q % TW) * kWave;
+      L.lvl[q] = q >= TW || lo >= R ? 0ull : (R - lo >= kWave ? ~0ull : (1ull << (R - lo)) - 1ull);
+    }
+    if (tid == 0) { L.lvl_base[0] = 0; L.lvl_base[1] = INT_MAX; L.lvl_base[2] = 0; L.lvl_base[3] = 0; }
+  }
   const int32_t ns = wp.hdr[0];
   for (int32_t q = tid; q < ns; q += NT) L.cn[q] = (int8_t)wp.cn[q];
   for (int32_t q = tid; q < ns * kTierMax; q += NT) {
@@ -1298,7 +1320,41 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
           // where none remained
           int32_t rr = INT_MAX;
           uint32_t cmin = 0xFFFFFFFFu;
-          for (uint32_t words = L.cw[st * kTierMax + ti] & vw; words; words &= words - 1) {
+          // The count window first, level by level, words ascending (four
+          // per batch of loads): the first hit is the lowest rank among the
+          // fewest services.  The first pass, through the lowest level
+          // (never empty when a round starts), notes the words that hold
+          // candidates.  With a price step of 0 the first candidate wins.
+          auto scan = [&](uint32_t words, const uint64_t* lv, uint32_t* cand_out) {
+            int32_t hit = INT_MAX;
+            while (words && hit == INT_MAX) {
+              int wi[4];
+              uint64_t xt[4], xl[4];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                wi[u] = words ? __builtin_ctz(words) : -1;
+                words &= words - 1u;
+              }
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                const int w = wi[u] < 0 ? 0 : wi[u];
+                xt[u] = wi[u] < 0 ? 0ull : tm[w] & vm[w];
+                xl[u] = lv ? xt[u] & lv[w] : xt[u];
+              }
+#pragma unroll
+              for (int u = 3; u >= 0; --u) {
+                if (cand_out && xt[u]) *cand_out |= 1u << wi[u];
+                if (xl[u]) hit = wi[u] * kWave + __builtin_ctzll(xl[u]);
+              }
+            }
+            return hit;
+          };
+          uint32_t cand = 0;
+          rr = scan(L.cw[st * kTierMax + ti] & vw, track ? L.lvl : nullptr, &cand);
+          if (!cand) continue;  // no valid rank in this tier
+          for (int k = 1; k < kLvl && rr == INT_MAX; ++k) rr = scan(cand, L.lvl + k * TW, nullptr);
+          // beyond the window: the bit-plane search over the candidate words
+          for (uint32_t words = rr == INT_MAX ? cand : 0u; words; words &= words - 1) {
             const int w = __builtin_ctz(words);
             uint64_t x = tm[w] & vm[w];
             if (!x) continue;
@@ -1332,6 +1388,8 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     // token loads above complete on their own before Y uses them.
     if (!block_or_lds<NT>(any, flagbuf, parity)) break;
     // ---- Y: transfers -----------------------------------------------------------------------
+    if constexpr (TW > 4)
+      if (tid == 0) L.lvl_base[2 + prv] = 0;  // read by every thread before the barrier above
     int32_t newmax = 0;
 #pragma unroll
     for (int i = 0; i < SPL; ++i) {
@@ -1357,6 +1415,18 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
               for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
                 atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]),
                           bit);
+              if constexpr (TW > 4) {
+                // the rank moves up one level of the count window; a word of
+                // the lowest level that empties is flagged for the round's end
+                const int32_t k0 = c0 - L.lvl_base[0];
+                if (k0 < kLvl) {
+                  const uint64_t old =
+                      atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl[k0 * TW + (r >> 6)]), bit);
+                  if (k0 == 0 && old == bit) L.lvl_base[2 + cur] = 1;
+                }
+                if (k0 + 1 < kLvl)
+                  atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl[(k0 + 1) * TW + (r >> 6)]), bit);
+              }
             }
           }
           if (have - x <= 0) {
@@ -1373,6 +1443,33 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
     __syncthreads();
     rounds = t;
+    if constexpr (TW > 4) {
+      bool l0_empty = false;
+      if (track && L.lvl_base[2 + cur]) {
+        l0_empty = true;
+#pragma unroll
+        for (int w = 0; w < TW; ++w) l0_empty &= L.lvl[w] == 0ull;
+      }
+      if (l0_empty) {
+        // Every rank has left the window's lowest level: the base moves to
+        // the new fewest services and the window is rebuilt from the counts.
+        // Rank r is thread r, so wave w builds word w.
+        const int32_t mine = tid < R ? L.cnt[tid] : INT_MAX;
+        const int32_t wmin = -wave_max_i32(-mine);
+        if (lane == 0) atomicMin(&L.lvl_base[1], wmin);
+        __syncthreads();
+        const int32_t nb = L.lvl_base[1];
+        const int32_t kr = tid < R ? L.cnt[tid] - nb : -1;
+#pragma unroll
+        for (int k = 0; k < kLvl; ++k) {
+          const uint64_t m = __ballot(kr == k);
+          if (lane == 0 && wid < TW) L.lvl[k * TW + wid] = m;
+        }
+        __syncthreads();
+        if (tid == 0) { L.lvl_base[0] = nb; L.lvl_base[1] = INT_MAX; }
+        __syncthreads();
+      }
+    }
   }
 
   int64_t left = 0;
