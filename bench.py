@@ -7,9 +7,13 @@ topology preferences) are generated on the device before the timed region
 and stay resident in HBM; outputs and workspaces are preallocated.
 
 Printed: one JSON line.  `value` is the batched Sinkhorn throughput in
-problem-iterations per second (B * iters / Sinkhorn time per step, HIP
+problem-iterations per second (B * iters / median Sinkhorn call time, HIP
 events on the launch stream); `ms_per_step` is the full planner latency.
-The default workload is the R = 256 one (1952 problems of 256 ranks).
+The default workload is the R = 256 one (1952 problems of 256 ranks); the
+planner latency of the other full-size workloads (1, 2, 4) follows, every
+stage with its roofline floor and fraction, beside the peak probes (HBM
+read, unpacked fp32 FMA, v_exp_f32, LDS read) measured in the same run and
+the fp64 oracle timed on the host.
 """
 import argparse
 import ctypes
@@ -22,8 +26,9 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0                      # MI355X HBM3E
+HBM_PEAK_GBS = 8000.0                      # MI355X HBM3E (datasheet)
 VALU_FMA_PEAK = 256 * 64 * 2.4e9           # fp32 FMA lanes/s without packed math (CU x lanes x clock)
+FP32_PUBLISHED_TFLOPS = 157.3              # datasheet fp32 vector peak (needs packed fp32, not used here)
 
 
 def parse():
@@ -41,6 +46,11 @@ def parse():
     ap.add_argument("--other-steps", type=int, default=3,
                     help="timed steps for the planner latency of workloads 1-4 other than --workload (0: skip)")
     ap.add_argument("--json-out", default=None)
+    ap.add_argument("--no-peaks", action="store_true", help="skip the peak probes")
+    ap.add_argument("--peaks-only", action="store_true", help="only run the peak probes and print them")
+    ap.add_argument("--cpu-extrapolate", type=int, default=1,
+                    help="time the oracle on one problem of each workload 1-4 and extrapolate its full-step "
+                         "latency (0: skip)")
     ap.add_argument("--report", default=None, metavar="P1,P2,...",
                     help="plan --workload once and print the planner's four-part report for these "
                          "problems (layers) instead of benchmarking")
@@ -59,8 +69,17 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-PLAN_LOADS_SOURCES = ["paper_2608_03676_amd/csrc/loads.hip", "paper_2608_03676_amd/csrc/common.h"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "plan_loads_workload3_traffic.txt")
+# Counter-measured HBM traffic of a stage's kernels, from the committed
+# rocprofv3 summaries; used only while the sources they were taken on are
+# unchanged (SHA-256 recorded in each summary).
+TRAFFIC = {
+    "plan_loads": (os.path.join(ROOT, "profiles", "plan_loads_workload3_traffic.txt"),
+                   ["paper_2608_03676_amd/csrc/loads.hip", "paper_2608_03676_amd/csrc/common.h"]),
+    "sinkhorn": (os.path.join(ROOT, "profiles", "sinkhorn_workload3_traffic.txt"),
+                 ["paper_2608_03676_amd/csrc/sinkhorn.hip", "paper_2608_03676_amd/csrc/sk_common.h",
+                  "paper_2608_03676_amd/csrc/sk_register.h", "paper_2608_03676_amd/csrc/sk_reg_w2g8.hip",
+                  "paper_2608_03676_amd/csrc/common.h"]),
+}
 
 
 def sources_digest(paths):
@@ -72,23 +91,101 @@ def sources_digest(paths):
     return h.hexdigest()
 
 
-def measured_traffic(workload):
-    """HBM bytes per plan_loads step from the committed counter summary, or
+def measured_traffic(stage, workload):
+    """HBM bytes per call of a stage from its committed counter summary, or
     None when it is for another workload or the kernels changed since."""
-    if workload != 3 or not os.path.exists(TRAFFIC_FILE):
+    if stage not in TRAFFIC or workload != 3:
+        return None
+    path, sources = TRAFFIC[stage]
+    if not os.path.exists(path):
         return None
     fields = {}
-    with open(TRAFFIC_FILE) as fh:
+    with open(path) as fh:
         for line in fh:
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
-    if fields.get("source_sha256") != sources_digest(PLAN_LOADS_SOURCES):
+    if fields.get("source_sha256") != sources_digest(sources):
         return None
     try:
         return float(fields["traffic_bytes_per_step"])
     except (KeyError, ValueError):
         return None
+
+
+def gpu_clocks():
+    """The GPU's clocks and power as amd-smi reports them (best effort; None
+    when the tool is missing or fails)."""
+    import subprocess
+    for cmd in (["amd-smi", "metric", "--clock", "--power", "--json"], ["rocm-smi", "--showclocks", "--showpower", "--json"]):
+        try:
+            r = subprocess.run(cmd, capture_output=True, text=True, timeout=20)
+        except (OSError, subprocess.TimeoutExpired):
+            continue
+        if r.returncode == 0 and r.stdout.strip():
+            try:
+                return {"tool": cmd[0], "report": json.loads(r.stdout)}
+            except ValueError:
+                return {"tool": cmd[0], "report": r.stdout.strip()[:2000]}
+    return None
+
+
+def measure_peaks(dev):
+    """Peak probes P1-P4 (libtaot_probes.so), HIP events on the launch stream,
+    best of 5 launches after one warm-up: HBM read GB/s, unpacked fp32 FMA/s,
+    v_exp_f32/s alone and beside as many FMAs, LDS read bytes/s."""
+    import torch
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2608_03676_amd", "libtaot_probes.so"))
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    L.taot_probe_hbm_read.argtypes = [P, SZ, I32, P, P]
+    L.taot_probe_fma.argtypes = [I32, I32, P, P]
+    L.taot_probe_exp.argtypes = [I32, I32, I32, P, P]
+    L.taot_probe_lds.argtypes = [I32, I32, P, P]
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    blocks = 2048  # eight 256-thread workgroups per compute unit
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+
+    def best(call):
+        call()
+        ts = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            rc = call()
+            b.record(stream)
+            torch.cuda.synchronize()
+            if rc != 0:
+                raise RuntimeError("peak probe launch failed")
+            ts.append(a.elapsed_time(b) * 1e-3)
+        return min(ts)
+
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    t_hbm = best(lambda: L.taot_probe_hbm_read(ctypes.c_void_p(buf.data_ptr()), nbytes, 16384,
+                                               ctypes.c_void_p(out.data_ptr()), sp))
+    del buf
+    it_fma, it_exp, it_lds = 20000, 5000, 20000
+    lanes = blocks * 256
+    t_fma = best(lambda: L.taot_probe_fma(blocks, it_fma, ctypes.c_void_p(out.data_ptr()), sp))
+    t_exp = best(lambda: L.taot_probe_exp(blocks, it_exp, 0, ctypes.c_void_p(out.data_ptr()), sp))
+    t_expf = best(lambda: L.taot_probe_exp(blocks, it_exp, 1, ctypes.c_void_p(out.data_ptr()), sp))
+    t_lds = best(lambda: L.taot_probe_lds(blocks, it_lds, ctypes.c_void_p(out.data_ptr()), sp))
+    fma = lanes * 64.0 * it_fma / t_fma
+    exps = lanes * 64.0 * it_exp / t_exp
+    exps_f = lanes * 64.0 * it_exp / t_expf
+    return {
+        "hbm_read_GBs": nbytes / t_hbm / 1e9,
+        "fp32_fma_per_s": fma, "fp32_tflops_unpacked": 2 * fma / 1e12,
+        "exp_per_s": exps, "exp_to_fma_rate": exps / fma,
+        # exp and FMA issued together take 1.5x the exponentials' time when
+        # they do not overlap (an exponential occupies two FMA issue slots)
+        "exp_with_fma_per_s": exps_f, "exp_plus_fma_time_ratio": t_expf / t_exp,
+        "lds_read_Bps": lanes * 8.0 * 16 * it_lds / t_lds,
+        "datasheet": {"hbm_GBs": HBM_PEAK_GBS, "fp32_fma_per_s_unpacked": VALU_FMA_PEAK,
+                      "fp32_tflops_published": FP32_PUBLISHED_TFLOPS,
+                      "lds_Bps_128B_per_clk": 256 * 128 * 2.4e9},
+    }
 
 
 def copy_calibration(mib):
@@ -165,11 +262,13 @@ def run_workload(w, K, steps, warmup, dev):
     loads_ms = [e[0].elapsed_time(e[1]) for e in events]
     sk_ms = [e[1].elapsed_time(e[2]) for e in events]
     sch_ms = [e[2].elapsed_time(e[3]) for e in events]
-    log(f"[bench] {steps} steps: {ms_step:.3f} ms/step (plan_loads {statistics.mean(loads_ms):.3f}, "
-        f"sinkhorn {statistics.mean(sk_ms):.3f}, round_schedule {statistics.mean(sch_ms):.3f} ms)")
+    step_ms = [e[0].elapsed_time(e[3]) for e in events]
+    log(f"[bench] {steps} steps: {ms_step:.3f} ms/step, median {statistics.median(step_ms):.3f} "
+        f"(plan_loads {statistics.median(loads_ms):.3f}, sinkhorn {statistics.median(sk_ms):.3f}, "
+        f"round_schedule {statistics.median(sch_ms):.3f} ms, medians)")
     del ids
     return dict(loads=loads, flow=flow, sched=sched, home_np=home_np, C_np=C_np, Bp_np=Bp_np, Ba_np=Ba_np,
-                loads_ms=loads_ms, sk_ms=sk_ms, sch_ms=sch_ms, ms_step=ms_step)
+                loads_ms=loads_ms, sk_ms=sk_ms, sch_ms=sch_ms, step_ms=step_ms, ms_step=ms_step)
 
 
 def plan_quality_table(w, K, dev):
@@ -311,13 +410,103 @@ def main():
         else:
             sys.stdout.write(text)
         return
+    peaks = None
+    if not args.no_peaks or args.peaks_only:
+        log("[bench] peak probes")
+        peaks = measure_peaks(dev)
+        log(f"[bench] peaks: {json.dumps(peaks)}")
+        if args.peaks_only:
+            print(json.dumps({"peaks_measured": peaks}), flush=True)
+            return
+    clocks_before = gpu_clocks()
     log(f"[bench] workload {w.index}: {w.name}; B={B} R={R} E={E} N={N} iters={w.iters} K={K}")
     run = run_workload(w, K, args.steps, args.warmup, dev)
-    loads, flow, sched = run["loads"], run["flow"], run["sched"]
-    home_np, C_np, Bp_np, Ba_np = run["home_np"], run["C_np"], run["Bp_np"], run["Ba_np"]
-    loads_ms, sk_ms, sch_ms, ms_step = run["loads_ms"], run["sk_ms"], run["sch_ms"], run["ms_step"]
+    rep = stage_report(w, K, run, peaks)
+    st = rep["stages"]
+    sk = st["sinkhorn"]
+    value = B * w.iters / (sk["ms_median"] * 1e-3)
 
-    # ---- algorithmic work of each stage --------------------------------------------
+    # the metric's own kernels: taot_sinkhorn_batched (the register kernel
+    # and its prepasses), fp32 FMA issue bound
+    roofline = {"kernel": "sinkhorn_reg_kernel<2,8> + prepasses (taot_sinkhorn_batched)", "bound": "alu",
+                "achieved": sk["achieved"], "peak": sk["peak"], "unit": "TFLOP/s", "frac": sk["frac"],
+                "traffic": measured_traffic("sinkhorn", w.index),
+                "peak_note": "unpacked fp32 FMA: 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz; the published "
+                             "157.3 TFLOP/s needs packed fp32, which this build does not use",
+                "frac_vs_published_157_3": sk["achieved"] / FP32_PUBLISHED_TFLOPS}
+    if peaks:
+        roofline["frac_vs_measured_peak"] = sk["achieved"] / peaks["fp32_tflops_unpacked"]
+    rec = {
+        "metric": "batched Sinkhorn problem-iters/s at R=256 + full planner latency (us)/step",
+        "value": value, "unit": "problem-iters/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": run["ms_step"], "planner_latency_us": run["ms_step"] * 1e3,
+        "planner_latency_us_median": rep["planner"]["ms_median"] * 1e3,
+        "planner_latency_us_min": rep["planner"]["ms_min"] * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32 (Sinkhorn), int32/int64 (histogram, schedule), f64 (scores)",
+        "data": "synthetic (seeded Zipf top-8 routing generated on device)",
+        "config": {"workload": f"workload {w.index}: {w.name}", "problems": B, "ranks": R, "experts": E,
+                   "ids_per_problem": R * N, "iters": w.iters, "eps": w.eps, "K": K},
+        "roofline": roofline,
+        "stages": st,
+        "planner": rep["planner"],
+        "status": rep["status"],
+    }
+    if peaks:
+        rec["peaks_measured"] = peaks
+
+    # ---- planner latency of the other full-size workloads (fewer steps) -------------
+    gpu_rounds = {w.index: rep["phase3_rounds_mean"]}
+    if args.other_steps > 0:
+        lat = {str(w.index): dict(problems=B, ranks=R, **rep["summary"], stages=st, planner=rep["planner"],
+                                  status=rep["status"])}
+        del run
+        torch.cuda.empty_cache()
+        for wi in (1, 2, 3, 4):
+            if wi == w.index:
+                continue
+            wo = W.WORKLOADS[wi]
+            log(f"[bench] planner latency, workload {wi}: {wo.name}")
+            r2 = run_workload(wo, wo.K, args.other_steps, 1, dev)
+            rep2 = stage_report(wo, wo.K, r2, peaks)
+            lat[str(wi)] = dict(problems=wo.B, ranks=wo.R, **rep2["summary"], stages=rep2["stages"],
+                                planner=rep2["planner"], status=rep2["status"])
+            gpu_rounds[wi] = rep2["phase3_rounds_mean"]
+            del r2
+            torch.cuda.empty_cache()
+        rec["planner_latency_by_workload"] = dict(sorted(lat.items()))
+    rec["clocks"] = {"before": clocks_before, "after": gpu_clocks()}
+
+    # ---- CPU baseline: the oracle on a bounded sample of the same workload ----------
+    if args.cpu_sample > 0:
+        rec["cpu_baseline"] = cpu_baseline(w, K, args, run_home(w), W.cost_matrix(w))
+        if args.cpu_extrapolate:
+            rec["cpu_baseline"]["extrapolated"] = cpu_extrapolate(gpu_rounds, rec["cpu_baseline"]["cores"])
+    line = json.dumps(rec)
+    print(line, flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as fh:
+            fh.write(line + "\n")
+
+
+def run_home(w):
+    import workloads as W
+    return W.home_map(w)
+
+
+def stage_report(w, K, run, peaks):
+    """Per-stage times (mean, median, min over the timed steps), algorithmic
+    work, roofline floors and fractions of one workload's planner step:
+    plan_loads against HBM (ids read once, n written and read back once),
+    the Sinkhorn against the unpacked fp32 FMA issue rate (one FMA per
+    support entry per half-step; the plan's HBM write checked too), the
+    schedule against the bytes it must move (X and the slots written, the
+    plan on the support and the slot experts' counts read: a latency-bound
+    chain of rounds, so this floor is far from reach), and the step against
+    the sum of the three floors."""
+    import numpy as np
+    B, R, E, N = w.B, w.R, w.E, w.N
+    loads, flow, sched = run["loads"], run["flow"], run["sched"]
     st_loads = loads.status.cpu().numpy().view(np.uint32)
     st_flow = flow.status.cpu().numpy().view(np.uint32)
     st_sched = sched.status.cpu().numpy().view(np.uint32)
@@ -327,82 +516,69 @@ def main():
     nc = (spare > 0).sum(1).astype(np.int64)
     support = int((nh * nc).sum())
     rounds = sched.rounds_used.cpu().numpy()
-    unfilled = int(sched.unfilled.sum().item())
-    # plan_loads bytes: ids read once, n written once and read once by the marginals
+    se = sched.slot_expert.cpu().numpy()
+    distinct = sum(len(set(row[row >= 0].tolist())) for row in se)
+    stats = lambda xs: {"ms": statistics.mean(xs), "ms_median": statistics.median(xs), "ms_min": min(xs)}
     loads_bytes = 4 * B * R * N + 2 * 4 * B * R * E
-    sk_fma = 2 * support * w.iters              # one FMA per support entry per half-step
-    mean = lambda xs: statistics.mean(xs)
-    stage = {
-        "plan_loads": {"bound": "hbm", "ms": mean(loads_ms), "achieved": loads_bytes / (mean(loads_ms) * 1e-3) / 1e9,
-                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "bytes_per_launch": loads_bytes},
-        "sinkhorn": {"bound": "alu", "ms": mean(sk_ms), "achieved": 2 * sk_fma / (mean(sk_ms) * 1e-3) / 1e12,
-                     "peak": 2 * VALU_FMA_PEAK / 1e12, "unit": "TFLOP/s", "fma_per_launch": sk_fma,
-                     "support_entries": support},
-        "round_schedule": {"bound": "latency", "ms": mean(sch_ms), "phase2_inner_mean": float(rounds[:, 0].mean()),
-                           "phase3_rounds_mean": float(rounds[:, 1].mean()), "phase3_rounds_max": int(rounds[:, 1].max())},
+    sk_fma = 2 * support * w.iters
+    sk_bytes = 4 * B * R * R + 2 * 4 * B * R   # plan and potentials written
+    sch_bytes = 4 * B * R * R * K + 12 * B * R * K + 4 * support + 4 * R * distinct
+    floor = {"plan_loads": loads_bytes / (HBM_PEAK_GBS * 1e9) * 1e3,
+             "sinkhorn": max(sk_fma / VALU_FMA_PEAK, sk_bytes / (HBM_PEAK_GBS * 1e9)) * 1e3,
+             "round_schedule": sch_bytes / (HBM_PEAK_GBS * 1e9) * 1e3}
+    stages = {
+        "plan_loads": dict(bound="hbm", **stats(run["loads_ms"]), bytes_per_launch=loads_bytes, peak=HBM_PEAK_GBS,
+                           unit="GB/s"),
+        "sinkhorn": dict(bound="alu", **stats(run["sk_ms"]), fma_per_launch=sk_fma, support_entries=support,
+                         peak=2 * VALU_FMA_PEAK / 1e12, unit="TFLOP/s"),
+        "round_schedule": dict(bound="latency", **stats(run["sch_ms"]), bytes_floor=sch_bytes,
+                               phase2_inner_mean=float(rounds[:, 0].mean()),
+                               phase3_rounds_mean=float(rounds[:, 1].mean()),
+                               phase3_rounds_max=int(rounds[:, 1].max())),
     }
-    for s in stage.values():
-        if "peak" in s:
-            s["frac"] = s["achieved"] / s["peak"]
-    # roofline of the longest stage that has one (the schedule is a chain of
-    # dependent rounds: latency, not bandwidth or ALU, bounds it)
-    dom_name = max(("plan_loads", "sinkhorn"), key=lambda k: stage[k]["ms"])
-    dom = stage[dom_name]
-    kernels = {"plan_loads": "histogram_kernel + marginals_kernel (taot_plan_loads)",
-               "sinkhorn": "sinkhorn_wave_kernel (taot_sinkhorn_batched)"}
-    traffic = measured_traffic(w.index) if dom_name == "plan_loads" else None
-    roofline = {"kernel": kernels[dom_name], "bound": dom["bound"], "achieved": dom["achieved"],
-                "peak": dom["peak"], "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
-
-    value = B * w.iters / (mean(sk_ms) * 1e-3)
-    rec = {
-        "metric": "batched Sinkhorn problem-iters/s at R=256 + full planner latency (us)/step",
-        "value": value, "unit": "problem-iters/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms_step, "planner_latency_us": ms_step * 1e3, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32 (Sinkhorn), int32/int64 (histogram, schedule), f64 (scores)",
-        "data": "synthetic (seeded Zipf top-8 routing generated on device)",
-        "config": {"workload": f"workload {w.index}: {w.name}", "problems": B, "ranks": R, "experts": E,
-                   "ids_per_problem": R * N, "iters": w.iters, "eps": w.eps, "K": K},
-        "roofline": roofline,
-        "stages": stage,
-        "status": {"loads_nonzero": int((st_loads != 0).sum()), "sinkhorn_nonzero": int((st_flow != 0).sum()),
-                   "schedule_unfilled": unfilled, "schedule_nonzero": int((st_sched != 0).sum())},
-    }
-
-    # ---- planner latency of the other full-size workloads (fewer steps) -------------
-    if args.other_steps > 0:
-        lat = {str(w.index): {"problems": B, "ranks": R, "ms_per_step": ms_step, "plan_loads_ms": mean(loads_ms),
-                              "sinkhorn_ms": mean(sk_ms), "round_schedule_ms": mean(sch_ms)}}
-        del run, loads, flow, sched
-        torch.cuda.empty_cache()
-        for wi in (1, 2, 3, 4):
-            if wi == w.index:
-                continue
-            wo = W.WORKLOADS[wi]
-            log(f"[bench] planner latency, workload {wi}: {wo.name}")
-            r2 = run_workload(wo, wo.K, args.other_steps, 1, dev)
-            lat[str(wi)] = {"problems": wo.B, "ranks": wo.R, "ms_per_step": r2["ms_step"],
-                            "plan_loads_ms": mean(r2["loads_ms"]), "sinkhorn_ms": mean(r2["sk_ms"]),
-                            "round_schedule_ms": mean(r2["sch_ms"]),
-                            "unfilled": int(r2["sched"].unfilled.sum().item())}
-            del r2
-            torch.cuda.empty_cache()
-        rec["planner_latency_by_workload"] = dict(sorted(lat.items()))
-
-    # ---- CPU baseline: the oracle on a bounded sample of the same workload ----------
-    if args.cpu_sample > 0:
-        rec["cpu_baseline"] = cpu_baseline(w, K, args, home_np, C_np, Bp_np, Ba_np)
-    line = json.dumps(rec)
-    print(line, flush=True)
-    if args.json_out:
-        with open(args.json_out, "w") as fh:
-            fh.write(line + "\n")
+    stages["plan_loads"]["achieved"] = loads_bytes / (stages["plan_loads"]["ms_median"] * 1e-3) / 1e9
+    stages["sinkhorn"]["achieved"] = 2 * sk_fma / (stages["sinkhorn"]["ms_median"] * 1e-3) / 1e12
+    for k in ("plan_loads", "sinkhorn"):
+        stages[k]["frac"] = stages[k]["achieved"] / stages[k]["peak"]
+    traffic = measured_traffic("plan_loads", w.index)
+    stages["plan_loads"]["traffic"] = traffic
+    if peaks:
+        stages["plan_loads"]["frac_vs_measured_peak"] = stages["plan_loads"]["achieved"] / peaks["hbm_read_GBs"]
+        stages["sinkhorn"]["frac_vs_measured_peak"] = stages["sinkhorn"]["achieved"] / peaks["fp32_tflops_unpacked"]
+    for k, f in floor.items():
+        stages[k]["floor_ms"] = f
+        stages[k]["frac_of_floor"] = f / stages[k]["ms_median"]
+    step = stats(run["step_ms"])
+    planner = dict(**step, floor_ms=sum(floor.values()), frac_of_floor=sum(floor.values()) / step["ms_median"])
+    summary = {"ms_per_step": run["ms_step"], "ms_median": step["ms_median"], "ms_min": step["ms_min"],
+               "plan_loads_ms": stages["plan_loads"]["ms_median"], "sinkhorn_ms": stages["sinkhorn"]["ms_median"],
+               "round_schedule_ms": stages["round_schedule"]["ms_median"],
+               "unfilled": int(sched.unfilled.sum().item())}
+    status = {"loads_nonzero": int((st_loads != 0).sum()), "sinkhorn_nonzero": int((st_flow != 0).sum()),
+              "schedule_unfilled": int(sched.unfilled.sum().item()), "schedule_nonzero": int((st_sched != 0).sum())}
+    return {"stages": stages, "planner": planner, "summary": summary, "status": status,
+            "phase3_rounds_mean": float(rounds[:, 1].mean())}
 
 
-def cpu_baseline(w, K, args, home_np, C_np, Bp_np, Ba_np):
+def host_cpu():
+    """The host's logical CPU count and model name."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "model": model}
+
+
+def cpu_baseline(w, K, args, home_np, C_np):
     """The oracle, as it is, on a sample of the workload's problems: ids made
-    on the host, plan_loads, then Sinkhorn passes over the sample until
-    --cpu-seconds have passed, then Phases 2-3 once."""
+    on the host (not timed), plan_loads (histogram ids/s), then Sinkhorn
+    passes over the sample until --cpu-seconds have passed, then Phases 2-3
+    once."""
     import numpy as np
 
     import oracle as O
@@ -411,36 +587,79 @@ def cpu_baseline(w, K, args, home_np, C_np, Bp_np, Ba_np):
     stride = max(1, B // args.cpu_sample)
     sample = list(range(0, B, stride))[: args.cpu_sample]
     threads = O.max_threads()
+    ids = np.stack([W.problem_ids_host(w, b) for b in sample])
     t = time.time()
-    parts = []
-    for b in sample:  # one problem of ids at a time (OpenMP over ranks; the buffer is reused)
-        ids = W.problem_ids_host(w, b)[None]
-        parts.append(O.plan_loads(ids, home_np, w.E))
-        del ids
-    t_gen_loads = time.time() - t
-    cat = lambda f: np.concatenate([getattr(x, f) for x in parts])
-    excess, spare, spill, alpha, n = cat("excess"), cat("spare"), cat("spill"), cat("alpha"), cat("n")
-    a, b, Cd = excess.astype(float), spare.astype(float), C_np.astype(float)
+    Lo = O.plan_loads(ids, home_np, w.E)
+    t_loads = time.time() - t
+    n_ids = ids.size
+    del ids
+    a, b, Cd = Lo.excess.astype(float), Lo.spare.astype(float), C_np.astype(float)
     passes, t_sk = 0, 0.0
     while t_sk < args.cpu_seconds or passes == 0:
         t = time.time()
         Po = O.sinkhorn(a, b, Cd, w.eps, w.iters)
         t_sk += time.time() - t
         passes += 1
+    Bp_np, Ba_np = O.topology_pref(C_np)
     t = time.time()
-    se, sa, _ = O.phase2(spill, spare, excess, alpha, home_np, Po.T.astype(np.float32), Bp_np, K)
-    O.phase3(n, se, sa, Ba_np, K, w.price_step)
+    se, sa, _ = O.phase2(Lo.spill, Lo.spare, Lo.excess, Lo.alpha, home_np, Po.T.astype(np.float32), Bp_np, K)
+    O.phase3(Lo.n, se, sa, Ba_np, K, w.price_step)
     t_sch = time.time() - t
     used = min(threads, len(sample))
-    log(f"[bench] oracle on {len(sample)} problems, {used} threads: ids + plan_loads {t_gen_loads:.1f}s, "
-        f"sinkhorn {passes} passes {t_sk:.1f}s, schedule {t_sch:.1f}s")
+    log(f"[bench] oracle on {len(sample)} problems, {used} threads: plan_loads {t_loads:.2f}s "
+        f"({n_ids / t_loads / 1e9:.2f} G ids/s), sinkhorn {passes} passes {t_sk:.1f}s, schedule {t_sch:.1f}s")
     return {
         "value": passes * len(sample) * w.iters / t_sk, "unit": "problem-iters/s", "cores": used, "kind": "oracle",
-        "sample": f"{len(sample)} of {B} problems (every {stride}th), ids generated on the host; fp64 C oracle "
-                  f"Sinkhorn at the full iteration count, {passes} passes over the sample ({t_sk:.1f} s), "
+        "sample": f"{len(sample)} of {B} problems (every {stride}th), ids generated on the host (not timed); fp64 "
+                  f"C oracle Sinkhorn at the full iteration count, {passes} passes over the sample ({t_sk:.1f} s), "
                   f"OpenMP over problems",
+        "histogram_ids_per_s": n_ids / t_loads,
         "schedule_s_per_problem": t_sch / len(sample),
+        "host": host_cpu(), "omp_threads": threads,
     }
+
+
+def cpu_extrapolate(gpu_rounds, cores):
+    """Full-step oracle latency of workloads 1-4, EXTRAPOLATED from one problem
+    of each on one thread: plan_loads as timed; the Sinkhorn timed for up to
+    20 iterations and scaled to the workload's count; Phase 2 as timed;
+    Phase 3 timed for up to 100 rounds and scaled by the mean rounds the GPU
+    schedule took; the B problems spread over `cores` threads."""
+    import numpy as np
+
+    import oracle as O
+    import workloads as W
+    out = {}
+    for wi in (1, 2, 3, 4):
+        w = W.WORKLOADS[wi]
+        home, C = W.home_map(w), W.cost_matrix(w)
+        ids = W.problem_ids_host(w, 0)[None]
+        t = time.time()
+        L = O.plan_loads(ids, home, w.E)
+        t_loads = time.time() - t
+        del ids
+        it = min(w.iters, 20)
+        t = time.time()
+        P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), w.eps, it)
+        t_sk = (time.time() - t) * w.iters / it
+        Bp, Ba = O.topology_pref(C)
+        t = time.time()
+        se, sa, _ = O.phase2(L.spill, L.spare, L.excess, L.alpha, home, P.T.astype(np.float32), Bp, w.K)
+        t_p2 = time.time() - t
+        tmax = 100
+        t = time.time()
+        _, _, rounds, _ = O.phase3(L.n, se, sa, Ba, w.K, w.price_step, t_max=tmax)
+        t_p3 = (time.time() - t) / max(int(rounds[0]), 1) * gpu_rounds.get(wi, int(rounds[0]))
+        per_problem = t_loads + t_sk + t_p2 + t_p3
+        waves = -(-w.B // cores)
+        out[str(wi)] = {"extrapolated_ms_per_step": per_problem * waves * 1e3,
+                        "per_problem_s": {"plan_loads": t_loads, "sinkhorn": t_sk, "phase2": t_p2, "phase3": t_p3},
+                        "note": f"extrapolated: one problem on one thread, x ceil({w.B} / {cores}) problems per "
+                                f"thread; Sinkhorn from {it} of {w.iters} iterations, Phase 3 from "
+                                f"{int(rounds[0])} rounds scaled to the GPU's mean"}
+        log(f"[bench] oracle extrapolation, workload {wi}: {per_problem:.2f} s per problem -> "
+            f"{per_problem * waves:.1f} s per step (extrapolated)")
+    return out
 
 
 if __name__ == "__main__":

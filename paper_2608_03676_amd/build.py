@@ -1,4 +1,5 @@
-"""Builds libtaot.so (all HIP sources, gfx950) in-tree with hipcc.
+"""Builds libtaot.so (all HIP sources, gfx950) and the benchmark's peak-probe
+library libtaot_probes.so in-tree with hipcc.
 
 Every floating-point operation rounds on its own (-ffp-contract=off; the
 Sinkhorn kernels request fused multiply-adds explicitly), and packed-FP32
@@ -17,6 +18,7 @@ ROOT = os.path.dirname(HERE)
 SOURCES = ["csrc/api.hip", "csrc/loads.hip", "csrc/sinkhorn.hip", "csrc/sk_reg_w4g4.hip", "csrc/sk_reg_w2g8.hip",
            "csrc/sk_reg_w2g2.hip", "csrc/schedule.hip"]
 LIB = os.path.join(HERE, "libtaot.so")
+PROBES_LIB = os.path.join(HERE, "libtaot_probes.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 FLAGS = ["-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-ffp-contract=off",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
@@ -46,6 +48,10 @@ def build(verbose: bool = False, incremental: bool = False):
     tmp = LIB + ".tmp"
     logs.append(_run(["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + [j[2] for j in jobs]))
     os.replace(tmp, LIB)
+    # the benchmark's peak probes: a library of their own
+    tmp = PROBES_LIB + ".tmp"
+    logs.append(_run(["hipcc", *FLAGS, "-shared", os.path.join(HERE, "csrc", "probes.hip"), "-o", tmp]))
+    os.replace(tmp, PROBES_LIB)
     if verbose:
         print("built", LIB)
         noise = "\n".join(l for l in logs if l)

@@ -31,6 +31,17 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_probe_library_exports_its_header():
+    """The benchmark's peak-probe library exports every symbol its header
+    declares (no kernel runs here)."""
+    src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "taot_probes.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(taot_probe_[a-z_]+)\s*\(", src)))
+    assert names == ["taot_probe_exp", "taot_probe_fma", "taot_probe_hbm_read", "taot_probe_lds"]
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_03676_amd", "libtaot_probes.so"))
+    for name in names:
+        assert hasattr(lib, name), name
+
+
 def test_status_strings():
     L = taot.lib()
     for code in range(5):
