@@ -521,11 +521,20 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 // the step is large against the spacing of doubles at the magnitudes reached,
 // bonus - price falls strictly with every service.  Within a tier the argmax
 // of the score is then the lowest-index rank among those with the fewest
-// services, found word by word (64 ranks) with a bit-sliced minimum over the
-// count bit-planes; the bid is the best tier result under (max score, lowest
-// rank), and tiers whose bonus is below the best score so far are skipped
-// (price >= 0).  A price step of 0 keeps every price at 0, and the argmax is
-// the lowest rank of the first non-empty tier.
+// services.  Every service raises one count by one and the counts of all
+// ranks stay close together, so the kernel keeps them relative to a base
+// (the fewest services of any rank): the rank set at the base count, and the
+// bit-planes of min(count - base, kRelMax), the relative code.  A tier's
+// fewest-services candidate is its lowest rank at the base count when there
+// is one, else the lowest rank of the smallest relative code (a bit-sliced
+// minimum over the four code planes, words jointly), and when every
+// candidate's code is saturated, the bit-sliced minimum over the planes of
+// the full counts.  The bid is the best tier result under (max score, lowest
+// rank).  No rank's price is below the price P0 of the base count, so a tier
+// whose bonus minus P0 is below the best score so far cannot win, nor can any
+// later (lower) tier.  A price step of 0 keeps every count and price at 0
+// (every rank stays at the base count), and the argmax is the lowest rank of
+// the first non-empty tier.
 //
 // Phase-3 arbitration by bonus.  Every live bid on rank r was placed at r's
 // current price (a slot re-bids when its rank serves), so among r's bidders
@@ -538,9 +547,8 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
 // slot-expert counts exceed the LDS layout.
 
 constexpr int kTierMax = 4;  // distinct bonus values per host column
-// The count window of the R = 1024 layout: the ranks with base + k services,
-// k < kLvl (base = the fewest services of any rank), as one rank set per k.
-constexpr int kLvl = 4;
+constexpr int kRelPlanes = 4;                       // bit-planes of the relative code
+constexpr int kRelMax = (1 << kRelPlanes) - 1;      // saturated code: count - base >= kRelMax
 
 struct LdsSmall {
   static constexpr int kT = 256;     // threads per problem
@@ -765,11 +773,13 @@ struct LdsState {
   double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
   int32_t* qbest;  // [R] q = min(spill, spare) of each cold rank's standing proposal
   // Phase 3 (aliases the Phase-2 region)
-  double* price; uint32_t* rkey; int32_t* work;
+  double* price; uint32_t* rkey; int32_t* work; uint32_t* sstate;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
-  // count window (TW > 4 only): [kLvl][TW] rank sets; lvl_base: base,
-  // minimum (rebase scratch), level-0 word emptied, by round parity (2)
-  uint64_t* lvl; int32_t* lvl_base;
+  // relative counts: lvl0 [TW] the ranks at the base count, rel [kRelPlanes]
+  // [TW] the code planes, p0 the price of the base count; misc: base,
+  // minimum (rebase scratch), a base-count word emptied (2, by round parity),
+  // a transfer made (2, by round parity), the base's epoch (rebases so far)
+  uint64_t* lvl0; uint64_t* rel; double* p0; int32_t* misc;
   int8_t* cn; double* cv; int32_t* cvr; uint32_t* cw; uint64_t* cm;
   size_t bytes;
 };
@@ -798,11 +808,14 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
   w.work = (int32_t*)take(4 * S1);
+  // slot bid states of the packed layout (16-word sets, at most two slots per thread)
+  w.sstate = (uint32_t*)take(TW > 4 && S1 <= 2 * (size_t)CF::kT ? 4 * S1 : 0);
   // the word lists guide the per-word search of sets wider than 4 words only
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
   w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
   w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * CF::kPL * TW);
-  w.lvl = (uint64_t*)take(TW > 4 ? 8 * kLvl * TW : 0); w.lvl_base = (int32_t*)take(TW > 4 ? 4 * 4 : 0);
+  w.lvl0 = (uint64_t*)take(8 * TW); w.rel = (uint64_t*)take(8 * kRelPlanes * TW);
+  w.p0 = (double*)take(8); w.misc = (int32_t*)take(4 * 8);
   w.cn = (int8_t*)take(SC);
   w.cv = (double*)take(8 * SC * kTierMax); w.cvr = (int32_t*)take(4 * SC * kTierMax);
   w.cw = (uint32_t*)take(4 * SC * kTierMax);
@@ -854,23 +867,6 @@ __device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
   const uint64_t m = __ballot(flag);
   if ((threadIdx.x & (kWave - 1)) == 0) buf[parity * NW + threadIdx.x / kWave] = m != 0;
   __syncthreads();
-  bool any = false;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) any |= buf[parity * NW + w] != 0;
-  parity ^= 1;
-  return any;
-}
-
-// block_or whose barrier orders LDS only: device-memory loads issued before it
-// may still be in flight after it (for values this thread itself uses later).
-template <int NT>
-__device__ __forceinline__ bool block_or_lds(bool flag, int32_t* buf, int& parity) {
-  constexpr int NW = NT / kWave;
-  const uint64_t m = __ballot(flag);
-  if ((threadIdx.x & (kWave - 1)) == 0) buf[parity * NW + threadIdx.x / kWave] = m != 0;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   bool any = false;
 #pragma unroll
   for (int w = 0; w < NW; ++w) any |= buf[parity * NW + w] != 0;
@@ -1172,14 +1168,14 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     L.cnt[r] = 0;
   }
   for (int32_t q = tid; q < CF::kPL * TW; q += NT) L.planes[q] = 0ull;
-  if constexpr (TW > 4) {
-    // count window: every rank starts with 0 services (level 0 of base 0)
-    for (int32_t q = tid; q < kLvl * TW; q += NT) {
-      const int32_t lo = (q % TW) * kWave;
-      L.lvl[q] = q >= TW || lo >= R ? 0ull : (R - lo >= kWave ? ~0ull : (1ull << (R - lo)) - 1ull);
-    }
-    if (tid == 0) { L.lvl_base[0] = 0; L.lvl_base[1] = INT_MAX; L.lvl_base[2] = 0; L.lvl_base[3] = 0; }
+  // every rank starts with 0 services: at the base count 0, code 0
+  for (int32_t q = tid; q < TW; q += NT) {
+    const int32_t lo = q * kWave;
+    L.lvl0[q] = lo >= R ? 0ull : (R - lo >= kWave ? ~0ull : (1ull << (R - lo)) - 1ull);
   }
+  for (int32_t q = tid; q < kRelPlanes * TW; q += NT) L.rel[q] = 0ull;
+  if (tid < 8) L.misc[tid] = tid == 1 ? INT_MAX : 0;
+  if (tid == 0) L.p0[0] = 0.0;
   const int32_t ns = wp.hdr[0];
   for (int32_t q = tid; q < ns; q += NT) L.cn[q] = (int8_t)wp.cn[q];
   for (int32_t q = tid; q < ns * kTierMax; q += NT) {
@@ -1204,271 +1200,406 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   __syncthreads();
 
   // Every bid names a rank, which then serves its best bidder with a positive
-  // amount; so every open slot with a valid rank bids again in every round,
-  // and the auction keeps a list of them.  A round is two steps, one barrier
-  // each, with the rank keys in two buffers by round parity and the list in
-  // one (every thread has read its items before the barrier that precedes
-  // the rewrite):
-  //   X: each listed slot bids and posts its key to the rank it bid for;
-  //   Y: the same thread moves tokens if its slot won, and keeps the slot on
-  //      next round's list while it still plans tokens.
+  // amount; so every open slot with a valid rank bids again in every round.
+  // A slot drops out once it is full or finds no valid rank (validity only
+  // ends).  The layout of 16-word rank sets (one problem per compute unit)
+  // keeps a list of the open slots, packed into the first waves each round,
+  // so that few waves issue the bid searches (the search is issue-bound),
+  // with each slot's bid state in LDS; the narrower layouts (several
+  // problems per compute unit, LDS scarce) and the largest slot counts keep
+  // each slot and its state with the thread that took it from the first
+  // round's list.  A round is two steps, one barrier each, with
+  // the rank keys and the list counts in two buffers by round parity and the
+  // list in one (every thread has read its entries before the barrier that
+  // precedes the rewrite):
+  //   X: each open slot bids and posts its key to the rank it bid for;
+  //   Y: the same thread moves tokens if its slot won, and keeps the slot
+  //      while it still plans tokens; a transfer marks the round, and a round
+  //      without one (no bid) ends the auction.
+  // Incremental bids.  A slot keeps, while the base count stays (an epoch),
+  // the first tier ts that holds a valid rank for it and a resume rank pos
+  // such that no valid rank of tier ts below pos is at the base count.  Both
+  // hold in later rounds: validity only ends and counts only rise.  So tiers
+  // before ts are empty, and the lowest base-count rank of tier ts at or
+  // after pos, when there is one, is the tier's fewest-services rank (score
+  // bonus - P0); the later tiers follow with the usual pruning.  Otherwise
+  // the full search runs from tier ts.  The bid rank becomes the next pos.
   const double step = p.price_step;
   const bool track = step > 0.0;  // counts order the prices; with step 0 all prices stay 0
   const int64_t tmax = p.t_max > 0 ? p.t_max : (int64_t)S * (R + 1);
   constexpr uint32_t kSlotMask = (1u << kItemSlotBits) - 1u, kExpMask = (1u << kItemExpertBits) - 1u;
+  constexpr int kPosBits = 11, kTsBits = 2;  // slot state: resume rank, first tier, epoch
+  static_assert(TW * kWave < (1 << kPosBits) && kTierMax <= (1 << kTsBits), "slot state fields");
+  // pack the open slots into the first waves each round (16-word sets, at
+  // most two slots per thread: the LDS of four does not hold their states)
+  constexpr bool kPack = TW > 4 && SPL <= 2;
+  int32_t item[SPL];
+  uint32_t state[SPL];
+#pragma unroll
+  for (int i = 0; i < SPL; ++i) {
+    item[i] = i * NT + tid < sh_nw[1] ? L.work[i * NT + tid] : -1;
+    state[i] = 0xFFFFFFFFu;  // no epoch matches it
+  }
+  if constexpr (kPack)
+    for (int32_t s = tid; s < S; s += NT) L.sstate[s] = 0xFFFFFFFFu;
   int64_t rounds = 0;
   for (int64_t t = 1; t <= tmax; ++t) {
     const int cur = (int)(t & 1), prv = cur ^ 1;
     uint32_t* rk = L.rkey + cur * R;
-    const int32_t* list = L.work;
-    const int32_t nw = sh_nw[cur];
     const int32_t maxc = sh_maxc;
     const int32_t nplanes = maxc > 0 ? 32 - __builtin_clz((uint32_t)maxc) : 0;
-    if (tid == 0) sh_nw[prv] = 0;
+    const double P0 = L.p0[0];
+    const uint32_t epoch = (uint32_t)L.misc[6];
+    const int32_t nw = sh_nw[cur];
+    if (kPack && tid == 0) sh_nw[prv] = 0;
     for (int32_t r = tid; r < R; r += NT) L.rkey[prv * R + r] = 0;
     // ---- X: bids --------------------------------------------------------------------------
-    int32_t item[SPL], bid[SPL], held[SPL];
+    int32_t bid[SPL], held[SPL];
     uint32_t key[SPL];
-    bool any = false;
 #pragma unroll
     for (int i = 0; i < SPL; ++i) {
-      const int32_t q = i * NT + tid;
-      item[i] = -1;
       bid[i] = -1;
       key[i] = 0;
       held[i] = 0;
-      if (q >= nw) continue;
-      const int32_t it = list[q];
-      item[i] = it;
+      if constexpr (kPack) {
+        const int32_t q = i * NT + tid;
+        item[i] = q < nw ? L.work[q] : -1;
+        if (item[i] >= 0) state[i] = L.sstate[item[i] & kSlotMask];
+      }
+      const int32_t it = item[i];
+      if (it < 0) continue;
       const int32_t s = it & kSlotMask, d = (it >> kItemSlotBits) & kExpMask;
       const int32_t st = it >> (kItemSlotBits + kItemExpertBits);
       // argmax over ranks holding tokens of the slot's expert of
       // Bauct[r][host] - price[r], lowest rank on ties, by tiers
       const int32_t nt = L.cn[st];
       const uint64_t* vm = L.vmask + d * TW;
+      int32_t ts = 0, pos = 0;
+      if ((state[i] >> (kPosBits + kTsBits)) == epoch) {
+        ts = (int32_t)((state[i] >> kPosBits) & ((1u << kTsBits) - 1u));
+        pos = (int32_t)(state[i] & ((1u << kPosBits) - 1u));
+      }
       double bs = -INFINITY;
       int32_t br = INT_MAX, bv = 0;
+      int32_t nts = -1, npos = R;  // the new state: first tier with a valid rank, its base-count rank
       if constexpr (TW <= 4) {
-        // rank sets of at most 4 words live in registers: a candidate set in
-        // one word takes a one-word bit-slice, others a joint one
+        // rank sets of at most 4 words live in registers; the tier data is
+        // read per tier (the registers of the capped builds are scarce)
         uint64_t valid[TW];
 #pragma unroll
         for (int w = 0; w < TW; ++w) valid[w] = vm[w];
-        for (int32_t ti = 0; ti < nt; ++ti) {
-          const double v = L.cv[st * kTierMax + ti];
-          if (v < bs) break;  // every score in this tier and the next is <= its bonus
+        // lowest valid rank of tier ti at the base count, at or after rank from
+        auto scan0 = [&](int32_t ti, int32_t from) {
           const uint64_t* tm = L.cm + (st * kTierMax + ti) * TW;
-          uint64_t c[TW];
-          uint32_t wm = 0;  // words holding candidates
+          int32_t hit = INT_MAX;
 #pragma unroll
-          for (int w = 0; w < TW; ++w) {
-            c[w] = tm[w] & valid[w];
-            wm |= (c[w] != 0ull ? 1u : 0u) << w;
+          for (int w = TW - 1; w >= 0; --w) {
+            uint64_t h = tm[w] & valid[w] & L.lvl0[w];
+            h = w < (from >> 6) ? 0ull : w == (from >> 6) ? h & (~0ull << (from & 63)) : h;
+            if (h) hit = w * kWave + __builtin_ctzll(h);
           }
-          if (!wm) continue;
-          int32_t r;
-          if ((wm & (wm - 1)) == 0) {
-            const int w = __builtin_ctz(wm);
-            uint64_t x = 0;
+          return hit;
+        };
+        // fewest services among the valid ranks of tier ti: the smallest
+        // relative code, then (all saturated) the smallest count; one plane
+        // per step; INT_MAX when the tier holds no valid rank
+        auto deep = [&](int32_t ti) {
+          const uint64_t* tm = L.cm + (st * kTierMax + ti) * TW;
+          uint64_t c[TW], m[TW];
+          uint64_t anyc = 0;
 #pragma unroll
-            for (int u = 0; u < TW; ++u) x = u == w ? c[u] : x;
-            if (track && (x & (x - 1))) {
-              // fewest services: keep the ranks with a 0 in each bit-plane, top
-              // down, whenever any remain (four planes per load batch)
-              for (int32_t j0 = nplanes - 1; j0 >= 0; j0 -= 4) {
-                uint64_t pl[4];
+          for (int w = 0; w < TW; ++w) { c[w] = tm[w] & valid[w]; anyc |= c[w]; }
+          if (!anyc) return (int32_t)INT_MAX;
+          bool sat = true;
+#pragma unroll 1
+          for (int j = kRelPlanes - 1; j >= 0; --j) {
+            uint64_t mm = 0;
 #pragma unroll
-                for (int u = 0; u < 4; ++u) pl[u] = j0 - u >= 0 ? L.planes[(j0 - u) * TW + w] : 0ull;
+            for (int w = 0; w < TW; ++w) { m[w] = c[w] & ~L.rel[j * TW + w]; mm |= m[w]; }
+            sat &= mm == 0ull;
+            if (mm) {
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                  const uint64_t m = x & ~pl[u];
-                  x = m ? m : x;
-                }
+              for (int w = 0; w < TW; ++w) c[w] = m[w];
+            }
+          }
+          if (sat && track) {
+            for (int32_t j = nplanes - 1; j >= 0; --j) {
+              uint64_t mm = 0;
+#pragma unroll
+              for (int w = 0; w < TW; ++w) { m[w] = c[w] & ~L.planes[j * TW + w]; mm |= m[w]; }
+              if (mm) {
+#pragma unroll
+                for (int w = 0; w < TW; ++w) c[w] = m[w];
               }
             }
-            r = w * kWave + __builtin_ctzll(x);
+          }
+          int32_t rr = INT_MAX;
+#pragma unroll
+          for (int w = TW - 1; w >= 0; --w)
+            if (c[w]) rr = w * kWave + __builtin_ctzll(c[w]);
+          return rr;
+        };
+        int32_t t0 = ts;
+        bool resume_fail = false;  // tier ts holds no valid rank at the base count
+        if (ts < nt) {
+          const int32_t h = scan0(ts, pos);
+          if (h != INT_MAX) {
+            bs = L.cv[st * kTierMax + ts] - P0;
+            br = h;
+            bv = L.cvr[st * kTierMax + ts];
+            nts = ts;
+            npos = h;
+            t0 = ts + 1;
           } else {
-            if (track) {
-              for (int32_t j = nplanes - 1; j >= 0; --j) {
-                uint64_t m[TW];
-                uint64_t mm = 0;
-#pragma unroll
-                for (int w = 0; w < TW; ++w) { m[w] = c[w] & ~L.planes[j * TW + w]; mm |= m[w]; }
-                if (mm) {
-#pragma unroll
-                  for (int w = 0; w < TW; ++w) c[w] = m[w];
-                }
-              }
-            }
-            r = INT_MAX;
-#pragma unroll
-            for (int w = TW - 1; w >= 0; --w)
-              if (c[w]) r = w * kWave + __builtin_ctzll(c[w]);
+            resume_fail = true;
           }
-          const double sc = v - L.price[r];
-          if (sc > bs || (sc == bs && r < br)) { bs = sc; br = r; bv = L.cvr[st * kTierMax + ti]; }
+        }
+        for (int32_t ti = t0; ti < nt; ++ti) {
+          const double v = L.cv[st * kTierMax + ti];
+          if (v - P0 < bs) break;  // no score in this tier or the next reaches bs
+          const int32_t h = resume_fail && ti == ts ? INT_MAX : scan0(ti, 0);
+          const bool at0 = h != INT_MAX;  // a candidate at the base count: its price is P0
+          const int32_t rr = at0 ? h : deep(ti);
+          if (rr == INT_MAX) continue;  // no valid rank in this tier
+          if (nts < 0) { nts = ti; npos = at0 ? h : R; }
+          const double sc = v - (at0 ? P0 : L.price[rr]);
+          if (sc > bs || (sc == bs && rr < br)) { bs = sc; br = rr; bv = L.cvr[st * kTierMax + ti]; }
         }
       } else {
         const uint32_t vw = L.vwords[d];
-        for (int32_t ti = 0; ti < nt; ++ti) {
-          const double v = L.cv[st * kTierMax + ti];
-          if (v < bs) break;  // every score in this tier and the next is <= its bonus
-          const uint64_t* tm = L.cm + (st * kTierMax + ti) * TW;
-          // fewest services among the tier's valid ranks, word by word over the
-          // words that hold both: keep the ranks with a 0 in each bit-plane, top
-          // down, whenever any remain; a word's minimum count is the planes
-          // where none remained
+        // the structure's tier bonuses, bonus ranks and words, loaded once
+        // (16-byte loads); the tier loop is unrolled so that they stay in
+        // registers
+        double cvv[kTierMax];
+        int32_t cvrr[kTierMax];
+        uint32_t cww[kTierMax];
+        {
+          const double2* cv2 = reinterpret_cast<const double2*>(L.cv + st * kTierMax);
+          const double2 a = cv2[0], b2 = cv2[1];
+          cvv[0] = a.x; cvv[1] = a.y; cvv[2] = b2.x; cvv[3] = b2.y;
+          const int4 r4 = *reinterpret_cast<const int4*>(L.cvr + st * kTierMax);
+          cvrr[0] = r4.x; cvrr[1] = r4.y; cvrr[2] = r4.z; cvrr[3] = r4.w;
+          const uint4 w4 = *reinterpret_cast<const uint4*>(L.cw + st * kTierMax);
+          cww[0] = w4.x; cww[1] = w4.y; cww[2] = w4.z; cww[3] = w4.w;
+        }
+        // lowest valid rank of a tier at the base count, at or after rank
+        // from: the tier's words with valid ranks, ascending, one per step
+        auto scan0 = [&](const uint64_t* tm, uint32_t words, int32_t from) {
+          const int32_t wf = from >> 6;
+          for (uint32_t ws = wf < 32 ? words & (~0u << wf) : 0u; ws; ws &= ws - 1u) {
+            const int w = __builtin_ctz(ws);
+            uint64_t h = tm[w] & vm[w] & L.lvl0[w];
+            if (w == wf) h &= ~0ull << (from & 63);
+            if (h) return w * kWave + __builtin_ctzll(h);
+          }
+          return (int32_t)INT_MAX;
+        };
+        // fewest services among the valid ranks of a tier: the smallest
+        // relative code over its words with valid ranks, up to four words per
+        // group (a bit-sliced minimum within the group; a group replaces the
+        // best only with a smaller code, so equal codes keep the lower
+        // words), then (all saturated) the bit-plane search over the full
+        // counts; INT_MAX when the tier holds no valid rank
+        auto deep = [&](const uint64_t* tm, uint32_t words) {
           int32_t rr = INT_MAX;
-          uint32_t cmin = 0xFFFFFFFFu;
-          // The count window first, level by level, words ascending (four
-          // per batch of loads): the first hit is the lowest rank among the
-          // fewest services.  The first pass, through the lowest level
-          // (never empty when a round starts), notes the words that hold
-          // candidates.  With a price step of 0 the first candidate wins.
-          auto scan = [&](uint32_t words, const uint64_t* lv, uint32_t* cand_out) {
-            int32_t hit = INT_MAX;
-            while (words && hit == INT_MAX) {
-              int wi[4];
-              uint64_t xt[4], xl[4];
+          uint32_t best = kRelMax + 1, cand = 0;
+          for (uint32_t wl = words; wl;) {
+            int wi[4];
+            uint64_t c[4];
 #pragma unroll
-              for (int u = 0; u < 4; ++u) {
-                wi[u] = words ? __builtin_ctz(words) : -1;
-                words &= words - 1u;
-              }
+            for (int u = 0; u < 4; ++u) {
+              wi[u] = wl ? __builtin_ctz(wl) : -1;
+              wl &= wl - 1u;
+            }
+            uint64_t pl[kRelPlanes][4];
+            uint64_t any = 0;
 #pragma unroll
-              for (int u = 0; u < 4; ++u) {
-                const int w = wi[u] < 0 ? 0 : wi[u];
-                xt[u] = wi[u] < 0 ? 0ull : tm[w] & vm[w];
-                xl[u] = lv ? xt[u] & lv[w] : xt[u];
-              }
+            for (int u = 0; u < 4; ++u) {
+              const int w = wi[u] < 0 ? 0 : wi[u];
+              c[u] = wi[u] < 0 ? 0ull : tm[w] & vm[w];
+              any |= c[u];
+              cand |= (c[u] != 0ull ? 1u : 0u) << w;
 #pragma unroll
-              for (int u = 3; u >= 0; --u) {
-                if (cand_out && xt[u]) *cand_out |= 1u << wi[u];
-                if (xl[u]) hit = wi[u] * kWave + __builtin_ctzll(xl[u]);
+              for (int j = 0; j < kRelPlanes; ++j) pl[j][u] = L.rel[j * TW + w];
+            }
+            if (!any) continue;
+            uint32_t code = 0;
+#pragma unroll
+            for (int j = kRelPlanes - 1; j >= 0; --j) {
+              uint64_t m[4], mm = 0;
+#pragma unroll
+              for (int u = 0; u < 4; ++u) { m[u] = c[u] & ~pl[j][u]; mm |= m[u]; }
+              if (mm) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) c[u] = m[u];
+              } else {
+                code |= 1u << j;
               }
             }
-            return hit;
-          };
-          uint32_t cand = 0;
-          rr = scan(L.cw[st * kTierMax + ti] & vw, track ? L.lvl : nullptr, &cand);
-          if (!cand) continue;  // no valid rank in this tier
-          for (int k = 1; k < kLvl && rr == INT_MAX; ++k) rr = scan(cand, L.lvl + k * TW, nullptr);
-          // beyond the window: the bit-plane search over the candidate words
-          for (uint32_t words = rr == INT_MAX ? cand : 0u; words; words &= words - 1) {
-            const int w = __builtin_ctz(words);
-            uint64_t x = tm[w] & vm[w];
-            if (!x) continue;
-            uint32_t mn = 0;
-            if (track) {
+            if (code < best) {
+              best = code;
+#pragma unroll
+              for (int u = 3; u >= 0; --u)
+                if (c[u]) rr = wi[u] * kWave + __builtin_ctzll(c[u]);
+            }
+          }
+          if (best == kRelMax && track) {
+            // a word's minimum count is the planes where no candidate remained
+            rr = INT_MAX;
+            uint32_t cmin = 0xFFFFFFFFu;
+            for (uint32_t ws = cand; ws; ws &= ws - 1) {
+              const int w = __builtin_ctz(ws);
+              uint64_t x = tm[w] & vm[w];
+              uint32_t mn = 0;
               for (int32_t j = nplanes - 1; j >= 0; --j) {
                 const uint64_t m = x & ~L.planes[j * TW + w];
                 if (m) x = m;
                 else mn |= 1u << j;
               }
-            }
-            if (mn < cmin) {  // words ascend: equal counts keep the lower rank
-              cmin = mn;
-              rr = w * kWave + __builtin_ctzll(x);
+              if (mn < cmin) {  // words ascend: equal counts keep the lower rank
+                cmin = mn;
+                rr = w * kWave + __builtin_ctzll(x);
+              }
             }
           }
-          if (rr == INT_MAX) continue;
-          const double sc = v - L.price[rr];
-          if (sc > bs || (sc == bs && rr < br)) { bs = sc; br = rr; bv = L.cvr[st * kTierMax + ti]; }
+          return rr;
+        };
+        bool resume_fail = false;  // tier ts holds no valid rank at the base count
+        int32_t t0 = ts;
+        if (ts < nt) {
+          // the register arrays indexed by ts without dynamic indexing
+          const uint32_t cw_ts = ts == 0 ? cww[0] : ts == 1 ? cww[1] : ts == 2 ? cww[2] : cww[3];
+          const int32_t h = scan0(L.cm + (st * kTierMax + ts) * TW, cw_ts & vw, pos);
+          if (h != INT_MAX) {
+            bs = (ts == 0 ? cvv[0] : ts == 1 ? cvv[1] : ts == 2 ? cvv[2] : cvv[3]) - P0;
+            br = h;
+            bv = ts == 0 ? cvrr[0] : ts == 1 ? cvrr[1] : ts == 2 ? cvrr[2] : cvrr[3];
+            nts = ts;
+            npos = h;
+            t0 = ts + 1;
+          } else {
+            resume_fail = true;
+          }
         }
+#pragma unroll
+        for (int ti = 0; ti < kTierMax; ++ti) {
+          if (ti < t0) continue;
+          if (ti >= nt) break;
+          const double v = cvv[ti];
+          if (v - P0 < bs) break;  // no score in this tier or the next reaches bs
+          const uint32_t cwt = cww[ti] & vw;
+          if (!cwt) continue;  // no valid rank in this tier
+          const uint64_t* tm = L.cm + (st * kTierMax + ti) * TW;
+          const int32_t h = resume_fail && ti == ts ? INT_MAX : scan0(tm, cwt, 0);
+          const bool at0 = h != INT_MAX;  // a candidate at the base count: its price is P0
+          const int32_t rr = at0 ? h : deep(tm, cwt);
+          if (rr == INT_MAX) continue;  // no valid rank in this tier
+          if (nts < 0) { nts = ti; npos = at0 ? h : R; }
+          const double sc = v - (at0 ? P0 : L.price[rr]);
+          if (sc > bs || (sc == bs && rr < br)) { bs = sc; br = rr; bv = cvrr[ti]; }
+        }
+      }
+      if (nts >= 0) {
+        state[i] = (uint32_t)npos | ((uint32_t)nts << kPosBits) | (epoch << (kPosBits + kTsBits));
+        if constexpr (kPack) L.sstate[s] = state[i];
       }
       if (br != INT_MAX) {
         bid[i] = br;
         key[i] = ((uint32_t)bv << 16) | (uint32_t)(0xFFFF - s);  // bonus, then lowest slot
         held[i] = np[(int64_t)d * R + br];
         atomicMax(&rk[br], key[i]);
-        any = true;
       }
     }
-    // no bid: the state is final.  The barrier orders the keys (LDS); the
-    // token loads above complete on their own before Y uses them.
-    if (!block_or_lds<NT>(any, flagbuf, parity)) break;
+    // the barrier orders the keys (LDS); the token loads above complete on
+    // their own before Y uses them
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
     // ---- Y: transfers -----------------------------------------------------------------------
-    if constexpr (TW > 4)
-      if (tid == 0) L.lvl_base[2 + prv] = 0;  // read by every thread before the barrier above
+    // the flags of the next round (read by every thread before the barrier above)
+    if (tid == 0) { L.misc[2 + prv] = 0; L.misc[4 + prv] = 0; }
     int32_t newmax = 0;
 #pragma unroll
     for (int i = 0; i < SPL; ++i) {
       const int32_t r = bid[i];
-      bool keep = false;
-      if (r >= 0) {
+      // a slot without a bid has no valid rank left (validity only ends)
+      bool keep = r >= 0;
+      if (keep && rk[r] == key[i]) {
         const int32_t s = item[i] & kSlotMask, d = (item[i] >> kItemSlotBits) & kExpMask;
         int32_t a = L.amt[s];
-        if (rk[r] == key[i]) {
-          const int32_t have = held[i];
-          const int32_t x = have < a ? have : a;
-          Xb[(int64_t)r * S + s] = x;
-          np[(int64_t)d * R + r] = have - x;
-          a -= x;
-          L.amt[s] = a;
-          const uint64_t bit = 1ull << (r & 63);
-          if (x > 0) {
-            L.price[r] = L.price[r] + step;
-            if (track) {
-              const int32_t c0 = L.cnt[r], c1 = c0 + 1;
-              L.cnt[r] = c1;
-              newmax = c1 > newmax ? c1 : newmax;
-              for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
-                atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]),
-                          bit);
-              if constexpr (TW > 4) {
-                // the rank moves up one level of the count window; a word of
-                // the lowest level that empties is flagged for the round's end
-                const int32_t k0 = c0 - L.lvl_base[0];
-                if (k0 < kLvl) {
-                  const uint64_t old =
-                      atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl[k0 * TW + (r >> 6)]), bit);
-                  if (k0 == 0 && old == bit) L.lvl_base[2 + cur] = 1;
-                }
-                if (k0 + 1 < kLvl)
-                  atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl[(k0 + 1) * TW + (r >> 6)]), bit);
-              }
+        const int32_t have = held[i];
+        const int32_t x = have < a ? have : a;
+        Xb[(int64_t)r * S + s] = x;
+        np[(int64_t)d * R + r] = have - x;
+        a -= x;
+        L.amt[s] = a;
+        keep = a > 0;
+        const uint64_t bit = 1ull << (r & 63);
+        if (x > 0) {
+          L.misc[4 + cur] = 1;
+          L.price[r] = L.price[r] + step;
+          if (track) {
+            const int32_t c0 = L.cnt[r], c1 = c0 + 1;
+            L.cnt[r] = c1;
+            newmax = c1 > newmax ? c1 : newmax;
+            for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
+              atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
+            // the relative code rises by one (below saturation); a word of the
+            // base-count set that empties is flagged for the round's end
+            const int32_t k0 = c0 - L.misc[0];
+            if (k0 < kRelMax)
+              for (uint32_t flip = (uint32_t)(k0 ^ (k0 + 1)); flip; flip &= flip - 1)
+                atomicXor(reinterpret_cast<unsigned long long*>(&L.rel[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
+            if (k0 == 0) {
+              const uint64_t old = atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl0[r >> 6]), bit);
+              if (old == bit) L.misc[2 + cur] = 1;
             }
           }
-          if (have - x <= 0) {
-            const uint64_t old = atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * TW + (r >> 6)]), ~bit);
-            if constexpr (TW > 4)  // the word list only guides the per-word search
-              if ((old & ~bit) == 0ull) atomicAnd(&L.vwords[d], ~(1u << (r >> 6)));
-          }
         }
-        keep = a > 0;
+        if (have - x <= 0) {
+          const uint64_t old = atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * TW + (r >> 6)]), ~bit);
+          if constexpr (TW > 4)  // the word list only guides the per-word search
+            if ((old & ~bit) == 0ull) atomicAnd(&L.vwords[d], ~(1u << (r >> 6)));
+        }
       }
-      list_append(keep, item[i], L.work, &sh_nw[prv]);
+      if constexpr (kPack)
+        list_append(keep, item[i], L.work, &sh_nw[prv]);
+      else if (!keep)
+        item[i] = -1;
     }
     newmax = wave_max_i32(newmax);
     if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
     __syncthreads();
+    if (!L.misc[4 + cur]) break;  // no bid this round: the state is final
     rounds = t;
-    if constexpr (TW > 4) {
-      bool l0_empty = false;
-      if (track && L.lvl_base[2 + cur]) {
-        l0_empty = true;
+    bool l0_empty = false;
+    if (track && L.misc[2 + cur]) {
+      l0_empty = true;
 #pragma unroll
-        for (int w = 0; w < TW; ++w) l0_empty &= L.lvl[w] == 0ull;
-      }
-      if (l0_empty) {
-        // Every rank has left the window's lowest level: the base moves to
-        // the new fewest services and the window is rebuilt from the counts.
-        // Rank r is thread r, so wave w builds word w.
-        const int32_t mine = tid < R ? L.cnt[tid] : INT_MAX;
-        const int32_t wmin = -wave_max_i32(-mine);
-        if (lane == 0) atomicMin(&L.lvl_base[1], wmin);
-        __syncthreads();
-        const int32_t nb = L.lvl_base[1];
-        const int32_t kr = tid < R ? L.cnt[tid] - nb : -1;
+      for (int w = 0; w < TW; ++w) l0_empty &= L.lvl0[w] == 0ull;
+    }
+    if (l0_empty) {
+      // Every rank has left the base count: the base moves to the new fewest
+      // services and the relative codes are rebuilt from the counts.  Rank r
+      // is thread r, so wave w builds word w; p0 takes the price of a rank at
+      // the new base (every such rank has the same price).
+      const int32_t mine = tid < R ? L.cnt[tid] : INT_MAX;
+      const int32_t wmin = -wave_max_i32(-mine);
+      if (lane == 0) atomicMin(&L.misc[1], wmin);
+      __syncthreads();
+      const int32_t nb = L.misc[1];
+      const int32_t kr = tid < R ? min(L.cnt[tid] - nb, kRelMax) : -1;
+      const uint64_t m0 = __ballot(kr == 0);
+      if (lane == 0 && wid < TW) L.lvl0[wid] = m0;
 #pragma unroll
-        for (int k = 0; k < kLvl; ++k) {
-          const uint64_t m = __ballot(kr == k);
-          if (lane == 0 && wid < TW) L.lvl[k * TW + wid] = m;
-        }
-        __syncthreads();
-        if (tid == 0) { L.lvl_base[0] = nb; L.lvl_base[1] = INT_MAX; }
-        __syncthreads();
+      for (int j = 0; j < kRelPlanes; ++j) {
+        const uint64_t m = __ballot(kr > 0 && ((kr >> j) & 1));
+        if (lane == 0 && wid < TW) L.rel[j * TW + wid] = m;
       }
+      if (kr == 0) L.p0[0] = L.price[tid];
+      __syncthreads();
+      if (tid == 0) { L.misc[0] = nb; L.misc[1] = INT_MAX; L.misc[6] += 1; }
+      __syncthreads();
     }
   }
 
