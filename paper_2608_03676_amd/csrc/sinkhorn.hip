@@ -40,8 +40,13 @@ namespace {
 // entries that holds a NaN or an infinity, once per call for a shared C and
 // once per problem for per-problem costs; the class prepass and the LDS and
 // streamed kernels OR the chunk marks of their problem's matrix.
-constexpr int64_t kScanChunk = 65536;
+// A chunk is 4096 entries: four 16-byte loads per thread of a 256-thread
+// block, all in flight at once (a longer chunk per block leaves the scan
+// waiting on one load after another).
+constexpr int64_t kScanChunk = 4096;
 constexpr int kScanThreads = 256;
+constexpr int kScanLoads = 4;
+static_assert(kScanChunk == 4 * kScanLoads * kScanThreads, "four float4 loads per thread and chunk");
 __host__ __device__ constexpr int32_t scan_chunks(int32_t R) {
   return (int32_t)(((int64_t)R * R + kScanChunk - 1) / kScanChunk);
 }
@@ -52,9 +57,17 @@ cost_scan_kernel(const float* __restrict__ C, int64_t R2, int32_t chunks, int32_
   const float* c = C + mat * R2;
   const int64_t lo = ch * kScanChunk, hi = lo + kScanChunk < R2 ? lo + kScanChunk : R2;
   int bad = 0;
-  for (int64_t q = lo + threadIdx.x; q < hi; q += kScanThreads) {
-    const float x = c[q];
-    bad |= !(x - x == 0.f);  // NaN or +-inf
+  auto nonfinite = [](float x) { return !(x - x == 0.f); };  // NaN or +-inf
+  if (hi - lo == kScanChunk && (reinterpret_cast<uintptr_t>(c + lo) & 15u) == 0) {
+    const float4* c4 = reinterpret_cast<const float4*>(c + lo) + threadIdx.x;
+    float4 x[kScanLoads];
+#pragma unroll
+    for (int k = 0; k < kScanLoads; ++k) x[k] = c4[k * kScanThreads];
+#pragma unroll
+    for (int k = 0; k < kScanLoads; ++k)
+      bad |= nonfinite(x[k].x) | nonfinite(x[k].y) | nonfinite(x[k].z) | nonfinite(x[k].w);
+  } else {
+    for (int64_t q = lo + threadIdx.x; q < hi; q += kScanThreads) bad |= nonfinite(c[q]);
   }
   bad = __syncthreads_or(bad);
   if (threadIdx.x == 0) cbad[blockIdx.x] = bad ? 1 : 0;
@@ -321,58 +334,51 @@ __global__ void __launch_bounds__(kWave) wave_class_kernel(SkParams p, int32_t* 
 }
 
 // Multi and single lists of the W-wave kernel (one block), each by descending
-// per-wave work (ascending index within equal work), so that the workgroups
-// dealt out in order start with the heaviest and mix heavy and light work on
-// every compute unit; single groups join problems of similar work.
+// per-wave work, so that the workgroups dealt out in order start with the
+// heaviest and mix heavy and light work on every compute unit; single groups
+// join problems of similar work.  A counting sort over the per-wave work
+// (below 64): count, exclusive scan from the heaviest down, place.  The order
+// within equal work is whatever the atomics give: it changes the placement
+// of problems on the chip, never a result.  Then the wide problems.
 __global__ void __launch_bounds__(kSkThreads) wave_order_kernel(const int32_t* __restrict__ cls, int32_t B, int32_t W,
                                                                 int32_t* __restrict__ multi,
                                                                 int32_t* __restrict__ single,
                                                                 int32_t* __restrict__ wide,
                                                                 int32_t* __restrict__ counts) {
-  __shared__ int32_t wave_cnt[kSkWaves];
-  __shared__ unsigned long long present[2];  // multi / single: bit w if some problem has per-wave work w
-  if (threadIdx.x == 0) present[0] = present[1] = 0ull;
+  __shared__ int32_t bins[3][64];  // multi, single, wide (bin 0) counts, then cursors
+  for (int q = threadIdx.x; q < 3 * 64; q += kSkThreads) (&bins[0][0])[q] = 0;
+  __syncthreads();
+  auto key = [&](int32_t c, int& list) {
+    if (is_wide_class(c)) { list = 2; return 0; }
+    if (!is_reg_class(c)) { list = -1; return 0; }
+    const int cpl = class_cpl(c), c8 = class_c8(c);
+    list = is_single(W, cpl, c8) ? 1 : 0;
+    return c8_per_wave(W, cpl, c8) * cpl;  // per-wave work, 1 .. 32
+  };
+  for (int32_t b = threadIdx.x; b < B; b += kSkThreads) {
+    int list;
+    const int wk = key(cls[b], list);
+    if (list >= 0) atomicAdd(&bins[list][wk], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    const int k = threadIdx.x;
+    int32_t s = 0;
+    for (int wk = 63; wk >= 0; --wk) {  // heaviest first
+      const int32_t n = bins[k][wk];
+      bins[k][wk] = s;
+      s += n;
+    }
+    counts[k] = s;
+  }
   __syncthreads();
   for (int32_t b = threadIdx.x; b < B; b += kSkThreads) {
-    const int32_t c = cls[b];
-    if (!is_reg_class(c)) continue;
-    const int cpl = class_cpl(c), c8 = class_c8(c);
-    atomicOr(&present[is_single(W, cpl, c8) ? 1 : 0], 1ull << (c8_per_wave(W, cpl, c8) * cpl));
+    int list;
+    const int wk = key(cls[b], list);
+    if (list < 0) continue;
+    const int32_t pos = atomicAdd(&bins[list][wk], 1);
+    (list == 0 ? multi : list == 1 ? single : wide)[pos] = b;
   }
-  __syncthreads();
-  for (int k = 0; k < 2; ++k) {
-    const unsigned long long works = present[k];
-    int32_t* list = k == 0 ? multi : single;
-    int32_t n = 0;
-    for (int32_t wk = 63; wk > 0; --wk) {
-      if (!((works >> wk) & 1ull)) continue;
-      for (int32_t base = 0; base < B; base += kSkThreads) {
-        const int32_t b = base + (int32_t)threadIdx.x;
-        const int32_t c = b < B ? cls[b] : 0;
-        bool f = false;
-        if (is_reg_class(c)) {
-          const int cpl = class_cpl(c), c8 = class_c8(c);
-          f = (is_single(W, cpl, c8) ? 1 : 0) == k && c8_per_wave(W, cpl, c8) * cpl == wk;
-        }
-        int32_t tot;
-        const int32_t pos = chunk_compact(f, wave_cnt, tot);
-        if (f) list[n + pos] = b;
-        n += tot;
-      }
-    }
-    if (threadIdx.x == 0) counts[k] = n;
-  }
-  // the wide problems, by index
-  int32_t n = 0;
-  for (int32_t base = 0; base < B; base += kSkThreads) {
-    const int32_t b = base + (int32_t)threadIdx.x;
-    const bool f = b < B && is_wide_class(cls[b]);
-    int32_t tot;
-    const int32_t pos = chunk_compact(f, wave_cnt, tot);
-    if (f) wide[n + pos] = b;
-    n += tot;
-  }
-  if (threadIdx.x == 0) counts[2] = n;
 }
 
 // ---------------------------------------------------------------------------
