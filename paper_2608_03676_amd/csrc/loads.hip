@@ -7,12 +7,18 @@
 // is exact; rho and alpha are one rounded fp64 division each.
 //
 // Kernels
-//   home_csr_kernel    (1 block)      rank -> experts lists of the home map.
+//   home_csr_kernel    (1 block)      rank -> experts lists of the home map
+//                                     (counts, scan, placement; the order of
+//                                     a rank's list is not used).
 //   histogram_kernel   (B*R blocks)   one (problem, source rank) row per block;
 //                                     streams the ids once (HBM-bound) into LDS
-//                                     counters privatised per lane group.
-//   marginals_kernel   (B blocks)     reads n once; loads, mean, excess/spare,
-//                                     rho, alpha, spill.
+//                                     counters privatised per lane group (32-bit,
+//                                     or two 16-bit counters per word when the
+//                                     experts are many and a row short enough).
+//   expert_load_kernel (B*E/256)      x_e = sum_r n_re: reads n once, coalesced,
+//                                     four experts per lane, rows over the waves.
+//   marginals_kernel   (B blocks)     loads, mean, excess/spare, rho, alpha,
+//                                     spill from x.
 #include <mutex>
 
 #include "common.h"
@@ -24,72 +30,101 @@ constexpr int kCsrThreads = 1024;
 constexpr int kHistThreads = 256;
 constexpr int kHistUnroll = 4;
 constexpr int kMargThreads = 256;
-constexpr int kHistLdsWords = 16384;  // 64 KiB of counters per block when possible
+constexpr int kColThreads = 256;
+constexpr int kColExperts = 4 * kWave;         // experts per expert_load_kernel block
+constexpr int kHistLdsWords = 16384;           // 64 KiB of 32-bit counters per block when possible
+constexpr int kHistLdsWords16 = 8200;          // about 32 KiB of 16-bit counter pairs
+constexpr int kHist16MinCopies = 4;            // 16-bit counters when 32-bit ones allow fewer copies
 
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
 // rank_ptr[R+1], rank_exp[E]: experts of rank r are rank_exp[rank_ptr[r] ..
-// rank_ptr[r+1]) in ascending id order.  bad_home = 1 if some home is outside
-// [0, R).  Also clears the per-problem counts of skipped ids, bad_prob[B].
+// rank_ptr[r+1]) in no particular order.  bad_home = 1 if some home is
+// outside [0, R).  Also clears the per-problem counts of skipped ids,
+// bad_prob[B].
 __global__ void __launch_bounds__(kCsrThreads)
 home_csr_kernel(const int32_t* __restrict__ home, int32_t B, int32_t R, int32_t E, int32_t* __restrict__ rank_ptr,
                 int32_t* __restrict__ rank_exp, int32_t* __restrict__ bad_home,
                 unsigned long long* __restrict__ bad_prob) {
-  __shared__ int32_t cnt[TAOT_MAX_RANKS + 1];
+  __shared__ int32_t cnt[TAOT_MAX_RANKS];
+  __shared__ int32_t wtot[kCsrThreads / kWave];
   __shared__ int32_t bad;
-  if (threadIdx.x == 0) bad = 0;
-  for (int32_t r = threadIdx.x; r < R; r += kCsrThreads) {
-    int32_t c = 0;
-    for (int32_t e = 0; e < E; ++e) c += (home[e] == r);
-    cnt[r] = c;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+  if (tid == 0) bad = 0;
+  for (int32_t r = tid; r < R; r += kCsrThreads) cnt[r] = 0;
+  __syncthreads();
+  for (int32_t e = tid; e < E; e += kCsrThreads) {
+    const int32_t h = home[e];
+    if (h < 0 || h >= R) bad = 1;
+    else atomicAdd(&cnt[h], 1);
   }
   __syncthreads();
-  for (int32_t e = threadIdx.x; e < E; e += kCsrThreads) {
-    int32_t h = home[e];
-    if (h < 0 || h >= R) atomicOr(&bad, 1);
+  // exclusive scan: thread t takes ranks [t*seg, t*seg + seg)
+  constexpr int kSeg = (TAOT_MAX_RANKS + kCsrThreads - 1) / kCsrThreads;
+  const int32_t lo = tid * kSeg;
+  int32_t mine = 0;
+#pragma unroll
+  for (int k = 0; k < kSeg; ++k) mine += lo + k < R ? cnt[lo + k] : 0;
+  int32_t incl = mine;  // inclusive scan over the wave
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int32_t y = __shfl_up(incl, o, kWave);
+    incl += lane >= o ? y : 0;
   }
-  if (threadIdx.x == 0) {
-    int32_t s = 0;
-    for (int32_t r = 0; r < R; ++r) {
-      int32_t c = cnt[r];
-      rank_ptr[r] = s;
-      cnt[r] = s;
-      s += c;
+  if (lane == kWave - 1) wtot[wid] = incl;
+  __syncthreads();
+  int32_t off = incl - mine;
+  for (int w = 0; w < wid; ++w) off += wtot[w];
+#pragma unroll
+  for (int k = 0; k < kSeg; ++k) {
+    if (lo + k < R) {
+      const int32_t c = cnt[lo + k];
+      rank_ptr[lo + k] = off;
+      cnt[lo + k] = off;  // now the placement cursor
+      off += c;
     }
-    rank_ptr[R] = s;
   }
+  if (lo < R && lo + kSeg >= R) rank_ptr[R] = off;  // the thread holding the last rank
   __syncthreads();
-  for (int32_t r = threadIdx.x; r < R; r += kCsrThreads) {
-    int32_t pos = cnt[r];
-    for (int32_t e = 0; e < E; ++e)
-      if (home[e] == r) rank_exp[pos++] = e;
+  for (int32_t e = tid; e < E; e += kCsrThreads) {
+    const int32_t h = home[e];
+    if (h >= 0 && h < R) rank_exp[atomicAdd(&cnt[h], 1)] = e;
   }
-  if (threadIdx.x == 0) bad_home[0] = bad;
-  for (int32_t b = threadIdx.x; b < B; b += kCsrThreads) bad_prob[b] = 0;
+  if (tid == 0) bad_home[0] = bad;
+  for (int32_t b = tid; b < B; b += kCsrThreads) bad_prob[b] = 0;
 }
 
 // One block per (problem, source rank) row of N ids.  LDS holds `copies`
-// private histograms of E+1 words; lane group (tid & (copies-1)) owns one
-// copy, which spreads the heavy Zipf bins over distinct LDS addresses.  Word E
-// of a copy is where ids outside [0, E) are counted, so the count carries no
-// branch and the extra word also rotates banks between copies.
+// private histograms; lane group (tid & (copies-1)) owns one copy, which
+// spreads the heavy Zipf bins over distinct LDS addresses.  Bin E of a copy
+// is where ids outside [0, E) are counted, so the count carries no branch.
+// With PACK16 two experts share a 32-bit word (expert e in half e & 1 of
+// word e >> 1); the host takes this form only when no copy can count past
+// 65535 in one half (a row short enough for the number of copies), and it
+// doubles the copies that fit the LDS.  Otherwise a copy is E+1 words; the
+// extra word also rotates banks between copies.
 //
 // Ids are read exactly once, so they stream past the caches.  The bulk of a
 // row goes in batches of kHistUnroll 16-byte loads per thread, none of them
 // predicated, with the next batch in flight while the current one is counted
 // (two register sets, a and b, take turns).  The first batch is issued before
 // the counters are cleared.
+template <bool PACK16>
 __global__ void __launch_bounds__(kHistThreads)
 histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t E, int32_t copies,
                  int32_t* __restrict__ n, unsigned long long* __restrict__ bad_prob) {
   extern __shared__ int32_t bins[];
   const int64_t row = blockIdx.x;
-  const int32_t stride = E + 1;
+  const int32_t stride = PACK16 ? (E >> 1) + 1 : E + 1;
   const int32_t words = copies * stride;
   int32_t* my = bins + (int32_t)(threadIdx.x & (copies - 1)) * stride;
   const int32_t* src = ids + row * N;
   const uint32_t uE = (uint32_t)E;
-  auto count = [&](int32_t q) { atomicAdd(&my[(uint32_t)q < uE ? q : E], 1); };
+  auto count = [&](int32_t q) {
+    const int32_t e = (uint32_t)q < uE ? q : E;
+    if constexpr (PACK16) atomicAdd(&my[e >> 1], (e & 1) ? 0x10000 : 1);
+    else atomicAdd(&my[e], 1);
+  };
   auto count4 = [&](const v4i& v) {
     count(v.x);
     count(v.y);
@@ -150,7 +185,12 @@ histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t 
   int32_t* dst = n + row * E;
   for (int32_t e = threadIdx.x; e <= E; e += kHistThreads) {
     int32_t s = 0;
-    for (int32_t c = 0; c < copies; ++c) s += bins[c * stride + e];
+    if constexpr (PACK16) {
+      const int sh = (e & 1) * 16;
+      for (int32_t c = 0; c < copies; ++c) s += (int32_t)(((uint32_t)bins[c * stride + (e >> 1)] >> sh) & 0xFFFFu);
+    } else {
+      for (int32_t c = 0; c < copies; ++c) s += bins[c * stride + e];
+    }
     if (e < E)
       __builtin_nontemporal_store(s, &dst[e]);
     else if (s != 0)
@@ -158,15 +198,62 @@ histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t 
   }
 }
 
-// One block per problem.
+// x_e = sum_r n_re for a block of kColExperts experts of one problem: lane l
+// of every wave sums experts 4l .. 4l+3 of the block (one 16-byte load per
+// row when rows are 16-byte aligned, else four 4-byte loads), wave w rows
+// w, w + 4, ...; the waves' partial sums meet in LDS.  Integer sums: exact in
+// any order.
+__global__ void __launch_bounds__(kColThreads)
+expert_load_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, int64_t* __restrict__ load_e) {
+  constexpr int kWaves = kColThreads / kWave;
+  constexpr int kRowsInFlight = 8;
+  __shared__ long long part[kWaves][kColExperts];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+  const int32_t chunks = (E + kColExperts - 1) / kColExperts;
+  const int64_t b = blockIdx.x / chunks;
+  const int32_t e0 = (int32_t)(blockIdx.x % chunks) * kColExperts + 4 * lane;
+  const int32_t* nb = n + b * (int64_t)R * E;
+  const bool vec = (E % 4 == 0) && ((reinterpret_cast<uintptr_t>(n) & 15u) == 0);
+  int64_t s[4] = {0, 0, 0, 0};
+  if (e0 < E) {
+    auto add_row = [&](int32_t r) {
+      const int32_t* q = nb + (int64_t)r * E + e0;
+      if (vec) {
+        const v4i v = *reinterpret_cast<const v4i*>(q);
+        s[0] += v.x; s[1] += v.y; s[2] += v.z; s[3] += v.w;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) s[k] += e0 + k < E ? q[k] : 0;
+      }
+    };
+    int32_t r = wid;
+    for (; r + (kRowsInFlight - 1) * kWaves < R; r += kRowsInFlight * kWaves) {
+#pragma unroll
+      for (int u = 0; u < kRowsInFlight; ++u) add_row(r + u * kWaves);
+    }
+    for (; r < R; r += kWaves) add_row(r);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) part[wid][4 * lane + k] = s[k];
+  __syncthreads();
+  const int32_t e = (int32_t)(blockIdx.x % chunks) * kColExperts + tid;
+  if (tid < kColExperts && e < E) {
+    int64_t t = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) t += part[w][tid];
+    load_e[b * E + e] = t;
+  }
+}
+
+// One block per problem; x_e comes from expert_load_kernel.
 __global__ void __launch_bounds__(kMargThreads)
-marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int32_t* __restrict__ home,
-                 const int32_t* __restrict__ rank_ptr, const int32_t* __restrict__ rank_exp,
-                 const int32_t* __restrict__ bad_home, const unsigned long long* __restrict__ bad_prob,
-                 int64_t* __restrict__ load_e, int64_t* __restrict__ load_r, int64_t* __restrict__ excess,
-                 int64_t* __restrict__ spare, int64_t* __restrict__ spill, float* __restrict__ supply,
-                 float* __restrict__ demand, double* __restrict__ rho, double* __restrict__ alpha,
-                 int64_t* __restrict__ bad_ids, uint32_t* __restrict__ status) {
+marginals_kernel(int32_t R, int32_t E, const int32_t* __restrict__ home, const int32_t* __restrict__ rank_ptr,
+                 const int32_t* __restrict__ rank_exp, const int32_t* __restrict__ bad_home,
+                 const unsigned long long* __restrict__ bad_prob, int64_t* __restrict__ load_e,
+                 int64_t* __restrict__ load_r, int64_t* __restrict__ excess, int64_t* __restrict__ spare,
+                 int64_t* __restrict__ spill, float* __restrict__ supply, float* __restrict__ demand,
+                 double* __restrict__ rho, double* __restrict__ alpha, int64_t* __restrict__ bad_ids,
+                 uint32_t* __restrict__ status) {
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x;
   __shared__ int64_t red_s[kMargThreads / kWave], red_m[kMargThreads / kWave];
@@ -190,23 +277,6 @@ marginals_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, const int3
     }
     return;
   }
-
-  // expert loads x_e = sum_r n_re (coalesced over e, 8 rows in flight)
-  const int32_t* nb_ = n + b * (int64_t)R * E;
-  for (int32_t e = tid; e < E; e += kMargThreads) {
-    int64_t s = 0;
-    int32_t r = 0;
-    for (; r + 8 <= R; r += 8) {
-      int32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = nb_[(int64_t)(r + u) * E + e];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
-    }
-    for (; r < R; ++r) s += nb_[(int64_t)r * E + e];
-    xe[e] = s;
-  }
-  __syncthreads();
 
   // rank loads, total and maximum
   int64_t ls = 0, lm = 0;
@@ -322,19 +392,36 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
   hipLaunchKernelGGL(home_csr_kernel, dim3(1), dim3(kCsrThreads), 0, stream, home, B, R, E, w.rank_ptr,
                      w.rank_exp, w.bad_home, w.bad_prob);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  // counter layout: 32-bit copies of E+1 words while 16 fit the LDS cap;
+  // else 16-bit pairs, twice as many copies in half the words, when no copy
+  // can count past 65535 (a copy's lane group reads at most N / copies ids
+  // plus one 16-byte batch tail per thread)
   int32_t copies = 16;
   while (copies > 1 && (int64_t)copies * (E + 1) > kHistLdsWords) copies >>= 1;
-  const size_t lds = (size_t)copies * (E + 1) * sizeof(int32_t);
-  if (lds > 65536 && hipFuncSetAttribute((const void*)histogram_kernel,
-                                          hipFuncAttributeMaxDynamicSharedMemorySize,
-                                          (int)lds) != hipSuccess)
+  int32_t copies16 = 16;
+  const int64_t stride16 = (E >> 1) + 1;
+  while (copies16 > 1 && (int64_t)copies16 * stride16 > kHistLdsWords16) copies16 >>= 1;
+  const bool pack16 = copies < kHist16MinCopies && copies16 > copies &&
+                      N / copies16 + 4 * kHistUnroll * (kHistThreads / copies16) * 4 <= 65535;
+  if (pack16) copies = copies16;
+  const size_t lds = (size_t)copies * (pack16 ? stride16 : (E + 1)) * sizeof(int32_t);
+  const void* hist = pack16 ? (const void*)histogram_kernel<true> : (const void*)histogram_kernel<false>;
+  if (lds > 65536 &&
+      hipFuncSetAttribute(hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(histogram_kernel, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
-                     ids, N, R, E, copies, n, w.bad_prob);
+  if (pack16)
+    hipLaunchKernelGGL(histogram_kernel<true>, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
+                       ids, N, R, E, copies, n, w.bad_prob);
+  else
+    hipLaunchKernelGGL(histogram_kernel<false>, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
+                       ids, N, R, E, copies, n, w.bad_prob);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(marginals_kernel, dim3((unsigned)B), dim3(kMargThreads), 0, stream, n, R, E, home,
-                     w.rank_ptr, w.rank_exp, w.bad_home, w.bad_prob, load_e, load_r, excess, spare,
-                     spill, supply, demand, rho, alpha, bad_ids, status);
+  hipLaunchKernelGGL(expert_load_kernel, dim3((unsigned)((int64_t)B * ((E + kColExperts - 1) / kColExperts))),
+                     dim3(kColThreads), 0, stream, n, R, E, load_e);
+  if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
+  hipLaunchKernelGGL(marginals_kernel, dim3((unsigned)B), dim3(kMargThreads), 0, stream, R, E, home, w.rank_ptr,
+                     w.rank_exp, w.bad_home, w.bad_prob, load_e, load_r, excess, spare, spill, supply, demand,
+                     rho, alpha, bad_ids, status);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   return TAOT_OK;
 }
