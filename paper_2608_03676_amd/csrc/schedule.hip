@@ -587,43 +587,85 @@ static_assert(LdsSmall::kT == LdsSmall::kTW * kWave && LdsTiny::kT == LdsTiny::k
 // list entries pack (slot, slot-expert index, host structure): 12 + 7 + 7 bits
 constexpr int kItemSlotBits = 12, kItemExpertBits = 7;
 
+// Exclusive position of `flag` among the NT threads (ascending thread id) and
+// the chunk total.  All threads must call it.
+template <int NT>
+__device__ __forceinline__ int32_t compact_pos_n(bool flag, int32_t* wave_cnt, int32_t& total) {
+  constexpr int NW = NT / kWave;
+  const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+  const uint64_t m = __ballot(flag);
+  const int32_t lp = __popcll(m & ((1ull << lane) - 1ull));
+  if (lane == 0) wave_cnt[wid] = __popcll(m);
+  __syncthreads();
+  int32_t off = 0, tot = 0;
+  for (int w = 0; w < NW; ++w) {
+    const int32_t c = wave_cnt[w];
+    off += w < wid ? c : 0;
+    tot += c;
+  }
+  __syncthreads();
+  total = tot;
+  return off + lp;
+}
+
 // Tier structure of column h of Bauct: its distinct bonuses in descending
 // order and the rank set of each ([h][kTierMax][TW] words); ntier[h] = -1 if
 // there are more than kTierMax.  NaN and -inf bonuses never win a bid and
-// belong to no tier.
+// belong to no tier; -0 and +0 are one value.  The distinct values come out
+// one per step as a block maximum over the values below the previous one
+// (order-preserving 64-bit keys).
+__device__ __forceinline__ double key_double(uint64_t k) {
+  return __longlong_as_double((long long)((k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k));
+}
+
+template <int NT>
+__device__ __forceinline__ uint64_t block_max_u64(uint64_t v, uint64_t* buf) {
+  constexpr int NW = NT / kWave;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = __shfl_xor(v, o, kWave);
+    v = y > v ? y : v;
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0) buf[threadIdx.x / kWave] = v;
+  __syncthreads();
+  uint64_t m = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) m = buf[w] > m ? buf[w] : m;
+  __syncthreads();
+  return m;
+}
+
 template <int TW>
 __global__ void __launch_bounds__(256)
 auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __restrict__ ntier,
                      double* __restrict__ tv, uint64_t* __restrict__ tmask) {
   __shared__ double col[TW * kWave];
   __shared__ double vals[kTierMax];
-  __shared__ int32_t nv;
+  __shared__ uint64_t red[256 / kWave];
   __shared__ unsigned long long msk[kTierMax * TW];
   const int32_t h = blockIdx.x, tid = threadIdx.x;
   for (int32_t q = tid; q < kTierMax * TW; q += blockDim.x) msk[q] = 0ull;
   for (int32_t r = tid; r < R; r += blockDim.x) col[r] = Bauct[(int64_t)r * R + h];
   __syncthreads();
-  if (tid == 0) {
-    int32_t n = 0;
-    for (int32_t r = 0; r < R && n >= 0; ++r) {
+  // the tier bonuses, descending: key 0 is below every value's key
+  uint64_t prev = ~0ull;
+  int32_t n = 0;
+  for (int t = 0; t <= kTierMax; ++t) {
+    uint64_t m = 0;
+    for (int32_t r = tid; r < R; r += blockDim.x) {
       const double v = col[r];
       if (v != v || v == -INFINITY) continue;
-      int32_t pos = 0;
-      bool dup = false;
-      for (int32_t i = 0; i < n; ++i) {
-        dup |= vals[i] == v;
-        pos += vals[i] > v;
-      }
-      if (dup) continue;
-      if (n == kTierMax) { n = -1; break; }
-      for (int32_t i = n; i > pos; --i) vals[i] = vals[i - 1];
-      vals[pos] = v;
-      ++n;
+      const uint64_t k = auction_key(v);
+      if (k < prev && k > m) m = k;
     }
-    nv = n;
+    m = block_max_u64<256>(m, red);
+    if (m == 0) break;  // no value below the previous one
+    if (t == kTierMax) { n = -1; break; }
+    if (tid == 0) vals[t] = key_double(m);
+    prev = m;
+    n = t + 1;
   }
   __syncthreads();
-  const int32_t n = nv;
   for (int32_t r = tid; r < R && n > 0; r += blockDim.x) {
     const double v = col[r];
     for (int32_t i = 0; i < n; ++i)
@@ -638,14 +680,16 @@ auction_tiers_kernel(const double* __restrict__ Bauct, int32_t R, int32_t* __res
 
 // Deduplicates the host tier structures into a table of at most SC entries
 // (one block, one thread per host; equal structures are found through a hash
-// of each and then compared in full) and ranks the table's distinct bonuses
-// (ascending): sidx[h] is host h's entry, cw the words that hold ranks of
-// each tier, cvr the bonus rank of each tier, hdr[0] the table size and
-// hdr[1] = 1 when the LDS-resident auction is exact for this Bauct and price
-// step: every column has at most kTierMax values, none is +inf, the table
-// fits, and both the step (if not 0) and every gap between distinct bonuses
-// exceed twice the spacing of doubles at max|bonus| + S * step (prices stay
-// below S * step: a rank serves each slot at most once).
+// of each and then compared in full; the table keeps first occurrences in
+// host order) and ranks the table's distinct bonuses (ascending, one per step
+// as a block minimum above the previous one): sidx[h] is host h's entry, cw
+// the words that hold ranks of each tier, cvr the bonus rank of each tier,
+// hdr[0] the table size and hdr[1] = 1 when the LDS-resident auction is exact
+// for this Bauct and price step: every column has at most kTierMax values,
+// none is +inf, the table fits, and both the step (if not 0) and every gap
+// between distinct bonuses exceed twice the spacing of doubles at max|bonus|
+// + S * step (prices stay below S * step: a rank serves each slot at most
+// once).
 template <class CF>
 __global__ void __launch_bounds__(CF::kT)
 auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restrict__ tv_g,
@@ -653,15 +697,19 @@ auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restr
                       int32_t* __restrict__ sidx, int32_t* __restrict__ cn, double* __restrict__ cv,
                       int32_t* __restrict__ cvr, uint32_t* __restrict__ cw, uint64_t* __restrict__ cm,
                       int32_t* __restrict__ hdr) {
+  constexpr int NT = CF::kT;
   constexpr int kRow = kTierMax * CF::kTW;
   constexpr int kMaxR = CF::kTW * kWave;
+  constexpr int kMaxDv = CF::kSC * kTierMax;
+  static_assert(NT >= kMaxR, "one thread per host");
   __shared__ int32_t ntier[kMaxR], first[kMaxR], sid[kMaxR], tab[CF::kSC];
   __shared__ uint64_t hsh[kMaxR];
   __shared__ double tv[kMaxR * kTierMax];
-  __shared__ double dv[CF::kSC * kTierMax];
-  __shared__ int32_t sh_ns, sh_ok;
+  __shared__ double dv[kMaxDv];
+  __shared__ uint64_t red[NT / kWave];
+  __shared__ int32_t wave_cnt[NT / kWave];
   const int32_t h = threadIdx.x;
-  for (int32_t q = h; q < R * kTierMax; q += blockDim.x) tv[q] = tv_g[q];
+  for (int32_t q = h; q < R * kTierMax; q += NT) tv[q] = tv_g[q];
   if (h < R) {
     const int32_t nh = ntier_g[h];
     ntier[h] = nh;
@@ -690,76 +738,86 @@ auction_struct_kernel(const int32_t* __restrict__ ntier_g, const double* __restr
     first[h] = f;
   }
   __syncthreads();
-  if (h == 0) {
-    int32_t ns = 0, nd = 0;
-    double vm = 0.0;
-    bool ok = true;
-    for (int32_t g = 0; g < R; ++g) {
-      ok &= ntier[g] >= 0;
-      if (first[g] != g) {
-        sid[g] = sid[first[g]];
-        continue;
-      }
-      const int32_t nt = ntier[g] > 0 ? ntier[g] : 0;
-      for (int32_t t = 0; t < nt; ++t) {
-        const double v = tv[g * kTierMax + t];
-        ok &= v != INFINITY;
-        vm = fmax(vm, fabs(v));
-      }
-      if (ns < CF::kSC) {
-        tab[ns] = g;
-        // distinct bonuses of the table, ascending
-        for (int32_t t = 0; t < nt; ++t) {
-          const double v = tv[g * kTierMax + t];
-          int32_t pos = 0;
-          bool dup = false;
-          for (int32_t i = 0; i < nd; ++i) {
-            dup |= dv[i] == v;
-            pos += dv[i] < v;
-          }
-          if (dup) continue;
-          for (int32_t i = nd; i > pos; --i) dv[i] = dv[i - 1];
-          dv[pos] = v;
-          ++nd;
-        }
-      }
-      sid[g] = ns;
-      ++ns;
+  // table entries: the first occurrences in host order
+  int32_t ns;
+  {
+    const bool f = h < R && first[h] == h;
+    const int32_t pos = compact_pos_n<NT>(f, wave_cnt, ns);
+    if (f) {
+      sid[h] = pos;
+      if (pos < CF::kSC) tab[pos] = h;
     }
-    ok &= ns <= CF::kSC;
+  }
+  __syncthreads();
+  if (h < R && first[h] != h) sid[h] = sid[first[h]];
+  // exactness conditions over all hosts: at most kTierMax values per column,
+  // no +inf, and max |bonus|
+  bool okh = true;
+  uint64_t vmk = 0;  // bits of max |bonus| (non-negative doubles order as integers)
+  if (h < R) {
+    okh = ntier[h] >= 0;
+    for (int32_t t = 0; t < ntier[h]; ++t) {
+      const double v = tv[h * kTierMax + t];
+      okh &= v != INFINITY;
+      const uint64_t a = (uint64_t)__double_as_longlong(fabs(v));
+      vmk = a > vmk ? a : vmk;
+    }
+  }
+  const bool all_ok = block_max_u64<NT>(okh ? 0ull : 1ull, red) == 0ull;
+  const double vm = __longlong_as_double((long long)block_max_u64<NT>(vmk, red));
+  // distinct bonuses of the table, ascending: value q is tier q % kTierMax of
+  // entry q / kTierMax, dealt out over the threads
+  const int32_t nt_tab = ns < CF::kSC ? ns : CF::kSC;
+  int32_t nd = 0;
+  {
+    uint64_t prev = 0;  // keys above this; the smallest first
+    for (;;) {
+      // minimum key above prev, as a maximum of complements
+      uint64_t c = 0;
+      for (int32_t q = h; q < nt_tab * kTierMax; q += NT) {
+        const int32_t g = tab[q / kTierMax], t = q % kTierMax;
+        if (t >= ntier[g]) continue;
+        const uint64_t k = auction_key(tv[g * kTierMax + t]);
+        if (k > prev && ~k > c) c = ~k;
+      }
+      const uint64_t m = block_max_u64<NT>(c, red);
+      if (m == 0) break;
+      const uint64_t kmin = ~m;
+      if (h == 0 && nd < kMaxDv) dv[nd] = key_double(kmin);
+      prev = kmin;
+      ++nd;
+    }
+  }
+  __syncthreads();
+  if (h == 0) {
+    bool ok = all_ok && ns <= CF::kSC;
     const double top = vm + (double)S * step * 1.01 + 1.0;
     const double spacing2 = 2.0 * (nextafter(top, INFINITY) - top);
     ok &= step == 0.0 || (step > 0.0 && step > spacing2);
     for (int32_t i = 0; i + 1 < nd; ++i) ok &= dv[i + 1] - dv[i] > spacing2;
-    sh_ns = ns < CF::kSC ? ns : CF::kSC;
-    sh_ok = ok ? 1 : 0;
-    // bonus ranks of the table's tiers
-    for (int32_t i = 0; i < sh_ns; ++i) {
-      const int32_t g = tab[i];
-      for (int32_t t = 0; t < kTierMax; ++t) {
-        int32_t rank = 0;
-        if (t < ntier[g])
-          while (dv[rank] != tv[g * kTierMax + t]) ++rank;
-        cvr[i * kTierMax + t] = rank;
-      }
-    }
+    hdr[0] = nt_tab;
+    hdr[1] = ok ? 1 : 0;
   }
-  __syncthreads();
-  const int32_t ns = sh_ns;
-  for (int32_t q = h; q < R; q += blockDim.x) sidx[q] = sid[q];
-  for (int32_t q = h; q < ns; q += blockDim.x) cn[q] = ntier[tab[q]] > 0 ? ntier[tab[q]] : 0;
-  for (int32_t q = h; q < ns * kTierMax; q += blockDim.x) {
+  // bonus ranks of the table's tiers
+  for (int32_t q = h; q < nt_tab * kTierMax; q += NT) {
+    const int32_t g = tab[q / kTierMax], t = q % kTierMax;
+    int32_t rank = 0;
+    if (t < ntier[g]) {
+      const double v = tv[g * kTierMax + t];
+      while (dv[rank] != v) ++rank;
+    }
+    cvr[q] = rank;
+  }
+  for (int32_t q = h; q < R; q += NT) sidx[q] = sid[q];
+  for (int32_t q = h; q < nt_tab; q += NT) cn[q] = ntier[tab[q]] > 0 ? ntier[tab[q]] : 0;
+  for (int32_t q = h; q < nt_tab * kTierMax; q += NT) {
     const int32_t g = tab[q / kTierMax], t = q % kTierMax;
     cv[q] = tv[g * kTierMax + t];
     uint32_t words = 0;
     for (int32_t w = 0; w < CF::kTW; ++w) words |= (tmask[(int64_t)g * kRow + t * CF::kTW + w] != 0ull ? 1u : 0u) << w;
     cw[q] = words;
   }
-  for (int32_t q = h; q < ns * kRow; q += blockDim.x) cm[q] = tmask[(int64_t)tab[q / kRow] * kRow + q % kRow];
-  if (h == 0) {
-    hdr[0] = ns;
-    hdr[1] = sh_ok;
-  }
+  for (int32_t q = h; q < nt_tab * kRow; q += NT) cm[q] = tmask[(int64_t)tab[q / kRow] * kRow + q % kRow];
 }
 
 template <class CF>
@@ -837,27 +895,6 @@ struct LdsParams {
   int32_t* nprime;       // [B][DC][R]
   int32_t NEC;           // candidate-expert capacity of the LDS layout
 };
-
-// Exclusive position of `flag` among the NT threads (ascending thread id) and
-// the chunk total.  All threads must call it.
-template <int NT>
-__device__ __forceinline__ int32_t compact_pos_n(bool flag, int32_t* wave_cnt, int32_t& total) {
-  constexpr int NW = NT / kWave;
-  const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-  const uint64_t m = __ballot(flag);
-  const int32_t lp = __popcll(m & ((1ull << lane) - 1ull));
-  if (lane == 0) wave_cnt[wid] = __popcll(m);
-  __syncthreads();
-  int32_t off = 0, tot = 0;
-  for (int w = 0; w < NW; ++w) {
-    const int32_t c = wave_cnt[w];
-    off += w < wid ? c : 0;
-    tot += c;
-  }
-  __syncthreads();
-  total = tot;
-  return off + lp;
-}
 
 // Block-wide OR with one barrier; flags alternate between two halves of buf
 // ([2][NT / 64]) so that a call never overwrites flags still being read.
