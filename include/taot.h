@@ -67,6 +67,14 @@ typedef enum {
                                      where its rows fit one wave's registers (by
                                      default small batches spread a problem over
                                      up to four waves)                              */
+#define TAOT_SK_DENSE 0x10u       /* dense streamed iterate (Sec. A.2, GEMV form): the
+                                     log-domain updates over all R x R entries of
+                                     every problem, with no support compaction; each
+                                     iteration streams the cost matrix from device
+                                     memory through every compute unit.  Same
+                                     outputs as the default paths (to rounding);
+                                     status TAOT_ST_STREAMED.  The other TAOT_SK_*
+                                     flags except NO_COLCAP are ignored           */
 
 /* round_schedule flags: ablations of the Phase-2 score (Sec. A.3 discusses
  * the contribution of each term).  Phase 3 is unaffected. */

@@ -16,7 +16,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = ["csrc/api.hip", "csrc/loads.hip", "csrc/sinkhorn.hip", "csrc/sk_reg_w4g4.hip", "csrc/sk_reg_w2g8.hip",
-           "csrc/sk_reg_w2g2.hip", "csrc/schedule.hip"]
+           "csrc/sk_reg_w2g2.hip", "csrc/sk_dense.hip", "csrc/schedule.hip"]
 LIB = os.path.join(HERE, "libtaot.so")
 PROBES_LIB = os.path.join(HERE, "libtaot_probes.so")
 OBJ_DIR = os.path.join(HERE, "_build")

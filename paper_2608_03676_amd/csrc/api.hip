@@ -87,7 +87,8 @@ taot_status taot_sinkhorn_batched(const float* a, const float* b, int32_t B, int
                                   uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
   if (bad_dims(B, R) || !(eps > 0.f) || !isfinite(eps) || iters < 1 ||
       (C_batch_stride != 0 && C_batch_stride != (int64_t)R * R) ||
-      (flags & ~(TAOT_SK_NO_COLCAP | TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER | TAOT_SK_WAVES_1)))
+      (flags & ~(TAOT_SK_NO_COLCAP | TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER | TAOT_SK_WAVES_1 |
+                 TAOT_SK_DENSE)))
     return TAOT_ERR_INVALID_ARG;
   if (R > TAOT_MAX_RANKS) return TAOT_ERR_UNSUPPORTED;
   if (B == 0) return TAOT_OK;

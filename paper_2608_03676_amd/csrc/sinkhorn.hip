@@ -57,7 +57,7 @@ cost_scan_kernel(const float* __restrict__ C, int64_t R2, int32_t chunks, int32_
   const float* c = C + mat * R2;
   const int64_t lo = ch * kScanChunk, hi = lo + kScanChunk < R2 ? lo + kScanChunk : R2;
   int bad = 0;
-  auto nonfinite = [](float x) { return !(x - x == 0.f); };  // NaN or +-inf
+  auto nonfinite = [](float x) { return (int)!(x - x == 0.f); };  // NaN or +-inf
   if (hi - lo == kScanChunk && (reinterpret_cast<uintptr_t>(c + lo) & 15u) == 0) {
     const float4* c4 = reinterpret_cast<const float4*>(c + lo) + threadIdx.x;
     float4 x[kScanLoads];
@@ -807,6 +807,8 @@ struct SkWs {
   int32_t* cbad;    // [B or 1][scan_chunks(R)] chunk marks of the cost scan
   float* kt;
   int64_t kt_stride;
+  float* dn;        // [B][dn_stride] state of the dense streamed iterate
+  int64_t dn_stride;
   size_t bytes;
 };
 
@@ -820,6 +822,8 @@ SkWs carve(void* ws, int32_t B, int32_t R) {
   w.cbad = c.take<int32_t>((size_t)B * scan_chunks(R));
   w.kt_stride = round_up((int64_t)R * R, 64);
   w.kt = c.take<float>((size_t)B * w.kt_stride);
+  w.dn_stride = round_up((int64_t)dense_state_floats(R), 64);
+  w.dn = c.take<float>((size_t)B * w.dn_stride);
   w.bytes = c.off;
   return w;
 }
@@ -834,13 +838,14 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
   if (B == 0) return TAOT_OK;
   SkWs w = carve(ws, B, R);
   SkParams p{a, b, B, R, C, C_stride, eps, iters, flags, T, f, g, status, w.flag, w.kt, w.kt_stride, 0, 0,
-             w.cbad, scan_chunks(R)};
+             w.cbad, scan_chunks(R), w.dn, w.dn_stride};
   {
     const int64_t mats = C_stride ? B : 1;
     hipLaunchKernelGGL(cost_scan_kernel, dim3((unsigned)(mats * p.cchunks)), dim3(kScanThreads), 0, stream, C,
                        (int64_t)R * R, p.cchunks, w.cbad);
     if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   }
+  if (flags & TAOT_SK_DENSE) return launch_dense(p, stream);
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
   if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {

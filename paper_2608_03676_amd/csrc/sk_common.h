@@ -28,6 +28,8 @@ struct SkParams {
   int32_t all_streamed;  // every problem goes to the streamed kernel
   const int32_t* cbad;   // [matrices][cchunks] 1 = the chunk of C holds a non-finite entry
   int32_t cchunks;       // chunks of kScanChunk entries per cost matrix
+  float* dn_ws;          // dense streamed iterate: per-problem state, dn_stride floats each
+  int64_t dn_stride;
 };
 
 namespace {
@@ -243,5 +245,9 @@ taot_status launch_reg_w2g8(const SkParams& p, const int32_t* multi, const int32
                             hipStream_t stream);
 taot_status launch_reg_w2g2(const SkParams& p, const int32_t* multi, const int32_t* single, const int32_t* counts,
                             hipStream_t stream);
+// The dense streamed iterate (TAOT_SK_DENSE) and its per-problem state in the
+// streamed-plan storage of the workspace.
+taot_status launch_dense(const SkParams& p, hipStream_t stream);
+size_t dense_state_floats(int32_t R);
 
 }  // namespace taot
