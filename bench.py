@@ -45,6 +45,10 @@ def parse():
                     help="only run a plain device copy of MIB MiB five times (HBM counter calibration)")
     ap.add_argument("--other-steps", type=int, default=3,
                     help="timed steps for the planner latency of workloads 1-4 other than --workload (0: skip)")
+    ap.add_argument("--dense-steps", type=int, default=3,
+                    help="timed calls of the dense streamed Sinkhorn (TAOT_SK_DENSE) at the workload-4 shape "
+                         "with one cost matrix per problem (0: skip)")
+    ap.add_argument("--dense-only", action="store_true", help="only run the dense streamed leg and print it")
     ap.add_argument("--json-out", default=None)
     ap.add_argument("--no-peaks", action="store_true", help="skip the peak probes")
     ap.add_argument("--peaks-only", action="store_true", help="only run the peak probes and print them")
@@ -73,12 +77,15 @@ def log(msg):
 # rocprofv3 summaries; used only while the sources they were taken on are
 # unchanged (SHA-256 recorded in each summary).
 TRAFFIC = {
-    "plan_loads": (os.path.join(ROOT, "profiles", "plan_loads_workload3_traffic.txt"),
+    "plan_loads": (os.path.join(ROOT, "profiles", "plan_loads_workload3_traffic.txt"), 3,
                    ["paper_2608_03676_amd/csrc/loads.hip", "paper_2608_03676_amd/csrc/common.h"]),
-    "sinkhorn": (os.path.join(ROOT, "profiles", "sinkhorn_workload3_traffic.txt"),
+    "sinkhorn": (os.path.join(ROOT, "profiles", "sinkhorn_workload3_traffic.txt"), 3,
                  ["paper_2608_03676_amd/csrc/sinkhorn.hip", "paper_2608_03676_amd/csrc/sk_common.h",
                   "paper_2608_03676_amd/csrc/sk_register.h", "paper_2608_03676_amd/csrc/sk_reg_w2g8.hip",
                   "paper_2608_03676_amd/csrc/common.h"]),
+    "dense": (os.path.join(ROOT, "profiles", "sinkhorn_dense_row_workload4_traffic.txt"), 4,
+              ["paper_2608_03676_amd/csrc/sk_dense.hip", "paper_2608_03676_amd/csrc/sk_common.h",
+               "paper_2608_03676_amd/csrc/common.h"]),
 }
 
 
@@ -94,9 +101,9 @@ def sources_digest(paths):
 def measured_traffic(stage, workload):
     """HBM bytes per call of a stage from its committed counter summary, or
     None when it is for another workload or the kernels changed since."""
-    if stage not in TRAFFIC or workload != 3:
+    if stage not in TRAFFIC or workload != TRAFFIC[stage][1]:
         return None
-    path, sources = TRAFFIC[stage]
+    path, _, sources = TRAFFIC[stage]
     if not os.path.exists(path):
         return None
     fields = {}
@@ -114,20 +121,30 @@ def measured_traffic(stage, workload):
 
 
 def gpu_clocks():
-    """The GPU's clocks and power as amd-smi reports them (best effort; None
-    when the tool is missing or fails)."""
-    import subprocess
-    for cmd in (["amd-smi", "metric", "--clock", "--power", "--json"], ["rocm-smi", "--showclocks", "--showpower", "--json"]):
-        try:
-            r = subprocess.run(cmd, capture_output=True, text=True, timeout=20)
-        except (OSError, subprocess.TimeoutExpired):
-            continue
-        if r.returncode == 0 and r.stdout.strip():
+    """The GPUs' current shader and memory clock levels and power as the
+    amdgpu driver exposes them in sysfs (best effort, read without starting
+    another program; None when nothing is readable)."""
+    import glob
+    out = {}
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        rec = {}
+        for name in ("pp_dpm_sclk", "pp_dpm_mclk"):
             try:
-                return {"tool": cmd[0], "report": json.loads(r.stdout)}
-            except ValueError:
-                return {"tool": cmd[0], "report": r.stdout.strip()[:2000]}
-    return None
+                with open(os.path.join(dev, name)) as fh:
+                    cur = [l.strip() for l in fh if l.strip().endswith("*")]
+                rec[name] = cur[0] if cur else None
+            except OSError:
+                pass
+        for pw in glob.glob(os.path.join(dev, "hwmon", "hwmon*", "power1_*")):
+            if pw.endswith(("_average", "_input")):
+                try:
+                    with open(pw) as fh:
+                        rec["power_W"] = int(fh.read().strip()) / 1e6
+                except (OSError, ValueError):
+                    pass
+        if rec:
+            out[os.path.basename(os.path.dirname(dev))] = rec
+    return out or None
 
 
 def measure_peaks(dev):
@@ -271,6 +288,64 @@ def run_workload(w, K, steps, warmup, dev):
                 loads_ms=loads_ms, sk_ms=sk_ms, sch_ms=sch_ms, step_ms=step_ms, ms_step=ms_step)
 
 
+def dense_streamed(dev, steps, warmup):
+    """The dense streamed Sinkhorn (TAOT_SK_DENSE: every R x R entry, no
+    support compaction) at the workload-4 shape with one cost matrix per
+    problem (the fat-tree costs scaled by 1 + 0.01 (b mod 7)), the workload's
+    eps and iteration count, marginals from its routing.  HIP events on the
+    launch stream around each call.  The row pass reads the stored K~ once
+    per iteration (B R^2 fp32) and forms both half-steps' sums from it; the
+    floors are that single sweep at 8 TB/s and, for context, the two sweeps
+    over C per iteration of the GEMV form (one per half-step)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_03676_amd as taot
+    import workloads as W
+    w = W.WORKLOADS[4]
+    B, R = w.B, w.R
+    ids = W.workload_ids_device(w, dev)
+    home = torch.from_numpy(W.home_map(w)).to(dev)
+    L = taot.plan_loads(ids, home, w.E)
+    del ids
+    torch.cuda.empty_cache()
+    C0 = torch.from_numpy(W.cost_matrix(w)).to(dev)
+    C = torch.stack([C0 * (1.0 + 0.01 * (b % 7)) for b in range(B)]).contiguous()
+    wsk = torch.empty(taot.workspace_bytes(B, R, w.E, w.K)["sinkhorn"], dtype=torch.uint8, device=dev)
+    out = taot.sinkhorn_batched(L.supply, L.demand, C, w.eps, w.iters, taot.SK_DENSE, workspace=wsk)
+    for _ in range(warmup):
+        taot.sinkhorn_batched(L.supply, L.demand, C, w.eps, w.iters, taot.SK_DENSE, out=out, workspace=wsk)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ms = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        taot.sinkhorn_batched(L.supply, L.demand, C, w.eps, w.iters, taot.SK_DENSE, out=out, workspace=wsk)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    st = out.status.cpu().numpy().view(np.uint32)
+    finite = bool(torch.isfinite(out.T).all().item())
+    med = statistics.median(ms)
+    per_iter = 4 * B * R * R
+    floor = per_iter * w.iters / (HBM_PEAK_GBS * 1e9) * 1e3
+    achieved = per_iter * w.iters / (med * 1e-3) / 1e9
+    traffic = measured_traffic("dense", 4)
+    log(f"[bench] dense streamed, workload-4 shape, per-problem C: {med:.2f} ms for {w.iters} iterations "
+        f"({med / w.iters * 1e3:.1f} us/iteration, {achieved:.0f} GB/s of K~)")
+    return {"workload": f"workload 4 shape ({B} problems x {R} ranks), one cost matrix per problem "
+                        f"(fat-tree costs x (1 + 0.01 (b mod 7))), TAOT_SK_DENSE",
+            "iters": w.iters, "eps": w.eps, "ms": statistics.mean(ms), "ms_median": med, "ms_min": min(ms),
+            "us_per_iteration": med / w.iters * 1e3, "bound": "hbm", "bytes_per_iteration": per_iter,
+            "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "floor_ms": floor, "frac_of_floor": floor / med,
+            "two_sweep_floor_ms": 2 * floor, "frac_of_two_sweep_floor": 2 * floor / med,
+            "traffic_bytes_per_iteration_row_pass": traffic,
+            "status_streamed": int((st == taot.ST_STREAMED).sum()), "status_other": int((st != taot.ST_STREAMED).sum()),
+            "plan_finite": finite}
+
+
 def plan_quality_table(w, K, dev):
     """Plan quality of the full score, of its ablations and of row-priority
     matching (round_schedule flags) on one batch: rho before and after the planned moves, replicas
@@ -388,6 +463,9 @@ def main():
     import workloads as W
 
     dev = torch.device("cuda:0")
+    if args.dense_only:
+        print(json.dumps({"dense_streamed": dense_streamed(dev, max(args.dense_steps, 1), args.warmup)}), flush=True)
+        return
     if args.hot_rank:
         hot_rank_sweep(dev, args.steps, args.warmup)
         return
@@ -475,6 +553,10 @@ def main():
             del r2
             torch.cuda.empty_cache()
         rec["planner_latency_by_workload"] = dict(sorted(lat.items()))
+    if args.dense_steps > 0:
+        torch.cuda.empty_cache()
+        rec["dense_streamed"] = dense_streamed(dev, args.dense_steps, 1)
+        torch.cuda.empty_cache()
     rec["clocks"] = {"before": clocks_before, "after": gpu_clocks()}
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload ----------

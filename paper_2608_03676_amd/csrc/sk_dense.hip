@@ -26,6 +26,8 @@
 // K~ is read once per iteration (the column partials come from the rows held
 // in LDS).  All reductions run in a fixed order, so results do not depend on
 // scheduling.
+#include <type_traits>
+
 #include "sk_common.h"
 
 namespace taot {
@@ -35,6 +37,7 @@ constexpr int kDnThreads = 256;
 constexpr int kDnWaves = kDnThreads / kWave;
 constexpr int kDnPhases = 8;  // row phases per row block
 constexpr int kDnColBlock = 16;  // columns per block of the column kernel
+constexpr int kDnDepth = 1;      // row tiles in flight behind the current one
 
 // Column layout of the row kernel: thread t owns KPT slots s, slot s being
 // the four columns 4 (t + 256 s) .. +3 when R % 4 == 0 (16-byte rows) and
@@ -166,6 +169,21 @@ struct OpMax {
   __device__ float operator()(float a, float b) const { return fmaxf(a, b); }
 };
 
+// Calls f(integral_constant<int, k>) for k = 0 .. N-1 in order.
+template <int N>
+struct Unrolled {
+  template <typename F>
+  __device__ __forceinline__ static void run(F& f) {
+    Unrolled<N - 1>::run(f);
+    f(std::integral_constant<int, N - 1>{});
+  }
+};
+template <>
+struct Unrolled<0> {
+  template <typename F>
+  __device__ __forceinline__ static void run(F&) {}
+};
+
 // Loads rows [0, nr) of the R-wide matrix at src into the thread's columns of
 // t (zeros for rows >= nr and columns >= R).
 template <int VEC, int KPT, int TR>
@@ -249,18 +267,26 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
 #pragma unroll
   for (int c = 0; c < NC; ++c) cs[c] = 0.f;
   const float* src = BUILD ? Cb : S.K;
-  float cur[TR][NC], nxt[TR][NC];
-  load_tile<VEC, KPT, TR>(src + (int64_t)r0 * R, R, R - r0 < TR ? R - r0 : TR, cur);
+  // tiles of the next kDnDepth phases in flight behind the current one
+  float buf[kDnDepth + 1][TR][NC];
+#pragma unroll
+  for (int d = 0; d < kDnDepth; ++d)
+    if (r0 + d * TR < R)
+      load_tile<VEC, KPT, TR>(src + (int64_t)(r0 + d * TR) * R, R, R - r0 - d * TR < TR ? R - r0 - d * TR : TR,
+                              buf[d]);
   __syncthreads();  // sal
   const int wr = (lane >> (6 - LG)) & (TR - 1);       // the row whose wave total this lane holds
   const bool writer = (lane & ((kWave >> LG) - 1)) == 0;
-#pragma unroll
-  for (int ph = 0; ph < kDnPhases; ++ph) {
+  // the phases, unrolled at compile time (the tile buffers stay in registers)
+  auto phase = [&](auto phc) __attribute__((always_inline)) {
+    constexpr int ph = decltype(phc)::value;
     const int32_t i0 = r0 + ph * TR;
-    if (i0 >= R) break;  // uniform
+    if (i0 >= R) return;  // uniform
     const int32_t nr = R - i0 < TR ? R - i0 : TR;
-    if (ph + 1 < kDnPhases && i0 + TR < R)
-      load_tile<VEC, KPT, TR>(src + (int64_t)(i0 + TR) * R, R, R - i0 - TR < TR ? R - i0 - TR : TR, nxt);
+    const int32_t ia = i0 + kDnDepth * TR;  // first row of the phase to issue
+    if (ph + kDnDepth < kDnPhases && ia < R)
+      load_tile<VEC, KPT, TR>(src + (int64_t)ia * R, R, R - ia < TR ? R - ia : TR, buf[(ph + kDnDepth) % (kDnDepth + 1)]);
+    float (&cur)[TR][NC] = buf[ph % (kDnDepth + 1)];
     const int par = ph & 1;
     float uo = 0.f;  // u_i of row i0 + tid (tid < TR)
     if (BUILD) {
@@ -373,11 +399,8 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
       }
     }
     if (tid < nr) S.u[i0 + tid] = uo;
-#pragma unroll
-    for (int r = 0; r < TR; ++r)
-#pragma unroll
-      for (int c = 0; c < NC; ++c) cur[r][c] = nxt[r][c];
-  }
+  };
+  Unrolled<kDnPhases>::run(phase);
   store_row<VEC, KPT>(S.part + (int64_t)blk * R, R, cs);
 }
 
@@ -412,7 +435,10 @@ __global__ void __launch_bounds__(kDnThreads) dense_col_kernel(SkParams p, float
   if (tid < kDnColBlock && j < R) {
     const float dj = p.b[pb * R + j];
     if (!(dj > 0.f)) {
-      S.v[j] = 0.f;  // no demand: no flow into this column
+      // no demand: no flow into this column, and its entries of K~ are zero
+      // in every later rebuild (G_j = -inf), so none can overflow
+      S.v[j] = 0.f;
+      S.G[j] = -INFINITY;
     } else {
       float xs = ps[0][cl];
 #pragma unroll

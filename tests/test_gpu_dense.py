@@ -117,3 +117,19 @@ def test_dense_deterministic(gpu):
     T1 = _dense(a, b, W.cost_matrix(w), w.eps, 100)[0]
     T2 = _dense(a, b, W.cost_matrix(w), w.eps, 100)[0]
     assert T1.tobytes() == T2.tobytes()
+
+
+def test_dense_long_run_potentials_grow(gpu):
+    """Enough iterations at the R = 1024 shape for the row potentials to pass
+    2^7 in log2 units: the rebuilt entries of K~ in columns without demand
+    must stay zero (not exp2 of a large F), so the plan stays finite and equal
+    to the oracle's."""
+    w = W.WORKLOADS[4]
+    problems = [2, 26]
+    print(f"[dense parity] workload 4 problems {problems}, 150 iterations", flush=True)
+    _, L = oracle_inputs(w, problems)
+    C0 = W.cost_matrix(w)
+    C = np.stack([C0 * np.float32(1.0 + 0.01 * (p % 7)) for p in problems])
+    T, f, g, st = _dense(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, 150)
+    assert np.isfinite(T).all()
+    _check(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, 150)
