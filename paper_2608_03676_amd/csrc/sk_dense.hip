@@ -15,16 +15,16 @@
 //
 // Each iteration is two grid-wide kernels over all problems, which keeps
 // every compute unit streaming K~ from device memory:
-//   dense_row_kernel  (B * row blocks)  a block takes RB = 4 TR rows in phases
-//       of TR: the phase's K~ rows go to LDS (16-byte coalesced loads), one
-//       wave per row forms K~ v and u_i, and every thread adds the phase's
-//       rows into u-weighted sums of its columns; the block writes its column
-//       partials once.  (The first iteration builds K~ instead, from the exact
-//       first row update.)
-//   dense_col_kernel  (B * R / 256)     sums the blocks' partials of a column in
-//       block order and sets v_j.
-// K~ is read once per iteration (the column partials come from the rows held
-// in LDS).  All reductions run in a fixed order, so results do not depend on
+//   row pass (B * R / 64 blocks of 64 rows): the rows' sums (K~ v)_i, u_i,
+//       and the u-weighted column sums of the same rows, from registers, so
+//       K~ is read once per iteration; the block writes its column partials
+//       once.  dense_roww_kernel (R % 4 == 0): each wave streams 16 rows
+//       with the next rows in flight; dense_row_kernel (other R): phases of
+//       rows shared by the block's four waves.  (The first iteration builds
+//       K~ instead, from the exact first row update.)
+//   dense_col_kernel (B * R / 16 blocks): sums the blocks' partials of a
+//       column in a fixed order and sets v_j.
+// All reductions run in a fixed order, so results do not depend on
 // scheduling.
 #include <type_traits>
 
@@ -35,24 +35,21 @@ namespace {
 
 constexpr int kDnThreads = 256;
 constexpr int kDnWaves = kDnThreads / kWave;
-constexpr int kDnPhases = 8;  // row phases per row block
+constexpr int kDnRowBlock = 64;  // rows per block of the row pass
 constexpr int kDnColBlock = 16;  // columns per block of the column kernel
 constexpr int kDnDepth = 1;      // row tiles in flight behind the current one
 
-// Column layout of the row kernel: thread t owns KPT slots s, slot s being
-// the four columns 4 (t + 256 s) .. +3 when R % 4 == 0 (16-byte rows) and
-// column t + 256 s otherwise.  A phase holds TR rows of the thread's NC =
-// VEC * KPT columns in registers (TR * NC <= 32), with the next phase's rows
-// in flight behind it.
-__host__ __device__ constexpr int dense_vec(int32_t R) { return (R & 3) == 0 ? 4 : 1; }
+// Row pass, R % 4 == 0 and C 16-byte aligned: the wave-streamed kernel, 16
+// rows per wave, lane l holding the 16-byte groups l + 64 k (k < KQ) of a
+// row.  Otherwise the phased kernel: thread t owns KPT columns t + 256 s, a
+// phase holds TR rows of them in registers (TR * KPT <= 32) with the next
+// phase's rows in flight.  Either way a block takes 64 rows.
+constexpr int kDnWaveRows = kDnRowBlock / kDnWaves;
 __host__ __device__ constexpr int pow2_at_least(int32_t x) { return x <= 1 ? 1 : x <= 2 ? 2 : x <= 4 ? 4 : 8; }
-__host__ __device__ constexpr int dense_kpt(int32_t R) {
-  return dense_vec(R) == 4 ? (R / 4 + kDnThreads - 1) / kDnThreads : pow2_at_least((R + kDnThreads - 1) / kDnThreads);
-}
+__host__ __device__ constexpr int dense_kq(int32_t R) { return pow2_at_least((R / 4 + kWave - 1) / kWave); }
+__host__ __device__ constexpr int dense_kpt(int32_t R) { return pow2_at_least((R + kDnThreads - 1) / kDnThreads); }
 __host__ __device__ constexpr int dense_tr_nc(int nc) { return 32 / nc < 8 ? 32 / nc : 8; }
-__host__ __device__ constexpr int32_t dense_tr(int32_t R) { return dense_tr_nc(dense_vec(R) * dense_kpt(R)); }
-__host__ __device__ constexpr int32_t dense_rb(int32_t R) { return kDnPhases * dense_tr(R); }
-__host__ __device__ constexpr int32_t dense_blocks(int32_t R) { return (R + dense_rb(R) - 1) / dense_rb(R); }
+__host__ __device__ constexpr int32_t dense_blocks(int32_t R) { return (R + kDnRowBlock - 1) / kDnRowBlock; }
 __host__ __device__ constexpr int ilog2c(int x) { return x <= 1 ? 0 : 1 + ilog2c(x / 2); }
 
 // Per-problem state (floats): F, G, u, v, s~ [R], then the column partials
@@ -240,7 +237,7 @@ __device__ __forceinline__ int32_t col_of(int c) {
 // builds K~.  The block writes its column partials once.
 template <int VEC, int KPT, bool BUILD>
 __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu(BUILD || VEC * KPT > 4 ? 1 : 4))) dense_row_kernel(SkParams p, float kappa) {
-  constexpr int NC = VEC * KPT, TR = dense_tr_nc(NC), RB = kDnPhases * TR, LG = ilog2c(TR);
+  constexpr int NC = VEC * KPT, TR = dense_tr_nc(NC), PH = kDnRowBlock / TR, RB = kDnRowBlock, LG = ilog2c(TR);
   __shared__ float4 red[2][2][TR];         // [phase parity][max, sum][row] per-wave totals
   __shared__ float fixr[2][kDnWaves];      // per-wave max / sum of a fixed row
   __shared__ float sal[RB];
@@ -284,7 +281,7 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
     if (i0 >= R) return;  // uniform
     const int32_t nr = R - i0 < TR ? R - i0 : TR;
     const int32_t ia = i0 + kDnDepth * TR;  // first row of the phase to issue
-    if (ph + kDnDepth < kDnPhases && ia < R)
+    if (ph + kDnDepth < PH && ia < R)
       load_tile<VEC, KPT, TR>(src + (int64_t)ia * R, R, R - ia < TR ? R - ia : TR, buf[(ph + kDnDepth) % (kDnDepth + 1)]);
     float (&cur)[TR][NC] = buf[ph % (kDnDepth + 1)];
     const int par = ph & 1;
@@ -400,8 +397,171 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
     }
     if (tid < nr) S.u[i0 + tid] = uo;
   };
-  Unrolled<kDnPhases>::run(phase);
+  Unrolled<PH>::run(phase);
   store_row<VEC, KPT>(S.part + (int64_t)blk * R, R, cs);
+}
+
+// Loads one row's 16-byte groups of lane l (l + 64 k, k < KQ; zeros past R).
+template <int KQ>
+__device__ __forceinline__ void load_row4(const float* row, int32_t R, float (&x)[4 * KQ]) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int k = 0; k < KQ; ++k) {
+    const int32_t q = lane + kWave * k;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (4 * q < R) v = reinterpret_cast<const float4*>(row)[q];
+    x[4 * k] = v.x;
+    x[4 * k + 1] = v.y;
+    x[4 * k + 2] = v.z;
+    x[4 * k + 3] = v.w;
+  }
+}
+template <int KQ>
+__device__ __forceinline__ void store_row4(float* row, int32_t R, const float (&x)[4 * KQ]) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int k = 0; k < KQ; ++k) {
+    const int32_t q = lane + kWave * k;
+    if (4 * q < R) reinterpret_cast<float4*>(row)[q] = make_float4(x[4 * k], x[4 * k + 1], x[4 * k + 2], x[4 * k + 3]);
+  }
+}
+
+// Exact log-domain update of one row on this wave: c holds the row of C on
+// entry (lane's columns), K~'s new row on exit; returns F_i.
+// F_i = log2 s~_i - LSE2_j (G_j + log2 v_j - C'_ij) over the columns with
+// v_j > 0, K~_ij = exp2(F_i + G_j - C'_ij) (0 where G_j = -inf).
+template <int NC>
+__device__ __forceinline__ float row_exact4(float (&c)[NC], const float (&G)[NC], const float (&vc)[NC], float sa,
+                                            float kappa) {
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < NC; ++j)
+    if (vc[j] > 0.f) mx = fmaxf(mx, (G[j] + flog2(vc[j])) - c[j] * kappa);
+  mx = lanes_max(mx);
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < NC; ++j)
+    if (vc[j] > 0.f) sum += fexp2(((G[j] + flog2(vc[j])) - c[j] * kappa) - mx);
+  sum = lanes_sum(sum);
+  const float fi = flog2(sa) - (mx + flog2(sum));
+#pragma unroll
+  for (int j = 0; j < NC; ++j) c[j] = G[j] != -INFINITY ? fexp2((fi + G[j]) - c[j] * kappa) : 0.f;
+  return fi;
+}
+
+// Row half-step for R % 4 == 0, wave-streamed: each wave takes 16 rows of
+// its block's 64, one at a time with the next P - 1 rows in flight (P rows
+// of registers).  A row's sum (K~ v)_i is a fixed-order fold of the lane's
+// products and then a butterfly over the wave (every lane gets the same
+// bits), so every lane derives u_i = s~_i / (K~ v)_i and adds u_i K~_ij into
+// its column sums.  An out-of-range u_i takes the exact log-domain update
+// from the row of C in place.  With BUILD (the first iteration) the rows are
+// of C and every row with supply takes the exact update from G = 0, v = 1,
+// which writes K~.  The block's four waves add their column sums in LDS in
+// wave order and write the block's partials once.
+template <int KQ, bool BUILD>
+__global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu(BUILD || KQ > 4 ? 1 : 4)))
+dense_roww_kernel(SkParams p, float kappa) {
+  constexpr int NC = 4 * KQ;
+  constexpr int P = 64 / NC < 8 ? 64 / NC : 8;  // rows of the ring
+  extern __shared__ __attribute__((aligned(16))) float wpart[];  // [kDnWaves][R] the waves' column sums
+  const int32_t R = p.R, RB = kDnRowBlock, NB = dense_blocks(R);
+  const int64_t pb = blockIdx.x / NB;
+  const int32_t blk = blockIdx.x % NB;
+  if (p.stream_flag[pb] != 0) return;  // uniform per block
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+  const DenseState S = dense_state(p, pb);
+  const float* Cb = p.C + pb * p.C_stride;
+  const int32_t r0 = blk * RB + wid * kDnWaveRows;
+  const int32_t nrows = R - r0 <= 0 ? 0 : (R - r0 < kDnWaveRows ? R - r0 : kDnWaveRows);
+  const float* src = BUILD ? Cb : S.K;
+  float buf[P][NC];
+#pragma unroll
+  for (int d = 0; d + 1 < P; ++d)
+    if (d < nrows) load_row4<KQ>(src + (int64_t)(r0 + d) * R, R, buf[d]);
+  float vc[NC];
+  load_row4<KQ>(S.v, R, vc);
+  const float sal = lane < nrows ? S.sA[r0 + lane] : 0.f;  // lane k: the supply of row r0 + k
+  float cs[NC];
+#pragma unroll
+  for (int j = 0; j < NC; ++j) cs[j] = 0.f;
+  float uo = 0.f;  // lane k: u of row r0 + k
+  uint32_t bad = 0;  // rows whose u left [2^-60, 2^60] (the same on every lane)
+  auto row = [&](auto kc) __attribute__((always_inline)) {
+    constexpr int k = decltype(kc)::value;
+    if (k >= nrows) return;  // uniform
+    if (k + P - 1 < nrows) load_row4<KQ>(src + (int64_t)(r0 + k + P - 1) * R, R, buf[(k + P - 1) % P]);
+    float (&x)[NC] = buf[k % P];
+    const int32_t i = r0 + k;
+    const float sa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sal), k));
+    float u = 0.f;
+    if (BUILD) {
+      if (sa > 0.f) {
+        float G[NC];
+        load_row4<KQ>(S.G, R, G);
+#pragma unroll
+        for (int j = 0; j < NC; ++j) {
+          const int32_t col = 4 * (lane + kWave * (j / 4)) + (j & 3);
+          G[j] = col < R ? G[j] : -INFINITY;
+        }
+        const float fi = row_exact4<NC>(x, G, vc, sa, kappa);
+        if (lane == 0) S.F[i] = fi;
+        u = 1.f;
+      } else {
+#pragma unroll
+        for (int j = 0; j < NC; ++j) x[j] = 0.f;
+        if (lane == 0) S.F[i] = -INFINITY;
+      }
+      store_row4<KQ>(S.K + (int64_t)i * R, R, x);
+    } else if (sa > 0.f) {
+      float y = 0.f;
+#pragma unroll
+      for (int j = 0; j < NC; ++j) y = __builtin_fmaf(x[j], vc[j], y);
+      y = lanes_sum(y);
+      u = sa * frcp(y);
+      if (!in_range(u)) {  // uniform: every lane holds the same y
+        bad |= 1u << k;    // updated after the stream, from C
+        u = 0.f;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NC; ++j) cs[j] = __builtin_fmaf(u, x[j], cs[j]);
+    if (lane == k) uo = u;
+  };
+  Unrolled<kDnWaveRows>::run(row);
+  // rows whose u left the range: the exact log-domain update from the row of
+  // C (u = 1), added to the column sums after the streamed rows
+  for (uint32_t m = (uint32_t)__builtin_amdgcn_readfirstlane((int)bad); m; m &= m - 1) {
+    const int k = __builtin_ctz(m);
+    const int32_t i = r0 + k;
+    const float sa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sal), k));
+    float x[NC], G[NC];
+    load_row4<KQ>(Cb + (int64_t)i * R, R, x);
+    load_row4<KQ>(S.G, R, G);
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const int32_t col = 4 * (lane + kWave * (j / 4)) + (j & 3);
+      G[j] = col < R ? G[j] : -INFINITY;
+    }
+    const float fi = row_exact4<NC>(x, G, vc, sa, kappa);
+    store_row4<KQ>(S.K + (int64_t)i * R, R, x);
+    if (lane == 0) S.F[i] = fi;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) cs[j] += x[j];
+    if (lane == k) uo = 1.f;
+  }
+  if (lane < nrows) S.u[r0 + lane] = uo;
+  store_row4<KQ>(wpart + (int64_t)wid * R, R, cs);
+  __syncthreads();
+  for (int32_t q = tid; q < R / 4; q += kDnThreads) {
+    float4 a = reinterpret_cast<const float4*>(wpart)[q];
+#pragma unroll
+    for (int w = 1; w < kDnWaves; ++w) {
+      const float4 b = reinterpret_cast<const float4*>(wpart + w * R)[q];
+      a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    }
+    reinterpret_cast<float4*>(S.part + (int64_t)blk * R)[q] = a;
+  }
 }
 
 // One column half-step for 16 columns of a problem: the 16 thread groups add
@@ -492,7 +652,7 @@ __global__ void __launch_bounds__(kDnThreads) dense_col_kernel(SkParams p, float
 // The plan of the row block, T_ij = u_i K~_ij v_j, and its column sums for
 // the column cap.
 __global__ void __launch_bounds__(kDnThreads) dense_plan_kernel(SkParams p) {
-  const int32_t R = p.R, RB = dense_rb(R), NB = dense_blocks(R);
+  const int32_t R = p.R, RB = kDnRowBlock, NB = dense_blocks(R);
   const int64_t pb = blockIdx.x / NB;
   const int32_t blk = blockIdx.x % NB;
   if (p.stream_flag[pb] != 0) return;
@@ -535,7 +695,7 @@ __global__ void __launch_bounds__(kDnThreads) dense_out_kernel(SkParams p, int32
 // T_ij *= cap_j over the rows of a row block, the thread's columns held in
 // registers (16-byte accesses when R % 4 == 0).
 __global__ void __launch_bounds__(kDnThreads) dense_cap_kernel(SkParams p) {
-  const int32_t R = p.R, RB = dense_rb(R), NB = dense_blocks(R);
+  const int32_t R = p.R, RB = kDnRowBlock, NB = dense_blocks(R);
   const int64_t pb = blockIdx.x / NB;
   const int32_t blk = blockIdx.x % NB;
   if (p.stream_flag[pb] != 0) return;
@@ -562,18 +722,32 @@ __global__ void __launch_bounds__(kDnThreads) dense_cap_kernel(SkParams p) {
 
 template <bool BUILD>
 taot_status launch_rows(const SkParams& p, float kappa, unsigned grid, hipStream_t stream) {
-  const int vec = dense_vec(p.R), kpt = dense_kpt(p.R);
-#define TAOT_DN_ROW(V, K)                                                                                     \
-  if (vec == V && kpt == K) {                                                                                 \
-    hipLaunchKernelGGL((dense_row_kernel<V, K, BUILD>), dim3(grid), dim3(kDnThreads), 0, stream, p, kappa); \
+  const int32_t R = p.R;
+  if ((R & 3) == 0 && (reinterpret_cast<uintptr_t>(p.C) & 15u) == 0) {
+    const size_t lds = (size_t)kDnWaves * R * sizeof(float);
+    const int kq = dense_kq(R);
+#define TAOT_DN_ROWW(K)                                                                                        \
+  if (kq == K) {                                                                                             \
+    hipLaunchKernelGGL((dense_roww_kernel<K, BUILD>), dim3(grid), dim3(kDnThreads), lds, stream, p, kappa); \
+    return TAOT_OK;                                                                                          \
+  }
+    TAOT_DN_ROWW(1)
+    TAOT_DN_ROWW(2)
+    TAOT_DN_ROWW(4)
+    TAOT_DN_ROWW(8)
+#undef TAOT_DN_ROWW
+    return TAOT_ERR_UNSUPPORTED;
+  }
+  const int kpt = dense_kpt(R);
+#define TAOT_DN_ROW(K)                                                                                        \
+  if (kpt == K) {                                                                                             \
+    hipLaunchKernelGGL((dense_row_kernel<1, K, BUILD>), dim3(grid), dim3(kDnThreads), 0, stream, p, kappa); \
     return TAOT_OK;                                                                                           \
   }
-  TAOT_DN_ROW(4, 1)
-  TAOT_DN_ROW(4, 2)
-  TAOT_DN_ROW(1, 1)
-  TAOT_DN_ROW(1, 2)
-  TAOT_DN_ROW(1, 4)
-  TAOT_DN_ROW(1, 8)
+  TAOT_DN_ROW(1)
+  TAOT_DN_ROW(2)
+  TAOT_DN_ROW(4)
+  TAOT_DN_ROW(8)
 #undef TAOT_DN_ROW
   return TAOT_ERR_UNSUPPORTED;
 }

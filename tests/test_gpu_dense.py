@@ -133,3 +133,36 @@ def test_dense_long_run_potentials_grow(gpu):
     T, f, g, st = _dense(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, 150)
     assert np.isfinite(T).all()
     _check(L.excess.astype(np.float32), L.spare.astype(np.float32), C, w.eps, 150)
+
+
+@pytest.mark.parametrize("R", [100, 1024])
+def test_dense_unaligned_costs(R, gpu):
+    """Costs 4 bytes off 16-byte alignment (a view into a larger buffer): the
+    R % 4 == 0 shapes then take the phased row kernel instead of the
+    wave-streamed one, with the same results against the oracle."""
+    rng = np.random.default_rng(R + 11)
+    B = 2
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p in range(B):
+        hot = rng.random(R) < 0.1
+        hot[0] = True
+        a[p, hot] = rng.integers(1, 3000, size=int(hot.sum()))
+        b[p, ~hot] = rng.integers(1, 3000, size=int((~hot).sum()))
+    C = rng.uniform(0.0, 4.0, size=(B, R, R)).astype(np.float32)
+    dev = torch.device("cuda:0")
+    flat = torch.empty(B * R * R + 1, dtype=torch.float32, device=dev)
+    Cv = flat[1:].view(B, R, R)
+    Cv.copy_(torch.from_numpy(C))
+    assert Cv.data_ptr() % 16 == 4
+    out = taot.sinkhorn_batched(torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev), Cv, 0.2, 40, taot.SK_DENSE)
+    torch.cuda.synchronize()
+    T, f, g = out.T.cpu().numpy(), out.f.cpu().numpy(), out.g.cpu().numpy()
+    st = out.status.cpu().numpy().view(np.uint32)
+    ref = O.sinkhorn(a.astype(np.float64), b.astype(np.float64), C.astype(np.float64), 0.2, 40)
+    assert np.all(st == taot.ST_STREAMED), st
+    sinkhorn_check(T, ref.T, a.astype(np.float64), b.astype(np.float64))
+    potentials_check(f, g, ref.f, ref.g, 0.2, 40)
+    # the aligned copy takes the wave-streamed kernel: the same plan to the tolerance
+    T2 = _dense(a, b, C, 0.2, 40)[0]
+    assert np.abs(T2.astype(np.float64) - T).sum() <= 1e-4 * np.abs(T).sum()
