@@ -586,6 +586,7 @@ __global__ void __launch_bounds__(kDnThreads) dense_col_kernel(SkParams p, float
   const int32_t j = (int32_t)(blockIdx.x % chunks) * kDnColBlock + cl;
   if (p.stream_flag[pb] != 0) return;  // uniform per block
   const DenseState S = dense_state(p, pb);
+  const float dj = tid < kDnColBlock && j < R ? p.b[pb * R + j] : 0.f;  // in flight with the partials
   float x = 0.f;
   if (j < R)
     for (int32_t t = NB * grp / G; t < NB * (grp + 1) / G; ++t) x += S.part[(int64_t)t * R + j];
@@ -593,7 +594,6 @@ __global__ void __launch_bounds__(kDnThreads) dense_col_kernel(SkParams p, float
   if (tid == 0) nfix = 0;
   __syncthreads();
   if (tid < kDnColBlock && j < R) {
-    const float dj = p.b[pb * R + j];
     if (!(dj > 0.f)) {
       // no demand: no flow into this column, and its entries of K~ are zero
       // in every later rebuild (G_j = -inf), so none can overflow
