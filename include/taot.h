@@ -68,13 +68,23 @@ typedef enum {
                                      default small batches spread a problem over
                                      up to four waves)                              */
 #define TAOT_SK_DENSE 0x10u       /* dense streamed iterate (Sec. A.2, GEMV form): the
-                                     log-domain updates over all R x R entries of
+                                     stabilised updates over all R x R entries of
                                      every problem, with no support compaction; each
-                                     iteration streams the cost matrix from device
-                                     memory through every compute unit.  Same
-                                     outputs as the default paths (to rounding);
-                                     status TAOT_ST_STREAMED.  The other TAOT_SK_*
-                                     flags except NO_COLCAP are ignored           */
+                                     iteration streams the stored kernel matrix
+                                     (built from C in the first) from device memory
+                                     through every compute unit.  Same outputs as
+                                     the default paths (to rounding); status
+                                     TAOT_ST_STREAMED.  The other TAOT_SK_* flags
+                                     except NO_COLCAP and LINEAR are ignored      */
+#define TAOT_SK_LINEAR 0x20u      /* the linear-domain GEMV form itself (Sec. A.2):
+                                     u = s~ / (M v), v = d / (M^T u) with
+                                     M = exp(-C / eps) formed once in fp32 and no
+                                     stabilisation, on the dense streamed kernels
+                                     (implies TAOT_SK_DENSE).  Valid only while M's
+                                     entries and the scalings stay in fp32's normal
+                                     range (costs up to about 80 eps); beyond it the
+                                     plan may hold zeros, inf or NaN, as the plain
+                                     form does                                     */
 
 /* round_schedule flags: ablations of the Phase-2 score (Sec. A.3 discusses
  * the contribution of each term).  Phase 3 is unaffected. */

@@ -24,7 +24,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtaot.so")
 
 ST_BAD_ID, ST_BAD_INPUT, ST_ZERO_MASS, ST_UNFILLED, ST_STREAMED = 0x1, 0x2, 0x4, 0x8, 0x10
-SK_NO_COLCAP, SK_FORCE_STREAM, SK_NO_REGISTER, SK_WAVES_1, SK_DENSE = 0x1, 0x2, 0x4, 0x8, 0x10
+SK_NO_COLCAP, SK_FORCE_STREAM, SK_NO_REGISTER, SK_WAVES_1, SK_DENSE, SK_LINEAR = 0x1, 0x2, 0x4, 0x8, 0x10, 0x20
 SCH_NO_TOPO, SCH_NO_FLOW, SCH_ROW_PRIORITY = 0x1, 0x2, 0x4  # Phase-2 ablations (round_schedule flags)
 STATUS_NAMES = {0: "ok", 1: "invalid argument", 2: "unsupported shape", 3: "workspace", 4: "launch"}
 

@@ -88,7 +88,7 @@ taot_status taot_sinkhorn_batched(const float* a, const float* b, int32_t B, int
   if (bad_dims(B, R) || !(eps > 0.f) || !isfinite(eps) || iters < 1 ||
       (C_batch_stride != 0 && C_batch_stride != (int64_t)R * R) ||
       (flags & ~(TAOT_SK_NO_COLCAP | TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER | TAOT_SK_WAVES_1 |
-                 TAOT_SK_DENSE)))
+                 TAOT_SK_DENSE | TAOT_SK_LINEAR)))
     return TAOT_ERR_INVALID_ARG;
   if (R > TAOT_MAX_RANKS) return TAOT_ERR_UNSUPPORTED;
   if (B == 0) return TAOT_OK;

@@ -845,7 +845,7 @@ taot_status launch_sinkhorn(const float* a, const float* b, int32_t B, int32_t R
                        (int64_t)R * R, p.cchunks, w.cbad);
     if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   }
-  if (flags & TAOT_SK_DENSE) return launch_dense(p, stream);
+  if (flags & (TAOT_SK_DENSE | TAOT_SK_LINEAR)) return launch_dense(p, stream);
   const size_t vec_bytes = (size_t)kVecArrays * R * sizeof(float);
   const bool lds_path = R <= kLdsMaxR;
   if (!(flags & (TAOT_SK_FORCE_STREAM | TAOT_SK_NO_REGISTER))) {

@@ -249,6 +249,7 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
   const DenseState S = dense_state(p, pb);
   const float* Cb = p.C + pb * p.C_stride;
   const int32_t r0 = blk * RB;
+  const bool linear = (p.flags & TAOT_SK_LINEAR) != 0;
   for (int32_t r = tid; r < RB; r += kDnThreads) sal[r] = r0 + r < R ? S.sA[r0 + r] : 0.f;
   // G_c, v_c and G_c + log2 v_c of the thread's columns (-inf off the matrix
   // and where v_c = 0)
@@ -286,7 +287,7 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
     float (&cur)[TR][NC] = buf[ph % (kDnDepth + 1)];
     const int par = ph & 1;
     float uo = 0.f;  // u_i of row i0 + tid (tid < TR)
-    if (BUILD) {
+    if (BUILD && !linear) {
       // exact first row update: x_ic = (G_c + log2 v_c) - C'_ic
       float pm[TR];
 #pragma unroll
@@ -330,6 +331,16 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
         }
       }
     } else {
+      if (BUILD) {
+        // linear domain: M_ij = exp(-C_ij / eps) = exp2(-C'_ij), stored once
+#pragma unroll
+        for (int r = 0; r < TR; ++r) {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) cur[r][c] = r < nr && col_of<VEC>(c) < R ? fexp2(-(cur[r][c] * kappa)) : 0.f;
+          if (r < nr) store_row<VEC, KPT>(S.K + (int64_t)(i0 + r) * R, R, cur[r]);
+        }
+        if (tid < nr) S.F[i0 + tid] = 0.f;
+      }
       float py[TR];
 #pragma unroll
       for (int r = 0; r < TR; ++r) {
@@ -347,7 +358,7 @@ __global__ void __launch_bounds__(kDnThreads) __attribute__((amdgpu_waves_per_eu
         const float4 w = red[par][0][r];
         const float sa = sal[ph * TR + r];
         u[r] = sa > 0.f ? sa * frcp(((w.x + w.y) + w.z) + w.w) : 0.f;
-        if (sa > 0.f && !in_range(u[r])) bad |= 1u << r;
+        if (!linear && sa > 0.f && !in_range(u[r])) bad |= 1u << r;
       }
       // rows out of range: exact log-domain update from C, one row at a time
       for (uint32_t m = bad; m; m &= m - 1) {
@@ -474,6 +485,7 @@ dense_roww_kernel(SkParams p, float kappa) {
   const float* Cb = p.C + pb * p.C_stride;
   const int32_t r0 = blk * RB + wid * kDnWaveRows;
   const int32_t nrows = R - r0 <= 0 ? 0 : (R - r0 < kDnWaveRows ? R - r0 : kDnWaveRows);
+  const bool linear = (p.flags & TAOT_SK_LINEAR) != 0;
   const float* src = BUILD ? Cb : S.K;
   float buf[P][NC];
 #pragma unroll
@@ -495,7 +507,18 @@ dense_roww_kernel(SkParams p, float kappa) {
     const int32_t i = r0 + k;
     const float sa = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sal), k));
     float u = 0.f;
-    if (BUILD) {
+    bool step = !BUILD;  // the row takes the scaling update from its row of K~
+    if (BUILD && linear) {
+      // M_ij = exp(-C_ij / eps) = exp2(-C'_ij), stored once
+#pragma unroll
+      for (int j = 0; j < NC; ++j) {
+        const int32_t col = 4 * (lane + kWave * (j / 4)) + (j & 3);
+        x[j] = col < R ? fexp2(-(x[j] * kappa)) : 0.f;
+      }
+      store_row4<KQ>(S.K + (int64_t)i * R, R, x);
+      if (lane == 0) S.F[i] = 0.f;
+      step = true;
+    } else if (BUILD) {
       if (sa > 0.f) {
         float G[NC];
         load_row4<KQ>(S.G, R, G);
@@ -513,13 +536,14 @@ dense_roww_kernel(SkParams p, float kappa) {
         if (lane == 0) S.F[i] = -INFINITY;
       }
       store_row4<KQ>(S.K + (int64_t)i * R, R, x);
-    } else if (sa > 0.f) {
+    }
+    if (step && sa > 0.f) {
       float y = 0.f;
 #pragma unroll
       for (int j = 0; j < NC; ++j) y = __builtin_fmaf(x[j], vc[j], y);
       y = lanes_sum(y);
       u = sa * frcp(y);
-      if (!in_range(u)) {  // uniform: every lane holds the same y
+      if (!linear && !in_range(u)) {  // uniform: every lane holds the same y
         bad |= 1u << k;    // updated after the stream, from C
         u = 0.f;
       }
@@ -604,7 +628,7 @@ __global__ void __launch_bounds__(kDnThreads) dense_col_kernel(SkParams p, float
 #pragma unroll
       for (int g = 1; g < G; ++g) xs += ps[g][cl];
       const float vn = dj * frcp(xs);
-      if (in_range(vn)) S.v[j] = vn;
+      if (in_range(vn) || (p.flags & TAOT_SK_LINEAR)) S.v[j] = vn;
       else fixl[atomicAdd(&nfix, 1)] = j;
     }
   }

@@ -166,3 +166,52 @@ def test_dense_unaligned_costs(R, gpu):
     # the aligned copy takes the wave-streamed kernel: the same plan to the tolerance
     T2 = _dense(a, b, C, 0.2, 40)[0]
     assert np.abs(T2.astype(np.float64) - T).sum() <= 1e-4 * np.abs(T).sum()
+
+
+@pytest.mark.parametrize("cfg,problems", [(0, [0]), (1, [0, 1, 2, 3])])
+def test_linear_domain_workloads(cfg, problems, gpu):
+    """TAOT_SK_LINEAR (the GEMV form on M = exp(-C / eps) without
+    stabilisation, Sec. A.2) against the oracle's linear-domain iterate at the
+    same N, on the workloads whose M stays in fp32's normal range."""
+    w = W.WORKLOADS[cfg]
+    print(f"[linear parity] workload {cfg} problems {problems}", flush=True)
+    _, L = oracle_inputs(w, problems)
+    a32, b32, C32 = L.excess.astype(np.float32), L.spare.astype(np.float32), W.cost_matrix(w)
+    T, f, g, st = _dense(a32, b32, C32, w.eps, w.iters, taot.SK_LINEAR)
+    a, b = a32.astype(np.float64), b32.astype(np.float64)
+    ref = O.sinkhorn(a, b, C32.astype(np.float64), w.eps, w.iters, domain="linear")
+    ok = ref.status == 0
+    assert np.all(st[ok] == taot.ST_STREAMED), st
+    sinkhorn_check(T[ok], ref.T[ok], a[ok], b[ok])
+    potentials_check(f[ok], g[ok], ref.f[ok], ref.g[ok], w.eps, w.iters)
+
+
+@pytest.mark.parametrize("R", [5, 17, 100, 300])
+def test_linear_domain_ragged(R, gpu):
+    """The linear mode on both row kernels (odd R takes the phased one),
+    costs up to 20 eps, shared and per-problem; also close to the stabilised
+    dense mode, which computes the same iterate.  Supply and demand have equal
+    totals, as excess and spare do: with a demand total many times the supply
+    the plain scalings grow by that ratio every iteration and leave fp32's
+    range within a few dozen iterations (fp64 only later), which the
+    stabilised modes absorb and the linear form, by definition, does not."""
+    rng = np.random.default_rng(R + 5)
+    B = 3
+    a = np.zeros((B, R), np.float32)
+    b = np.zeros((B, R), np.float32)
+    for p in range(B):
+        hot = rng.random(R) < 0.3
+        hot[0] = True
+        hot[-1] = False
+        a[p, hot] = rng.integers(1, 3000, size=int(hot.sum()))
+        cold = rng.uniform(1.0, 3000.0, size=int((~hot).sum()))
+        b[p, ~hot] = (cold * (a[p].sum(dtype=np.float64) / cold.sum())).astype(np.float32)
+    for shape in ((R, R), (B, R, R)):
+        C = rng.uniform(0.0, 2.0, size=shape).astype(np.float32)
+        T, f, g, st = _dense(a, b, C, 0.1, 50, taot.SK_LINEAR)
+        ref = O.sinkhorn(a.astype(np.float64), b.astype(np.float64), C.astype(np.float64), 0.1, 50, domain="linear")
+        assert np.all(st == taot.ST_STREAMED), st
+        sinkhorn_check(T, ref.T, a.astype(np.float64), b.astype(np.float64))
+        potentials_check(f, g, ref.f, ref.g, 0.1, 50)
+        Ts = _dense(a, b, C, 0.1, 50)[0]
+        assert np.abs(Ts.astype(np.float64) - T).sum() <= 1e-4 * np.abs(T).sum()
