@@ -123,6 +123,12 @@ const char* taot_status_string(taot_status s);
  *   rho     [B]       double  imbalance (max_r l_r - L/R) / (L/R) (0 if L = 0), nullable.
  *   alpha   [B]       double  score scale alpha = mean * R / E = L / E.
  *   bad_ids [B]       int64   ids outside [0, E), nullable.
+ *   hot_idx [B][R]    int32   the hot set H = {r : l_r > m} in ascending rank
+ *                             order, then -1 (nullable);
+ *   cold_idx [B][R]   int32   the cold set C = {r : l_r < m} likewise (nullable);
+ *   hot_cnt, cold_cnt [B] int32  |H| and |C| (each nullable).  The Sinkhorn
+ *                             derives its support from a and b itself, so
+ *                             these are outputs for the caller only.
  *   status  [B]       uint32  TAOT_ST_BAD_ID, TAOT_ST_BAD_INPUT (home out of range).
  * Limits: 1 <= R <= TAOT_MAX_RANKS, 1 <= E <= TAOT_MAX_EXPERTS, B >= 0,
  * 0 <= N <= 2^31 - 1 and B * R <= 2^31 - 1 (else TAOT_ERR_UNSUPPORTED).
@@ -132,6 +138,7 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
                             const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
                             int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                             float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                            int32_t* hot_idx, int32_t* cold_idx, int32_t* hot_cnt, int32_t* cold_cnt,
                             uint32_t* status, void* ws, size_t ws_bytes, void* stream);
 
 /* Allocation-free variant of taot_plan_loads, for callers that cannot
@@ -152,6 +159,7 @@ taot_status taot_plan_loads_noalloc(const int32_t* ids, int32_t B, int32_t R, in
                                     const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
                                     int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                                     float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                                    int32_t* hot_idx, int32_t* cold_idx, int32_t* hot_cnt, int32_t* cold_cnt,
                                     uint32_t* status, void* stream);
 /* Largest B taot_plan_loads_noalloc accepts for R ranks and E experts (0 for
  * an invalid or unsupported R or E). */

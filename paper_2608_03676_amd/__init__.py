@@ -51,7 +51,7 @@ def lib():
         L.taot_plan_loads_workspace_size.restype = _SZ
         L.taot_plan_loads_workspace_size.argtypes = [_I32, _I32, _I32]
         L.taot_plan_loads.restype = ctypes.c_int
-        L.taot_plan_loads.argtypes = [_P, _I32, _I32, _I64, _I32] + [_P] * 13 + [_P, _SZ, _P]
+        L.taot_plan_loads.argtypes = [_P, _I32, _I32, _I64, _I32] + [_P] * 17 + [_P, _SZ, _P]
         L.taot_sinkhorn_workspace_size.restype = _SZ
         L.taot_sinkhorn_workspace_size.argtypes = [_I32, _I32]
         L.taot_sinkhorn_batched.restype = ctypes.c_int
@@ -109,6 +109,10 @@ class Loads:
     alpha: torch.Tensor    # [B] float64
     bad_ids: torch.Tensor  # [B] int64
     status: torch.Tensor   # [B] int32 (uint32 bits)
+    hot_idx: Optional[torch.Tensor] = None   # [B][R] int32: ranks with excess > 0, ascending, then -1
+    cold_idx: Optional[torch.Tensor] = None  # [B][R] int32: ranks with spare > 0, ascending, then -1
+    hot_cnt: Optional[torch.Tensor] = None   # [B] int32
+    cold_cnt: Optional[torch.Tensor] = None  # [B] int32
 
 
 def plan_loads(ids: torch.Tensor, home: torch.Tensor, E: int, out: Optional[Loads] = None,
@@ -123,13 +127,19 @@ def plan_loads(ids: torch.Tensor, home: torch.Tensor, E: int, out: Optional[Load
             ((B, R, E), torch.int32), ((B, E), torch.int64), ((B, R), torch.int64), ((B, R), torch.int64),
             ((B, R), torch.int64), ((B, E), torch.int64), ((B, R), torch.float32), ((B, R), torch.float32),
             ((B,), torch.float64), ((B,), torch.float64), ((B,), torch.int64), ((B,), torch.int32))))
+    if out.hot_idx is None:
+        out.hot_idx = torch.empty((B, R), dtype=torch.int32, device=dev)
+        out.cold_idx = torch.empty((B, R), dtype=torch.int32, device=dev)
+        out.hot_cnt = torch.empty((B,), dtype=torch.int32, device=dev)
+        out.cold_cnt = torch.empty((B,), dtype=torch.int32, device=dev)
     need = lib().taot_plan_loads_workspace_size(B, R, E)
     ws = workspace if workspace is not None else _workspace(need, dev)
     _check("taot_plan_loads", lib().taot_plan_loads(
         ids.data_ptr(), B, R, N, E, home.data_ptr(), out.n.data_ptr(), out.load_e.data_ptr(),
         out.load_r.data_ptr(), out.excess.data_ptr(), out.spare.data_ptr(), out.spill.data_ptr(),
         out.supply.data_ptr(), out.demand.data_ptr(), out.rho.data_ptr(), out.alpha.data_ptr(),
-        out.bad_ids.data_ptr(), out.status.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)))
+        out.bad_ids.data_ptr(), _ptr(out.hot_idx), _ptr(out.cold_idx), _ptr(out.hot_cnt), _ptr(out.cold_cnt),
+        out.status.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)))
     return out
 
 

@@ -35,6 +35,7 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
                             const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
                             int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                             float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                            int32_t* hot_idx, int32_t* cold_idx, int32_t* hot_cnt, int32_t* cold_cnt,
                             uint32_t* status, void* ws, size_t ws_bytes, void* stream) {
   if (bad_dims(B, R) || E <= 0 || N < 0) return TAOT_ERR_INVALID_ARG;
   if (R > TAOT_MAX_RANKS || E > TAOT_MAX_EXPERTS) return TAOT_ERR_UNSUPPORTED;
@@ -44,13 +45,15 @@ taot_status taot_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t N,
   if ((int64_t)B * R > 0x7fffffffLL || N > 0x7fffffffLL) return TAOT_ERR_UNSUPPORTED;
   if (!ws || ws_bytes < plan_loads_ws(B, R, E)) return TAOT_ERR_WORKSPACE;
   return launch_plan_loads(ids, B, R, N, E, home, n, load_e, load_r, excess, spare, spill, supply,
-                           demand, rho, alpha, bad_ids, status, ws, static_cast<hipStream_t>(stream));
+                           demand, rho, alpha, bad_ids, hot_idx, cold_idx, hot_cnt, cold_cnt, status, ws,
+                           static_cast<hipStream_t>(stream));
 }
 
 taot_status taot_plan_loads_noalloc(const int32_t* ids, int32_t B, int32_t R, int64_t N, int32_t E,
                                     const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
                                     int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                                     float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                                    int32_t* hot_idx, int32_t* cold_idx, int32_t* hot_cnt, int32_t* cold_cnt,
                                     uint32_t* status, void* stream) {
   if (bad_dims(B, R) || E <= 0 || N < 0) return TAOT_ERR_INVALID_ARG;
   if (R > TAOT_MAX_RANKS || E > TAOT_MAX_EXPERTS) return TAOT_ERR_UNSUPPORTED;
@@ -62,7 +65,8 @@ taot_status taot_plan_loads_noalloc(const int32_t* ids, int32_t B, int32_t R, in
   void* ws = plan_loads_scratch();
   if (!ws) return TAOT_ERR_LAUNCH;
   return launch_plan_loads(ids, B, R, N, E, home, n, load_e, load_r, excess, spare, spill, supply,
-                           demand, rho, alpha, bad_ids, status, ws, static_cast<hipStream_t>(stream));
+                           demand, rho, alpha, bad_ids, hot_idx, cold_idx, hot_cnt, cold_cnt, status, ws,
+                           static_cast<hipStream_t>(stream));
 }
 
 size_t taot_plan_loads_noalloc_max_problems(int32_t R, int32_t E) {

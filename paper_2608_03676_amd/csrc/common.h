@@ -69,6 +69,7 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
                               const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
                               int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                               float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                              int32_t* hot_idx, int32_t* cold_idx, int32_t* hot_cnt, int32_t* cold_cnt,
                               uint32_t* status, void* ws, hipStream_t stream);
 size_t plan_loads_ws(int32_t B, int32_t R, int32_t E);
 size_t plan_loads_scratch_limit();

@@ -245,6 +245,42 @@ expert_load_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, int64_t*
   }
 }
 
+// Optional hot/cold rank lists of the marginals: [B][R] ascending lists
+// (padded with -1) and [B] counts, each nullable.
+struct HotCold {
+  int32_t* hot_idx;
+  int32_t* cold_idx;
+  int32_t* hot_cnt;
+  int32_t* cold_cnt;
+};
+
+// Exclusive positions of two flags among the kMargThreads threads (ascending
+// thread id) and their totals.  All threads must call it.
+__device__ __forceinline__ void block_scan2(bool f0, bool f1, int32_t (*cnt)[kMargThreads / kWave], int32_t& p0,
+                                            int32_t& p1, int32_t& t0, int32_t& t1) {
+  const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+  const uint64_t m0 = __ballot(f0), m1 = __ballot(f1);
+  const uint64_t below = (1ull << lane) - 1ull;
+  if (lane == 0) {
+    cnt[0][wid] = __popcll(m0);
+    cnt[1][wid] = __popcll(m1);
+  }
+  __syncthreads();
+  int32_t o0 = 0, o1 = 0, s0 = 0, s1 = 0;
+  for (int w = 0; w < kMargThreads / kWave; ++w) {
+    const int32_t a = cnt[0][w], c = cnt[1][w];
+    o0 += w < wid ? a : 0;
+    o1 += w < wid ? c : 0;
+    s0 += a;
+    s1 += c;
+  }
+  __syncthreads();  // every thread has read cnt before the next call rewrites it
+  p0 = o0 + __popcll(m0 & below);
+  p1 = o1 + __popcll(m1 & below);
+  t0 = s0;
+  t1 = s1;
+}
+
 // One block per problem; x_e comes from expert_load_kernel.
 __global__ void __launch_bounds__(kMargThreads)
 marginals_kernel(int32_t R, int32_t E, const int32_t* __restrict__ home, const int32_t* __restrict__ rank_ptr,
@@ -253,10 +289,11 @@ marginals_kernel(int32_t R, int32_t E, const int32_t* __restrict__ home, const i
                  int64_t* __restrict__ load_r, int64_t* __restrict__ excess, int64_t* __restrict__ spare,
                  int64_t* __restrict__ spill, float* __restrict__ supply, float* __restrict__ demand,
                  double* __restrict__ rho, double* __restrict__ alpha, int64_t* __restrict__ bad_ids,
-                 uint32_t* __restrict__ status) {
+                 HotCold hc, uint32_t* __restrict__ status) {
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x;
   __shared__ int64_t red_s[kMargThreads / kWave], red_m[kMargThreads / kWave];
+  __shared__ int32_t scan_cnt[2][kMargThreads / kWave];
   __shared__ int64_t sh_L, sh_max;
   const bool home_bad = bad_home[0] != 0;
   const int64_t skipped = (int64_t)bad_prob[b];  // ids of this problem outside [0, E)
@@ -269,10 +306,16 @@ marginals_kernel(int32_t R, int32_t E, const int32_t* __restrict__ home, const i
       if (supply) supply[b * R + r] = 0.f;
       if (demand) demand[b * R + r] = 0.f;
     }
+    for (int32_t r = tid; r < R; r += kMargThreads) {
+      if (hc.hot_idx) hc.hot_idx[b * R + r] = -1;
+      if (hc.cold_idx) hc.cold_idx[b * R + r] = -1;
+    }
     if (tid == 0) {
       if (rho) rho[b] = 0.0;
       alpha[b] = 0.0;
       if (bad_ids) bad_ids[b] = skipped;
+      if (hc.hot_cnt) hc.hot_cnt[b] = 0;
+      if (hc.cold_cnt) hc.cold_cnt[b] = 0;
       if (status) status[b] = TAOT_ST_BAD_INPUT | (skipped ? TAOT_ST_BAD_ID : 0u);
     }
     return;
@@ -308,6 +351,30 @@ marginals_kernel(int32_t R, int32_t E, const int32_t* __restrict__ home, const i
     spare[b * R + r] = sp;
     if (supply) supply[b * R + r] = (float)ex;
     if (demand) demand[b * R + r] = (float)sp;
+  }
+  // the hot and cold sets H = {r : l_r > m}, C = {r : l_r < m} (Sec. A.1) as
+  // ascending rank lists padded with -1 (each thread reads back the loads it
+  // wrote above: same rank stride)
+  if (hc.hot_idx || hc.cold_idx || hc.hot_cnt || hc.cold_cnt) {
+    int32_t nh = 0, nc = 0;
+    for (int32_t base = 0; base < R; base += kMargThreads) {
+      const int32_t r = base + tid;
+      const int64_t l = r < R ? load_r[b * R + r] : mean;
+      int32_t ph, pc, th, tc;
+      block_scan2(l > mean, l < mean, scan_cnt, ph, pc, th, tc);
+      if (l > mean && hc.hot_idx) hc.hot_idx[b * R + nh + ph] = r;
+      if (l < mean && hc.cold_idx) hc.cold_idx[b * R + nc + pc] = r;
+      nh += th;
+      nc += tc;
+    }
+    for (int32_t r = tid; r < R; r += kMargThreads) {
+      if (hc.hot_idx && r >= nh) hc.hot_idx[b * R + r] = -1;
+      if (hc.cold_idx && r >= nc) hc.cold_idx[b * R + r] = -1;
+    }
+    if (tid == 0) {
+      if (hc.hot_cnt) hc.hot_cnt[b] = nh;
+      if (hc.cold_cnt) hc.cold_cnt[b] = nc;
+    }
   }
   if (tid == 0) {
     if (rho) rho[b] = L > 0 ? (double)((int64_t)R * sh_max - L) / (double)L : 0.0;
@@ -386,6 +453,7 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
                               const int32_t* home, int32_t* n, int64_t* load_e, int64_t* load_r,
                               int64_t* excess, int64_t* spare, int64_t* spill, float* supply,
                               float* demand, double* rho, double* alpha, int64_t* bad_ids,
+                              int32_t* hot_idx, int32_t* cold_idx, int32_t* hot_cnt, int32_t* cold_cnt,
                               uint32_t* status, void* ws, hipStream_t stream) {
   if (B == 0) return TAOT_OK;
   LoadsWs w = carve(ws, B, R, E);
@@ -421,7 +489,7 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   hipLaunchKernelGGL(marginals_kernel, dim3((unsigned)B), dim3(kMargThreads), 0, stream, R, E, home, w.rank_ptr,
                      w.rank_exp, w.bad_home, w.bad_prob, load_e, load_r, excess, spare, spill, supply, demand,
-                     rho, alpha, bad_ids, status);
+                     rho, alpha, bad_ids, HotCold{hot_idx, cold_idx, hot_cnt, cold_cnt}, status);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   return TAOT_OK;
 }

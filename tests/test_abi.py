@@ -65,7 +65,8 @@ def test_host_validation_plan_loads():
     L = taot.lib()
     P = _fake()
     args = lambda B, R, N, E, ids=P, ws=P, wsb=1 << 30: L.taot_plan_loads(
-        ids, B, R, N, E, P, P, P, P, P, P, P, None, None, None, P, None, None, ws, wsb, None)
+        ids, B, R, N, E, P, P, P, P, P, P, P, None, None, None, P, None, None, None, None, None, None, ws, wsb,
+        None)
     assert args(1, 0, 8, 4) == 1            # R <= 0
     assert args(1, 4, -1, 4) == 1           # N < 0
     assert args(1, 4, 8, 0) == 1            # E <= 0
@@ -135,7 +136,7 @@ def test_noalloc_limits_on_host():
     L = taot.lib()
     L.taot_plan_loads_noalloc.restype = ctypes.c_int
     L.taot_plan_loads_noalloc.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
-                                          ctypes.c_int32] + [ctypes.c_void_p] * 14
+                                          ctypes.c_int32] + [ctypes.c_void_p] * 18
     L.taot_plan_loads_noalloc_max_problems.restype = ctypes.c_size_t
     L.taot_plan_loads_noalloc_max_problems.argtypes = [ctypes.c_int32, ctypes.c_int32]
     cap16 = L.taot_plan_loads_noalloc_max_problems(16, 64)
@@ -145,7 +146,7 @@ def test_noalloc_limits_on_host():
     assert L.taot_plan_loads_noalloc_max_problems(16, 32769) == 0
     # the workspace of cap16 problems fits 1 MiB, one more does not
     assert L.taot_plan_loads_workspace_size(cap16, 16, 64) <= 1 << 20 < L.taot_plan_loads_workspace_size(cap16 + 1, 16, 64)
-    p = [_fake()] * 13
+    p = [_fake()] * 17
     assert L.taot_plan_loads_noalloc(_fake(), cap16 + 1, 16, 8, 64, *p, None) == 5
     assert L.taot_status_string(5).startswith(b"needs more than the fixed scratch")
     assert L.taot_plan_loads_noalloc(None, 1, 16, 8, 64, *p, None) == 1  # ids NULL with N > 0

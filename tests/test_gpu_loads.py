@@ -33,6 +33,13 @@ def _compare(g, ref, label=""):
     assert g["alpha"].tobytes() == ref.alpha.tobytes(), f"{label} alpha"
     assert np.array_equal(g["bad_ids"], ref.bad), f"{label} bad ids"
     assert np.array_equal(g["status"].view(np.uint32), ref.status), f"{label} status"
+    # the hot and cold sets (Sec. A.1) as ascending lists padded with -1
+    for p in range(ref.excess.shape[0]):
+        for name, vals in (("hot", ref.excess[p]), ("cold", ref.spare[p])):
+            want = np.flatnonzero(vals > 0)
+            got = g[name + "_idx"][p]
+            assert g[name + "_cnt"][p] == want.size, f"{label} {name} count"
+            assert np.array_equal(got[:want.size], want) and np.all(got[want.size:] == -1), f"{label} {name} list"
 
 
 @pytest.mark.parametrize("cfg,problems", [(0, [0]), (1, list(range(58))), (2, [0, 1, 2, 3, 191, 383]),
@@ -88,6 +95,8 @@ def test_bad_home_sets_status(gpu):
     g = _gpu_loads(ids, home, 4)
     assert np.all(g["status"].view(np.uint32) & taot.ST_BAD_INPUT)
     assert not g["load_r"].any() and not g["spill"].any()
+    assert not g["hot_cnt"].any() and not g["cold_cnt"].any()
+    assert np.all(g["hot_idx"] == -1) and np.all(g["cold_idx"] == -1)
 
 
 def test_deterministic(gpu):

@@ -20,7 +20,7 @@ _P, _I32, _I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 def _lib():
     L = taot.lib()
     L.taot_plan_loads_noalloc.restype = ctypes.c_int
-    L.taot_plan_loads_noalloc.argtypes = [_P, _I32, _I32, _I64, _I32] + [_P] * 13 + [_P]
+    L.taot_plan_loads_noalloc.argtypes = [_P, _I32, _I32, _I64, _I32] + [_P] * 17 + [_P]
     L.taot_plan_loads_noalloc_max_problems.restype = ctypes.c_size_t
     L.taot_plan_loads_noalloc_max_problems.argtypes = [_I32, _I32]
     return L
@@ -30,7 +30,8 @@ def _outputs(B, R, E, dev):
     return taot.Loads(*(torch.full(s, -7, dtype=d, device=dev) for s, d in (
         ((B, R, E), torch.int32), ((B, E), torch.int64), ((B, R), torch.int64), ((B, R), torch.int64),
         ((B, R), torch.int64), ((B, E), torch.int64), ((B, R), torch.float32), ((B, R), torch.float32),
-        ((B,), torch.float64), ((B,), torch.float64), ((B,), torch.int64), ((B,), torch.int32))))
+        ((B,), torch.float64), ((B,), torch.float64), ((B,), torch.int64), ((B,), torch.int32),
+        ((B, R), torch.int32), ((B, R), torch.int32), ((B,), torch.int32), ((B,), torch.int32))))
 
 
 def _noalloc(ids, home, E, out):
@@ -40,12 +41,13 @@ def _noalloc(ids, home, E, out):
         ids.data_ptr(), B, R, N, E, home.data_ptr(), out.n.data_ptr(), out.load_e.data_ptr(),
         out.load_r.data_ptr(), out.excess.data_ptr(), out.spare.data_ptr(), out.spill.data_ptr(),
         out.supply.data_ptr(), out.demand.data_ptr(), out.rho.data_ptr(), out.alpha.data_ptr(),
-        out.bad_ids.data_ptr(), out.status.data_ptr(), ctypes.c_void_p(stream))
+        out.bad_ids.data_ptr(), out.hot_idx.data_ptr(), out.cold_idx.data_ptr(), out.hot_cnt.data_ptr(),
+        out.cold_cnt.data_ptr(), out.status.data_ptr(), ctypes.c_void_p(stream))
 
 
 def _same(a, b):
     for name in ("n", "load_e", "load_r", "excess", "spare", "spill", "supply", "demand", "rho", "alpha",
-                 "bad_ids", "status"):
+                 "bad_ids", "status", "hot_idx", "cold_idx", "hot_cnt", "cold_cnt"):
         x, y = getattr(a, name).cpu().numpy(), getattr(b, name).cpu().numpy()
         assert x.tobytes() == y.tobytes(), name
 
