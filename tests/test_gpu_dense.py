@@ -48,12 +48,14 @@ def test_dense_workloads(cfg, problems, gpu):
     _check(L.excess.astype(np.float32), L.spare.astype(np.float32), W.cost_matrix(w), w.eps, w.iters)
 
 
-@pytest.mark.parametrize("R", [1, 2, 5, 17, 100, 300, 1100])
+@pytest.mark.parametrize("R", [1, 2, 5, 17, 100, 300, 1027, 1100])
 @pytest.mark.parametrize("per_problem", [False, True])
 def test_dense_ragged_shapes(R, per_problem, gpu):
-    """R across one and several row blocks, partial LDS phases and column
-    chunks (R = 1100 takes 7-row phases); random supports with zeros on both
-    sides; costs shared or one matrix per problem."""
+    """R across one and several row blocks of 64, partial waves and phases,
+    both row kernels (R % 4 != 0 takes the phased one: 8 columns per thread
+    and 4-row phases at R = 1027) and both column-update widths (R > 1024);
+    random supports with zeros on both sides; costs shared or one matrix per
+    problem."""
     rng = np.random.default_rng(R * 7 + per_problem)
     B = 3
     a = np.zeros((B, R), np.float32)
