@@ -833,11 +833,12 @@ struct LdsState {
   // Phase 3 (aliases the Phase-2 region)
   double* price; uint32_t* rkey; int32_t* work; uint32_t* sstate;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
-  // relative counts: lvl0 [TW] the ranks at the base count, rel [kRelPlanes]
-  // [TW] the code planes, p0 the price of the base count; misc: base,
+  // relative counts: lvl0 [TW] the ranks at the base count, lvl1 [TW] those
+  // one service above it, rel [kRelPlanes] [TW] the code planes, p0 the
+  // price of the base count; misc: base,
   // minimum (rebase scratch), a base-count word emptied (2, by round parity),
   // a transfer made (2, by round parity), the base's epoch (rebases so far)
-  uint64_t* lvl0; uint64_t* rel; double* p0; int32_t* misc;
+  uint64_t* lvl0; uint64_t* lvl1; uint64_t* rel; double* p0; int32_t* misc;
   int8_t* cn; double* cv; int32_t* cvr; uint32_t* cw; uint64_t* cm;
   size_t bytes;
 };
@@ -872,7 +873,8 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
   w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
   w.cnt = (int32_t*)take(4 * R_); w.planes = (uint64_t*)take(8 * CF::kPL * TW);
-  w.lvl0 = (uint64_t*)take(8 * TW); w.rel = (uint64_t*)take(8 * kRelPlanes * TW);
+  w.lvl0 = (uint64_t*)take(8 * TW); w.lvl1 = (uint64_t*)take(8 * TW);
+  w.rel = (uint64_t*)take(8 * kRelPlanes * TW);
   w.p0 = (double*)take(8); w.misc = (int32_t*)take(4 * 8);
   w.cn = (int8_t*)take(SC);
   w.cv = (double*)take(8 * SC * kTierMax); w.cvr = (int32_t*)take(4 * SC * kTierMax);
@@ -1209,6 +1211,7 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   for (int32_t q = tid; q < TW; q += NT) {
     const int32_t lo = q * kWave;
     L.lvl0[q] = lo >= R ? 0ull : (R - lo >= kWave ? ~0ull : (1ull << (R - lo)) - 1ull);
+    L.lvl1[q] = 0ull;
   }
   for (int32_t q = tid; q < kRelPlanes * TW; q += NT) L.rel[q] = 0ull;
   if (tid < 8) L.misc[tid] = tid == 1 ? INT_MAX : 0;
@@ -1347,6 +1350,17 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
 #pragma unroll
           for (int w = 0; w < TW; ++w) { c[w] = tm[w] & valid[w]; anyc |= c[w]; }
           if (!anyc) return (int32_t)INT_MAX;
+          // no candidate is at the base count, so the lowest one a service
+          // above it, when there is one, has the fewest services
+          {
+            int32_t r1 = INT_MAX;
+#pragma unroll
+            for (int w = TW - 1; w >= 0; --w) {
+              const uint64_t h1 = c[w] & L.lvl1[w];
+              if (h1) r1 = w * kWave + __builtin_ctzll(h1);
+            }
+            if (r1 != INT_MAX) return r1;
+          }
           bool sat = true;
 #pragma unroll 1
           for (int j = kRelPlanes - 1; j >= 0; --j) {
@@ -1448,7 +1462,7 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
               wi[u] = wl ? __builtin_ctz(wl) : -1;
               wl &= wl - 1u;
             }
-            uint64_t pl[kRelPlanes][4];
+            uint64_t pl[kRelPlanes][4], l1[4];
             uint64_t any = 0;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
@@ -1456,10 +1470,23 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
               c[u] = wi[u] < 0 ? 0ull : tm[w] & vm[w];
               any |= c[u];
               cand |= (c[u] != 0ull ? 1u : 0u) << w;
+              l1[u] = L.lvl1[w];
 #pragma unroll
               for (int j = 0; j < kRelPlanes; ++j) pl[j][u] = L.rel[j * TW + w];
             }
             if (!any) continue;
+            // no candidate is at the base count, so a candidate one service
+            // above it has the fewest services: the first group (words
+            // ascending) that holds one gives the lowest such rank
+            {
+              int32_t r1 = INT_MAX;
+#pragma unroll
+              for (int u = 3; u >= 0; --u) {
+                const uint64_t h1 = c[u] & l1[u];
+                if (h1) r1 = wi[u] * kWave + __builtin_ctzll(h1);
+              }
+              if (r1 != INT_MAX) return r1;
+            }
             uint32_t code = 0;
 #pragma unroll
             for (int j = kRelPlanes - 1; j >= 0; --j) {
@@ -1591,6 +1618,8 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
               const uint64_t old = atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl0[r >> 6]), bit);
               if (old == bit) L.misc[2 + cur] = 1;
             }
+            // the rank enters (code 0 -> 1) or leaves (1 -> 2) the set one above the base
+            if (k0 == 0 || k0 == 1) atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl1[r >> 6]), bit);
           }
         }
         if (have - x <= 0) {
@@ -1626,8 +1655,11 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       __syncthreads();
       const int32_t nb = L.misc[1];
       const int32_t kr = tid < R ? min(L.cnt[tid] - nb, kRelMax) : -1;
-      const uint64_t m0 = __ballot(kr == 0);
-      if (lane == 0 && wid < TW) L.lvl0[wid] = m0;
+      const uint64_t m0 = __ballot(kr == 0), m1 = __ballot(kr == 1);
+      if (lane == 0 && wid < TW) {
+        L.lvl0[wid] = m0;
+        L.lvl1[wid] = m1;
+      }
 #pragma unroll
       for (int j = 0; j < kRelPlanes; ++j) {
         const uint64_t m = __ballot(kr > 0 && ((kr >> j) & 1));
