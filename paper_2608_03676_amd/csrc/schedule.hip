@@ -1590,7 +1590,11 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       bool keep = r >= 0;
       if (keep && rk[r] == key[i]) {
         const int32_t s = item[i] & kSlotMask, d = (item[i] >> kItemSlotBits) & kExpMask;
+        // the winner's reads first, so that they share one LDS round trip
+        // (the stores below may alias them as far as the compiler knows)
         int32_t a = L.amt[s];
+        const double pr = L.price[r];
+        const int32_t c0 = L.cnt[r], base = L.misc[0];
         const int32_t have = held[i];
         const int32_t x = have < a ? have : a;
         Xb[(int64_t)r * S + s] = x;
@@ -1601,16 +1605,16 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         const uint64_t bit = 1ull << (r & 63);
         if (x > 0) {
           L.misc[4 + cur] = 1;
-          L.price[r] = L.price[r] + step;
+          L.price[r] = pr + step;
           if (track) {
-            const int32_t c0 = L.cnt[r], c1 = c0 + 1;
+            const int32_t c1 = c0 + 1;
             L.cnt[r] = c1;
             newmax = c1 > newmax ? c1 : newmax;
             for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
               atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
             // the relative code rises by one (below saturation); a word of the
             // base-count set that empties is flagged for the round's end
-            const int32_t k0 = c0 - L.misc[0];
+            const int32_t k0 = c0 - base;
             if (k0 < kRelMax)
               for (uint32_t flip = (uint32_t)(k0 ^ (k0 + 1)); flip; flip &= flip - 1)
                 atomicXor(reinterpret_cast<unsigned long long*>(&L.rel[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
