@@ -1280,8 +1280,10 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     item[i] = i * NT + tid < sh_nw[1] ? L.work[i * NT + tid] : -1;
     state[i] = 0xFFFFFFFFu;  // no epoch matches it
   }
-  if constexpr (kPack)
+  if constexpr (kPack) {
     for (int32_t s = tid; s < S; s += NT) L.sstate[s] = 0xFFFFFFFFu;
+    __syncthreads();  // the first round reads states other threads cleared
+  }
   int64_t rounds = 0;
   for (int64_t t = 1; t <= tmax; ++t) {
     const int cur = (int)(t & 1), prv = cur ^ 1;
