@@ -831,7 +831,7 @@ struct LdsState {
   double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
   int32_t* qbest;  // [R] q = min(spill, spare) of each cold rank's standing proposal
   // Phase 3 (aliases the Phase-2 region)
-  double* price; uint32_t* rkey; int32_t* work; uint32_t* sstate;
+  double* price; uint32_t* rkey; int32_t* work; uint32_t* sstate; int16_t* gnext;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
   // relative counts: lvl0 [TW] the ranks at the base count, lvl1 [TW] those
   // one service above it, rel [kRelPlanes] [TW] the code planes, p0 the
@@ -869,6 +869,8 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   w.work = (int32_t*)take(4 * S1);
   // slot bid states of the packed layout (16-word sets, at most two slots per thread)
   w.sstate = (uint32_t*)take(TW > 4 && S1 <= 2 * (size_t)CF::kT ? 4 * S1 : 0);
+  // and the next open slot of each slot's bid group (same layout only)
+  w.gnext = (int16_t*)take(TW > 4 && S1 <= 2 * (size_t)CF::kT ? 2 * S1 : 0);
   // the word lists guide the per-word search of sets wider than 4 words only
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
   w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
@@ -1190,14 +1192,67 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     }
   }
   // the active-slot list of the first round: every slot with tokens planned
+  // (packed layout: the first slot of each bid group, see below)
+  constexpr bool kPack = TW > 4 && SPL <= 2;
   if (tid < 2) sh_nw[tid] = 0;
+  auto slot_item = [&](int32_t s, bool& f) {
+    const int32_t ec = s < S ? L.slot_ec[s] : -1;
+    f = ec >= 0 && L.amt[s] > 0;
+    return f ? s | (L.dmap[ec] << kItemSlotBits) | (wp.sidx[s / K] << (kItemSlotBits + kItemExpertBits)) : 0;
+  };
+  if constexpr (kPack) {
+    // Bid groups.  Two open slots with the same host tier structure and the
+    // same expert (the item's bits above the slot) make the same bid: the
+    // search reads only those and the shared state.  Their keys then differ
+    // in the slot alone, so the lower slot wins wherever both bid, and a
+    // slot of a group can only be served once every lower open slot of the
+    // group is full.  A group without a valid rank is without one for all
+    // its slots (validity depends on the expert only).  So each group bids
+    // with its lowest open slot only; when that slot fills, the next open
+    // slot of the group takes its place (and its bid state, which depends on
+    // the group alone).  The rounds, bids and transfers are the same as
+    // with every open slot bidding.  gnext[s] is that next slot (-1: none);
+    // sstate holds the group keys while it is built.
+    for (int32_t s = tid; s < S; s += NT) {
+      bool f;
+      const int32_t item = slot_item(s, f);
+      L.sstate[s] = f ? (uint32_t)item >> kItemSlotBits : 0xFFFFFFFFu;
+    }
+    __syncthreads();
+    for (int32_t s = tid; s < S; s += NT) {
+      const uint32_t k = L.sstate[s];
+      int32_t nx = -1;
+      if (k != 0xFFFFFFFFu) {
+        int32_t q = s + 1;
+        for (; q < S && (q & 3); ++q)
+          if (L.sstate[q] == k) { nx = q; break; }
+        if (nx < 0) {
+          // four keys per 16-byte load (sstate is 16-byte aligned)
+          for (; q + 3 < S; q += 4) {
+            const uint4 kq = *reinterpret_cast<const uint4*>(L.sstate + q);
+            if (kq.x == k || kq.y == k || kq.z == k || kq.w == k) {
+              nx = kq.x == k ? q : kq.y == k ? q + 1 : kq.z == k ? q + 2 : q + 3;
+              break;
+            }
+          }
+          if (nx < 0)
+            for (; q < S; ++q)
+              if (L.sstate[q] == k) { nx = q; break; }
+        }
+      }
+      L.gnext[s] = (int16_t)nx;
+    }
+    __syncthreads();
+    // a slot with a lower open slot in its group waits (one writer per slot)
+    for (int32_t s = tid; s < S; s += NT)
+      if (L.gnext[s] >= 0) L.sstate[L.gnext[s]] = 0xFFFFFFFEu;
+  }
   __syncthreads();
   for (int32_t base = 0; base < S; base += NT) {
     const int32_t s = base + tid;
-    const int32_t ec = s < S ? L.slot_ec[s] : -1;
-    const bool f = ec >= 0 && L.amt[s] > 0;
-    const int32_t item =
-        f ? s | (L.dmap[ec] << kItemSlotBits) | (wp.sidx[s / K] << (kItemSlotBits + kItemExpertBits)) : 0;
+    bool f;
+    const int32_t item = slot_item(s, f);
+    if constexpr (kPack) f = f && L.sstate[s] != 0xFFFFFFFEu;
     list_append(f, item, L.work, &sh_nw[1]);  // the list of round 1 (odd)
   }
   for (int32_t r = tid; r < R; r += NT) {
@@ -1272,7 +1327,6 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   static_assert(TW * kWave < (1 << kPosBits) && kTierMax <= (1 << kTsBits), "slot state fields");
   // pack the open slots into the first waves each round (16-word sets, at
   // most two slots per thread: the LDS of four does not hold their states)
-  constexpr bool kPack = TW > 4 && SPL <= 2;
   int32_t item[SPL];
   uint32_t state[SPL];
 #pragma unroll
@@ -1304,6 +1358,9 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       key[i] = 0;
       held[i] = 0;
       if constexpr (kPack) {
+        // list entry q goes to lane (q >> 2) & 63 of wave (q & 3) + 4 (q >> 8):
+        // up to 256 entries sit on waves 0-3, one per SIMD (waves are dealt
+        // to the SIMDs in turn), so that short lists use all four
         const int32_t q = i * NT + tid;
         item[i] = q < nw ? L.work[q] : -1;
         if (item[i] >= 0) state[i] = L.sstate[item[i] & kSlotMask];
@@ -1590,6 +1647,7 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       const int32_t r = bid[i];
       // a slot without a bid has no valid rank left (validity only ends)
       bool keep = r >= 0;
+      int32_t succ = -1;  // packed layout: the slot that takes over a filled slot's group
       if (keep && rk[r] == key[i]) {
         const int32_t s = item[i] & kSlotMask, d = (item[i] >> kItemSlotBits) & kExpMask;
         // the winner's reads first, so that they share one LDS round trip
@@ -1597,6 +1655,34 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         int32_t a = L.amt[s];
         const double pr = L.price[r];
         const int32_t c0 = L.cnt[r], base = L.misc[0];
+        const int32_t gn = kPack ? (int32_t)L.gnext[s] : -1;
+        const uint64_t bit = 1ull << (r & 63);
+        // A winner always moves tokens (x > 0): its rank held tokens of the
+        // slot's expert when the slot bid (a valid rank), one slot at most is
+        // served per rank and round, and a listed slot still plans tokens.  So
+        // the price and count updates come first, while the token count loaded
+        // with the bid (device memory) is still on its way.
+        L.misc[4 + cur] = 1;
+        L.price[r] = pr + step;
+        if (track) {
+          const int32_t c1 = c0 + 1;
+          L.cnt[r] = c1;
+          newmax = c1 > newmax ? c1 : newmax;
+          for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
+            atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
+          // the relative code rises by one (below saturation); a word of the
+          // base-count set that empties is flagged for the round's end
+          const int32_t k0 = c0 - base;
+          if (k0 < kRelMax)
+            for (uint32_t flip = (uint32_t)(k0 ^ (k0 + 1)); flip; flip &= flip - 1)
+              atomicXor(reinterpret_cast<unsigned long long*>(&L.rel[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
+          if (k0 == 0) {
+            const uint64_t old = atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl0[r >> 6]), bit);
+            if (old == bit) L.misc[2 + cur] = 1;
+          }
+          // the rank enters (code 0 -> 1) or leaves (1 -> 2) the set one above the base
+          if (k0 == 0 || k0 == 1) atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl1[r >> 6]), bit);
+        }
         const int32_t have = held[i];
         const int32_t x = have < a ? have : a;
         Xb[(int64_t)r * S + s] = x;
@@ -1604,40 +1690,24 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         a -= x;
         L.amt[s] = a;
         keep = a > 0;
-        const uint64_t bit = 1ull << (r & 63);
-        if (x > 0) {
-          L.misc[4 + cur] = 1;
-          L.price[r] = pr + step;
-          if (track) {
-            const int32_t c1 = c0 + 1;
-            L.cnt[r] = c1;
-            newmax = c1 > newmax ? c1 : newmax;
-            for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
-              atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
-            // the relative code rises by one (below saturation); a word of the
-            // base-count set that empties is flagged for the round's end
-            const int32_t k0 = c0 - base;
-            if (k0 < kRelMax)
-              for (uint32_t flip = (uint32_t)(k0 ^ (k0 + 1)); flip; flip &= flip - 1)
-                atomicXor(reinterpret_cast<unsigned long long*>(&L.rel[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
-            if (k0 == 0) {
-              const uint64_t old = atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl0[r >> 6]), bit);
-              if (old == bit) L.misc[2 + cur] = 1;
-            }
-            // the rank enters (code 0 -> 1) or leaves (1 -> 2) the set one above the base
-            if (k0 == 0 || k0 == 1) atomicXor(reinterpret_cast<unsigned long long*>(&L.lvl1[r >> 6]), bit);
-          }
-        }
+        if (!keep) succ = gn;
         if (have - x <= 0) {
           const uint64_t old = atomicAnd(reinterpret_cast<unsigned long long*>(&L.vmask[d * TW + (r >> 6)]), ~bit);
           if constexpr (TW > 4)  // the word list only guides the per-word search
             if ((old & ~bit) == 0ull) atomicAnd(&L.vwords[d], ~(1u << (r >> 6)));
         }
       }
-      if constexpr (kPack)
-        list_append(keep, item[i], L.work, &sh_nw[prv]);
-      else if (!keep)
+      if constexpr (kPack) {
+        int32_t next = item[i];
+        if (succ >= 0) {
+          next = (next & ~(int32_t)kSlotMask) | succ;
+          L.sstate[succ] = state[i];  // read in the next round, after the barrier
+          keep = true;
+        }
+        list_append(keep, next, L.work, &sh_nw[prv]);
+      } else if (!keep) {
         item[i] = -1;
+      }
     }
     newmax = wave_max_i32(newmax);
     if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
