@@ -1358,9 +1358,6 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       key[i] = 0;
       held[i] = 0;
       if constexpr (kPack) {
-        // list entry q goes to lane (q >> 2) & 63 of wave (q & 3) + 4 (q >> 8):
-        // up to 256 entries sit on waves 0-3, one per SIMD (waves are dealt
-        // to the SIMDs in turn), so that short lists use all four
         const int32_t q = i * NT + tid;
         item[i] = q < nw ? L.work[q] : -1;
         if (item[i] >= 0) state[i] = L.sstate[item[i] & kSlotMask];
