@@ -34,8 +34,8 @@ FP32_PUBLISHED_TFLOPS = 157.3              # datasheet fp32 vector peak (needs p
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--K", type=int, default=None, help="guest slots per rank (default: the workload's)")
     ap.add_argument("--cpu-sample", type=int, default=32, help="problems in the oracle CPU baseline (0: skip)")
@@ -43,8 +43,9 @@ def parse():
                     help="oracle Sinkhorn passes over the sample repeat until this much time has passed")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (HBM counter calibration)")
-    ap.add_argument("--other-steps", type=int, default=3,
-                    help="timed steps for the planner latency of workloads 1-4 other than --workload (0: skip)")
+    ap.add_argument("--other-steps", type=int, default=10,
+                    help="timed steps for the planner latency of workloads 1-4 other than --workload, after "
+                         "--warmup untimed ones (0: skip)")
     ap.add_argument("--dense-steps", type=int, default=3,
                     help="timed calls of the dense streamed Sinkhorn (TAOT_SK_DENSE) at the workload-4 shape "
                          "with one cost matrix per problem (0: skip)")
@@ -533,7 +534,7 @@ def main():
     if peaks:
         rec["peaks_measured"] = peaks
 
-    # ---- planner latency of the other full-size workloads (fewer steps) -------------
+    # ---- planner latency of the other full-size workloads ---------------------------
     gpu_rounds = {w.index: rep["phase3_rounds_mean"]}
     if args.other_steps > 0:
         lat = {str(w.index): dict(problems=B, ranks=R, **rep["summary"], stages=st, planner=rep["planner"],
@@ -545,7 +546,7 @@ def main():
                 continue
             wo = W.WORKLOADS[wi]
             log(f"[bench] planner latency, workload {wi}: {wo.name}")
-            r2 = run_workload(wo, wo.K, args.other_steps, 1, dev)
+            r2 = run_workload(wo, wo.K, args.other_steps, args.warmup, dev)
             rep2 = stage_report(wo, wo.K, r2, peaks)
             lat[str(wi)] = dict(problems=wo.B, ranks=wo.R, **rep2["summary"], stages=rep2["stages"],
                                 planner=rep2["planner"], status=rep2["status"])
