@@ -176,6 +176,33 @@ def test_large_rank_counts(R, gpu):
     _compare(L, home, P.T.astype(np.float32), Bp, Ba, 2, label=f"R{R}")
 
 
+@pytest.mark.parametrize("t_max", [0, 5])
+def test_bid_groups(t_max, gpu):
+    """The 1024-thread layout with few experts and three distinct bonus
+    columns: slots of one (bonus column, expert) group bid alike, only the
+    lowest open one is listed, and the next takes over when it fills (many
+    such hand-overs here); with a round cap, slots still waiting count as
+    unfilled."""
+    R, K, E, N, B = 512, 2, 8, 400, 2
+    print(f"[schedule parity] bid groups R={R} t_max={t_max}", flush=True)
+    rng = np.random.default_rng(4242)
+    p = rng.dirichlet(np.full(E, 0.3))
+    ids = rng.choice(E, size=(B, R, N), p=p).astype(np.int32)
+    home = rng.integers(0, R, size=E).astype(np.int32)
+    L = O.plan_loads(ids, home, E)
+    C = W.cost_matrix_for(R, ("fat_tree", 1.0, 4.0, 16.0, 64))
+    P = O.sinkhorn(L.excess.astype(float), L.spare.astype(float), C.astype(float), 0.3, 40)
+    Bp, _ = O.topology_pref(C)
+    pool = np.array([1.5, 0.75, 0.0, -0.25])
+    cols = [pool[rng.integers(0, 4, size=R)] for _ in range(3)]
+    Ba = np.stack([cols[h % 3] for h in range(R)], axis=1)
+    se, sa, X, unfilled = _compare(L, home, P.T.astype(np.float32), Bp, Ba, K, t_max=t_max, label=f"groups t{t_max}")
+    # the instance really has large groups
+    open_ = (se >= 0) & (sa > 0)
+    keys = {(b, h % 3, e) for b in range(B) for h, e in zip(np.nonzero(open_[b])[0] // K, se[b][open_[b]])}
+    assert open_.sum() >= 4 * len(keys)
+
+
 def test_workload4_problem(gpu):
     """One problem of the R = 1024 workload (4096 experts, ~11000 auction rounds)."""
     w = W.WORKLOADS[4]
