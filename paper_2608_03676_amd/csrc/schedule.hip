@@ -831,7 +831,7 @@ struct LdsState {
   double* prop_s; int32_t* assigned; int32_t* spill_p; uint64_t* ekey; int32_t* ewin;
   int32_t* qbest;  // [R] q = min(spill, spare) of each cold rank's standing proposal
   // Phase 3 (aliases the Phase-2 region)
-  double* price; uint32_t* rkey; int32_t* work; uint32_t* sstate; int16_t* gnext;
+  double* price; uint32_t* rkey; int32_t* work; uint16_t* sstate;
   uint64_t* vmask; uint32_t* vwords; int32_t* dexp; int32_t* dmap; int32_t* cnt; uint64_t* planes;
   // relative counts: lvl0 [TW] the ranks at the base count, lvl1 [TW] those
   // one service above it, rel [kRelPlanes] [TW] the code planes, p0 the
@@ -865,12 +865,10 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   w.qbest = (int32_t*)take(4 * R_);
   const size_t end2 = off;
   off = split;
-  w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(2 * 4 * R_);
+  w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(4 * R_);
   w.work = (int32_t*)take(4 * S1);
-  // slot bid states of the packed layout (16-word sets, at most two slots per thread)
-  w.sstate = (uint32_t*)take(TW > 4 && S1 <= 2 * (size_t)CF::kT ? 4 * S1 : 0);
-  // and the next open slot of each slot's bid group (same layout only)
-  w.gnext = (int16_t*)take(TW > 4 && S1 <= 2 * (size_t)CF::kT ? 2 * S1 : 0);
+  // slot bid states of the packed layout (several waves, at most two slots per thread)
+  w.sstate = (uint16_t*)take(CF::kT > kWave && S1 <= 2 * (size_t)CF::kT ? 2 * S1 : 0);
   // the word lists guide the per-word search of sets wider than 4 words only
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
   w.dexp = (int32_t*)take(4 * DC); w.dmap = (int32_t*)take(4 * N_);
@@ -1193,13 +1191,16 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   }
   // the active-slot list of the first round: every slot with tokens planned
   // (packed layout: the first slot of each bid group, see below)
-  constexpr bool kPack = TW > 4 && SPL <= 2;
+  constexpr bool kPack = NW > 1 && SPL <= 2;
   if (tid < 2) sh_nw[tid] = 0;
   auto slot_item = [&](int32_t s, bool& f) {
     const int32_t ec = s < S ? L.slot_ec[s] : -1;
     f = ec >= 0 && L.amt[s] > 0;
     return f ? s | (L.dmap[ec] << kItemSlotBits) | (wp.sidx[s / K] << (kItemSlotBits + kItemExpertBits)) : 0;
   };
+  // packed layout: the next open slot of each slot's bid group (-1: none),
+  // over the slot experts, which nothing reads once the items are built
+  int16_t* const gnext = L.slot_ec;
   if constexpr (kPack) {
     // Bid groups.  Two open slots with the same host tier structure and the
     // same expert (the item's bits above the slot) make the same bid: the
@@ -1211,54 +1212,66 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     // with its lowest open slot only; when that slot fills, the next open
     // slot of the group takes its place (and its bid state, which depends on
     // the group alone).  The rounds, bids and transfers are the same as
-    // with every open slot bidding.  gnext[s] is that next slot (-1: none);
-    // sstate holds the group keys while it is built.
+    // with every open slot bidding.  The items are built once, by slot, in
+    // the list array (-1: no tokens planned).
     for (int32_t s = tid; s < S; s += NT) {
       bool f;
       const int32_t item = slot_item(s, f);
-      L.sstate[s] = f ? (uint32_t)item >> kItemSlotBits : 0xFFFFFFFFu;
+      L.work[s] = f ? item : -1;
     }
     __syncthreads();
     for (int32_t s = tid; s < S; s += NT) {
-      const uint32_t k = L.sstate[s];
+      const int32_t it0 = L.work[s];
       int32_t nx = -1;
-      if (k != 0xFFFFFFFFu) {
+      if (it0 >= 0) {
+        // the group key; a slot without tokens (-1) has key -1
+        const int32_t k = it0 >> kItemSlotBits;
         int32_t q = s + 1;
         for (; q < S && (q & 3); ++q)
-          if (L.sstate[q] == k) { nx = q; break; }
+          if ((L.work[q] >> kItemSlotBits) == k) { nx = q; break; }
         if (nx < 0) {
-          // four keys per 16-byte load (sstate is 16-byte aligned)
+          // four items per 16-byte load (the list array is 16-byte aligned)
           for (; q + 3 < S; q += 4) {
-            const uint4 kq = *reinterpret_cast<const uint4*>(L.sstate + q);
-            if (kq.x == k || kq.y == k || kq.z == k || kq.w == k) {
-              nx = kq.x == k ? q : kq.y == k ? q + 1 : kq.z == k ? q + 2 : q + 3;
+            const int4 w4 = *reinterpret_cast<const int4*>(L.work + q);
+            const bool x0 = (w4.x >> kItemSlotBits) == k, x1 = (w4.y >> kItemSlotBits) == k,
+                       x2 = (w4.z >> kItemSlotBits) == k, x3 = (w4.w >> kItemSlotBits) == k;
+            if (x0 || x1 || x2 || x3) {
+              nx = x0 ? q : x1 ? q + 1 : x2 ? q + 2 : q + 3;
               break;
             }
           }
           if (nx < 0)
             for (; q < S; ++q)
-              if (L.sstate[q] == k) { nx = q; break; }
+              if ((L.work[q] >> kItemSlotBits) == k) { nx = q; break; }
         }
       }
-      L.gnext[s] = (int16_t)nx;
+      gnext[s] = (int16_t)nx;
     }
     __syncthreads();
-    // a slot with a lower open slot in its group waits (one writer per slot)
+    // a slot with a lower open slot in its group waits: its item is marked
+    // negative (one writer per slot)
     for (int32_t s = tid; s < S; s += NT)
-      if (L.gnext[s] >= 0) L.sstate[L.gnext[s]] = 0xFFFFFFFEu;
-  }
-  __syncthreads();
-  for (int32_t base = 0; base < S; base += NT) {
-    const int32_t s = base + tid;
-    bool f;
-    const int32_t item = slot_item(s, f);
-    if constexpr (kPack) f = f && L.sstate[s] != 0xFFFFFFFEu;
-    list_append(f, item, L.work, &sh_nw[1]);  // the list of round 1 (odd)
+      if (gnext[s] >= 0) L.work[gnext[s]] |= (int32_t)0x80000000u;
+    __syncthreads();
+    // the groups' first slots, compacted into the list of round 1 (odd)
+    int32_t mine[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) mine[i] = i * NT + tid < S ? L.work[i * NT + tid] : -1;
+    __syncthreads();  // every item is read before the list overwrites the array
+#pragma unroll
+    for (int i = 0; i < 2; ++i) list_append(mine[i] >= 0, mine[i], L.work, &sh_nw[1]);
+  } else {
+    __syncthreads();
+    for (int32_t base = 0; base < S; base += NT) {
+      const int32_t s = base + tid;
+      bool f;
+      const int32_t item = slot_item(s, f);
+      list_append(f, item, L.work, &sh_nw[1]);  // the list of round 1 (odd)
+    }
   }
   for (int32_t r = tid; r < R; r += NT) {
     L.price[r] = 0.0;
     L.rkey[r] = 0;
-    L.rkey[R + r] = 0;
     L.cnt[r] = 0;
   }
   for (int32_t q = tid; q < CF::kPL * TW; q += NT) L.planes[q] = 0ull;
@@ -1304,9 +1317,11 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   // problems per compute unit, LDS scarce) and the largest slot counts keep
   // each slot and its state with the thread that took it from the first
   // round's list.  A round is two steps, one barrier each, with
-  // the rank keys and the list counts in two buffers by round parity and the
-  // list in one (every thread has read its entries before the barrier that
-  // precedes the rewrite):
+  // the list counts in two buffers by round parity and the list and the rank
+  // keys in one (every thread has read its entries before the barrier that
+  // precedes the rewrite; each rank's winner clears its key, and a bidder
+  // that reads the key after that sees 0, not its own key, and loses as it
+  // should):
   //   X: each open slot bids and posts its key to the rank it bid for;
   //   Y: the same thread moves tokens if its slot won, and keeps the slot
   //      while it still plans tokens; a transfer marks the round, and a round
@@ -1323,9 +1338,15 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   const bool track = step > 0.0;  // counts order the prices; with step 0 all prices stay 0
   const int64_t tmax = p.t_max > 0 ? p.t_max : (int64_t)S * (R + 1);
   constexpr uint32_t kSlotMask = (1u << kItemSlotBits) - 1u, kExpMask = (1u << kItemExpertBits) - 1u;
-  constexpr int kPosBits = 11, kTsBits = 2;  // slot state: resume rank, first tier, epoch
+  // Slot state: resume rank (bits 0-10), first tier (11-12), then the
+  // epoch.  The packed layout keeps it in LDS in 16 bits, with the epoch's
+  // parity (bit 13) and a valid bit (14): a listed slot rewrites its state
+  // in every round it bids, and the base moves at most once per round, so a
+  // state read back is from the current epoch or the one before; a slot
+  // that takes over a group inherits a state written in the round before.
+  constexpr int kPosBits = 11, kTsBits = 2;
   static_assert(TW * kWave < (1 << kPosBits) && kTierMax <= (1 << kTsBits), "slot state fields");
-  // pack the open slots into the first waves each round (16-word sets, at
+  // pack the open slots into the first waves each round (several waves, at
   // most two slots per thread: the LDS of four does not hold their states)
   int32_t item[SPL];
   uint32_t state[SPL];
@@ -1335,20 +1356,19 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     state[i] = 0xFFFFFFFFu;  // no epoch matches it
   }
   if constexpr (kPack) {
-    for (int32_t s = tid; s < S; s += NT) L.sstate[s] = 0xFFFFFFFFu;
+    for (int32_t s = tid; s < S; s += NT) L.sstate[s] = 0;  // not valid
     __syncthreads();  // the first round reads states other threads cleared
   }
   int64_t rounds = 0;
   for (int64_t t = 1; t <= tmax; ++t) {
     const int cur = (int)(t & 1), prv = cur ^ 1;
-    uint32_t* rk = L.rkey + cur * R;
+    uint32_t* rk = L.rkey;
     const int32_t maxc = sh_maxc;
     const int32_t nplanes = maxc > 0 ? 32 - __builtin_clz((uint32_t)maxc) : 0;
     const double P0 = L.p0[0];
     const uint32_t epoch = (uint32_t)L.misc[6];
     const int32_t nw = sh_nw[cur];
     if (kPack && tid == 0) sh_nw[prv] = 0;
-    for (int32_t r = tid; r < R; r += NT) L.rkey[prv * R + r] = 0;
     // ---- X: bids --------------------------------------------------------------------------
     int32_t bid[SPL], held[SPL];
     uint32_t key[SPL];
@@ -1371,7 +1391,9 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       const int32_t nt = L.cn[st];
       const uint64_t* vm = L.vmask + d * TW;
       int32_t ts = 0, pos = 0;
-      if ((state[i] >> (kPosBits + kTsBits)) == epoch) {
+      const bool st_ok = kPack ? ((state[i] >> 14) & 1u) && ((state[i] >> 13) & 1u) == (epoch & 1u)
+                               : (state[i] >> (kPosBits + kTsBits)) == epoch;
+      if (st_ok) {
         ts = (int32_t)((state[i] >> kPosBits) & ((1u << kTsBits) - 1u));
         pos = (int32_t)(state[i] & ((1u << kPosBits) - 1u));
       }
@@ -1620,8 +1642,12 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         }
       }
       if (nts >= 0) {
-        state[i] = (uint32_t)npos | ((uint32_t)nts << kPosBits) | (epoch << (kPosBits + kTsBits));
-        if constexpr (kPack) L.sstate[s] = state[i];
+        if constexpr (kPack) {
+          state[i] = (uint32_t)npos | ((uint32_t)nts << kPosBits) | ((epoch & 1u) << 13) | (1u << 14);
+          L.sstate[s] = (uint16_t)state[i];
+        } else {
+          state[i] = (uint32_t)npos | ((uint32_t)nts << kPosBits) | (epoch << (kPosBits + kTsBits));
+        }
       }
       if (br != INT_MAX) {
         bid[i] = br;
@@ -1652,7 +1678,8 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         int32_t a = L.amt[s];
         const double pr = L.price[r];
         const int32_t c0 = L.cnt[r], base = L.misc[0];
-        const int32_t gn = kPack ? (int32_t)L.gnext[s] : -1;
+        const int32_t gn = kPack ? (int32_t)gnext[s] : -1;
+        rk[r] = 0u;  // the rank's key is cleared for the next round
         const uint64_t bit = 1ull << (r & 63);
         // A winner always moves tokens (x > 0): its rank held tokens of the
         // slot's expert when the slot bid (a valid rank), one slot at most is
@@ -1698,7 +1725,7 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         int32_t next = item[i];
         if (succ >= 0) {
           next = (next & ~(int32_t)kSlotMask) | succ;
-          L.sstate[succ] = state[i];  // read in the next round, after the barrier
+          L.sstate[succ] = (uint16_t)state[i];  // read in the next round, after the barrier
           keep = true;
         }
         list_append(keep, next, L.work, &sh_nw[prv]);
@@ -1746,7 +1773,9 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   }
 
   int64_t left = 0;
-  for (int32_t s = tid; s < S; s += NT) left += L.slot_ec[s] >= 0 ? L.amt[s] : 0;
+  // (a slot without an expert plans 0 tokens; the slot experts may hold the
+  // bid groups' links by now)
+  for (int32_t s = tid; s < S; s += NT) left += L.amt[s];
   left = wave_sum_i64(left);
   __syncthreads();
   if (tid == 0) sh_sum = 0;
