@@ -1191,7 +1191,11 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   }
   // the active-slot list of the first round: every slot with tokens planned
   // (packed layout: the first slot of each bid group, see below)
-  constexpr bool kPack = NW > 1 && SPL <= 2;
+  // (the packed list pays where the bid search competes for issue slots: the
+  // 16-wave layout, and the 4-wave one when it runs many problems per
+  // compute unit; with few problems per compute unit a round is a chain of
+  // latencies, and compacting the list only lengthens it)
+  constexpr bool kPack = SPL <= 2 && (TW > 4 || (NW > 1 && WPE > 1));
   if (tid < 2) sh_nw[tid] = 0;
   auto slot_item = [&](int32_t s, bool& f) {
     const int32_t ec = s < S ? L.slot_ec[s] : -1;
