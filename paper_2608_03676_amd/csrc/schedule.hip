@@ -1175,17 +1175,26 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   if constexpr (TW > 4)
     for (int32_t d = tid; d < D; d += NT) L.vwords[d] = 0u;
   __syncthreads();
-  for (int32_t d = 0; d < D; ++d) {
-    const int32_t e = L.dexp[d];
-    for (int32_t w = wid; w < TW; w += NW) {
-      const int32_t r = w * kWave + lane;
-      const int32_t v = r < R ? nb[(int64_t)r * E + e] : 0;
-      if (r < R) np[(int64_t)d * R + r] = v;
-      const uint64_t m = __ballot(v > 0);
-      if (lane == 0) {
-        L.vmask[d * TW + w] = m;
-        if constexpr (TW > 4)
-          if (m) atomicOr(&L.vwords[d], 1u << w);
+  // (wave w takes word w, rank r on its lane; the strided loads of eight
+  // experts are issued before any is used)
+  static_assert(TW == NW, "one rank word per wave");
+  {
+    const int32_t r = wid * kWave + lane;
+    for (int32_t d0 = 0; d0 < D; d0 += 8) {
+      int32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = d0 + u < D && r < R ? nb[(int64_t)r * E + L.dexp[d0 + u]] : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int32_t d = d0 + u;
+        if (d >= D) break;
+        if (r < R) np[(int64_t)d * R + r] = v[u];
+        const uint64_t m = __ballot(v[u] > 0);
+        if (lane == 0) {
+          L.vmask[d * TW + wid] = m;
+          if constexpr (TW > 4)
+            if (m) atomicOr(&L.vwords[d], 1u << wid);
+        }
       }
     }
   }
