@@ -867,7 +867,9 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(4 * R_);
   w.work = (int32_t*)take(4 * S1);
-  // slot bid states of the packed layout (several waves, at most two slots per thread)
+  // slot bid states of the packed layout (several waves, at most two slots
+  // per thread; the 4-wave build for few problems per compute unit leaves
+  // them unused)
   w.sstate = (uint16_t*)take(CF::kT > kWave && S1 <= 2 * (size_t)CF::kT ? 2 * S1 : 0);
   // the word lists guide the per-word search of sets wider than 4 words only
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
@@ -1324,12 +1326,14 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   // amount; so every open slot with a valid rank bids again in every round.
   // A slot drops out once it is full or finds no valid rank (validity only
   // ends).  The layout of 16-word rank sets (one problem per compute unit)
-  // keeps a list of the open slots, packed into the first waves each round,
-  // so that few waves issue the bid searches (the search is issue-bound),
-  // with each slot's bid state in LDS; the narrower layouts (several
-  // problems per compute unit, LDS scarce) and the largest slot counts keep
-  // each slot and its state with the thread that took it from the first
-  // round's list.  A round is two steps, one barrier each, with
+  // and the 4-wave layout in its build for many problems per compute unit
+  // keep a list of the open slots, packed into the first waves each round,
+  // so that few waves issue the bid searches (there the search competes for
+  // issue slots), with each slot's bid state in LDS; the one-wave layout,
+  // the 4-wave layout with few problems per compute unit (a round is then a
+  // chain of latencies) and the largest slot counts keep each slot and its
+  // state with the thread that took it from the first round's list.  A
+  // round is two steps, one barrier each, with
   // the list counts in two buffers by round parity and the list and the rank
   // keys in one (every thread has read its entries before the barrier that
   // precedes the rewrite; each rank's winner clears its key, and a bidder
