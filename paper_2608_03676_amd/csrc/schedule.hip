@@ -1745,7 +1745,17 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
           L.sstate[succ] = (uint16_t)state[i];  // read in the next round, after the barrier
           keep = true;
         }
-        list_append(keep, next, L.work, &sh_nw[prv]);
+        if (nw <= kWave) {
+          // the round's whole list sits on wave 0 (entries 0 .. nw-1), so the
+          // next one is compacted there without an atomic
+          if (i == 0 && wid == 0) {
+            const uint64_t m = __ballot(keep);
+            if (keep) L.work[__popcll(m & ((1ull << lane) - 1ull))] = next;
+            if (lane == 0) sh_nw[prv] = (int32_t)__popcll(m);
+          }
+        } else {
+          list_append(keep, next, L.work, &sh_nw[prv]);
+        }
       } else if (!keep) {
         item[i] = -1;
       }
