@@ -1681,7 +1681,6 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     // ---- Y: transfers -----------------------------------------------------------------------
     // the flags of the next round (read by every thread before the barrier above)
     if (tid == 0) { L.misc[2 + prv] = 0; L.misc[4 + prv] = 0; }
-    int32_t newmax = 0;
 #pragma unroll
     for (int i = 0; i < SPL; ++i) {
       const int32_t r = bid[i];
@@ -1708,7 +1707,7 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         if (track) {
           const int32_t c1 = c0 + 1;
           L.cnt[r] = c1;
-          newmax = c1 > newmax ? c1 : newmax;
+          if (c1 > maxc) atomicMax(&sh_maxc, c1);  // a new largest count (rare)
           for (uint32_t flip = (uint32_t)(c0 ^ c1); flip; flip &= flip - 1)
             atomicXor(reinterpret_cast<unsigned long long*>(&L.planes[__builtin_ctz(flip) * TW + (r >> 6)]), bit);
           // the relative code rises by one (below saturation); a word of the
@@ -1760,8 +1759,6 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
         item[i] = -1;
       }
     }
-    newmax = wave_max_i32(newmax);
-    if (lane == 0 && newmax > 0) atomicMax(&sh_maxc, newmax);
     __syncthreads();
     if (!L.misc[4 + cur]) break;  // no bid this round: the state is final
     rounds = t;
