@@ -867,9 +867,9 @@ __host__ __device__ inline LdsState<CF> carve_lds(char* base, int32_t R, int32_t
   off = split;
   w.price = (double*)take(8 * R_); w.rkey = (uint32_t*)take(4 * R_);
   w.work = (int32_t*)take(4 * S1);
-  // slot bid states of the packed layout (several waves, at most two slots
-  // per thread; the 4-wave build for few problems per compute unit leaves
-  // them unused)
+  // bid states of the packed layout's list entries, by list position
+  // (several waves, at most two slots per thread; the 4-wave build for few
+  // problems per compute unit leaves them unused)
   w.sstate = (uint16_t*)take(CF::kT > kWave && S1 <= 2 * (size_t)CF::kT ? 2 * S1 : 0);
   // the word lists guide the per-word search of sets wider than 4 words only
   w.vmask = (uint64_t*)take(8 * DC * TW); w.vwords = (uint32_t*)take(TW > 4 ? 4 * DC : 0);
@@ -916,14 +916,17 @@ __device__ __forceinline__ bool block_or(bool flag, int32_t* buf, int& parity) {
 }
 
 // Appends the flagged items of a wave to a list whose length lives in LDS
-// (*count); the order of the list is unspecified.  All lanes must call it.
-__device__ __forceinline__ void list_append(bool flag, int32_t item, int32_t* list, int32_t* count) {
+// (*count); the order of the list is unspecified.  All lanes must call it;
+// a flagged lane gets its item's position.
+__device__ __forceinline__ int32_t list_append(bool flag, int32_t item, int32_t* list, int32_t* count) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t m = __ballot(flag);
   int32_t base = 0;
   if (lane == 0 && m) base = atomicAdd(count, __popcll(m));
   base = __builtin_amdgcn_readlane(base, 0);
-  if (flag) list[base + __popcll(m & ((1ull << lane) - 1ull))] = item;
+  const int32_t pos = base + __popcll(m & ((1ull << lane) - 1ull));
+  if (flag) list[pos] = item;
+  return pos;
 }
 
 template <int CTRL>
@@ -1356,11 +1359,12 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
   const int64_t tmax = p.t_max > 0 ? p.t_max : (int64_t)S * (R + 1);
   constexpr uint32_t kSlotMask = (1u << kItemSlotBits) - 1u, kExpMask = (1u << kItemExpertBits) - 1u;
   // Slot state: resume rank (bits 0-10), first tier (11-12), then the
-  // epoch.  The packed layout keeps it in LDS in 16 bits, with the epoch's
-  // parity (bit 13) and a valid bit (14): a listed slot rewrites its state
+  // epoch.  The packed layout keeps it in LDS in 16 bits beside the slot's
+  // list entry (same position, read together with it), with the epoch's
+  // parity (bit 13) and a valid bit (14): a listed slot's state is rewritten
   // in every round it bids, and the base moves at most once per round, so a
   // state read back is from the current epoch or the one before; a slot
-  // that takes over a group inherits a state written in the round before.
+  // that takes over a group gets the state of the slot it replaces.
   constexpr int kPosBits = 11, kTsBits = 2;
   static_assert(TW * kWave < (1 << kPosBits) && kTierMax <= (1 << kTsBits), "slot state fields");
   // pack the open slots into the first waves each round (several waves, at
@@ -1395,9 +1399,13 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       key[i] = 0;
       held[i] = 0;
       if constexpr (kPack) {
-        const int32_t q = i * NT + tid;
-        item[i] = q < nw ? L.work[q] : -1;
-        if (item[i] >= 0) state[i] = L.sstate[item[i] & kSlotMask];
+        // the entry and its state are read together (states travel with
+        // the list entries); positions past the list are read and dropped
+        const int32_t q = i * NT + tid, qc = q < S ? q : 0;
+        const int32_t wq = L.work[qc];
+        const uint32_t sq = L.sstate[qc];
+        item[i] = q < nw ? wq : -1;
+        state[i] = sq;
       }
       const int32_t it = item[i];
       if (it < 0) continue;
@@ -1661,7 +1669,6 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       if (nts >= 0) {
         if constexpr (kPack) {
           state[i] = (uint32_t)npos | ((uint32_t)nts << kPosBits) | ((epoch & 1u) << 13) | (1u << 14);
-          L.sstate[s] = (uint16_t)state[i];
         } else {
           state[i] = (uint32_t)npos | ((uint32_t)nts << kPosBits) | (epoch << (kPosBits + kTsBits));
         }
@@ -1739,21 +1746,26 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
       }
       if constexpr (kPack) {
         int32_t next = item[i];
-        if (succ >= 0) {
+        if (succ >= 0) {  // takes the filled slot's place and its bid state
           next = (next & ~(int32_t)kSlotMask) | succ;
-          L.sstate[succ] = (uint16_t)state[i];  // read in the next round, after the barrier
           keep = true;
         }
+        const uint16_t nst = (uint16_t)state[i];
         if (nw <= kWave) {
           // the round's whole list sits on wave 0 (entries 0 .. nw-1), so the
           // next one is compacted there without an atomic
           if (i == 0 && wid == 0) {
             const uint64_t m = __ballot(keep);
-            if (keep) L.work[__popcll(m & ((1ull << lane) - 1ull))] = next;
+            if (keep) {
+              const int32_t pos = (int32_t)__popcll(m & ((1ull << lane) - 1ull));
+              L.work[pos] = next;
+              L.sstate[pos] = nst;
+            }
             if (lane == 0) sh_nw[prv] = (int32_t)__popcll(m);
           }
         } else {
-          list_append(keep, next, L.work, &sh_nw[prv]);
+          const int32_t pos = list_append(keep, next, L.work, &sh_nw[prv]);
+          if (keep) L.sstate[pos] = nst;
         }
       } else if (!keep) {
         item[i] = -1;
