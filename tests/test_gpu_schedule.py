@@ -214,12 +214,13 @@ def test_workload4_problem(gpu):
     _compare(L, W.home_map(w), P.T.astype(np.float32), Bp, Ba, w.K, label="cfg4")
 
 
-@pytest.mark.parametrize("R,K", [(16, 2), (48, 4), (100, 2)])
+@pytest.mark.parametrize("R,K", [(16, 2), (48, 4), (100, 2), (200, 2)])
 def test_large_batches(R, K, gpu):
     """Batches of more than six problems per compute unit take the
     register-capped builds of the LDS kernels (eight problems per compute
     unit): the one-wave configuration up to R = 64, the 256-thread one
-    above; every problem bit-exact with the oracle."""
+    above, which packs its auction list (one slot per thread at R K <= 256,
+    two above); every problem bit-exact with the oracle."""
     B = 1600 if R <= 64 else 1700
     print(f"[schedule parity] large batch B={B} R={R} K={K}", flush=True)
     _, L, home, T32, Bp, Ba = _instance(500 + R, R, E=2 * R, N=120, B=B)
