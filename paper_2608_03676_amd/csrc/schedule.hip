@@ -418,6 +418,10 @@ __global__ void __launch_bounds__(kSchThreads) schedule_kernel(SchParams p) {
         if (f) sl.work[nw + pos] = (int32_t)s;
         nw += tot;
       }
+      // the list (in the slab, device memory) is read by other waves below:
+      // without this barrier a wave can read an entry of the previous round's
+      // list, and a slot that must bid again keeps its old bid for a round
+      __syncthreads();
       // one wave per slot: argmax over ranks r with tokens of the slot's expert
       // of Bauct[r][host] - price[r], lowest r on ties
       for (int32_t w = wid; w < nw; w += kSchWaves) {
