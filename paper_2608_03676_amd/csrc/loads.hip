@@ -14,9 +14,12 @@
 //                                     streams the ids once (HBM-bound) into LDS
 //                                     counters privatised per lane group (32-bit,
 //                                     or two 16-bit counters per word when the
-//                                     experts are many and a row short enough).
+//                                     experts are many and a row short enough);
+//                                     writes a row's counts as 16-bit pairs when
+//                                     the row is short enough.
 //   expert_load_kernel (B*E/256)      x_e = sum_r n_re: reads n once, coalesced,
-//                                     four experts per lane, rows over the waves.
+//                                     four experts per lane, rows over the waves;
+//                                     widens 16-bit pairs to n in place.
 //   marginals_kernel   (B blocks)     loads, mean, excess/spare, rho, alpha,
 //                                     spill from x.
 #include <mutex>
@@ -37,6 +40,7 @@ constexpr int kHistLdsWords16 = 8200;          // about 32 KiB of 16-bit counter
 constexpr int kHist16MinCopies = 4;            // 16-bit counters when 32-bit ones allow fewer copies
 
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 
 // rank_ptr[R+1], rank_exp[E]: experts of rank r are rank_exp[rank_ptr[r] ..
 // rank_ptr[r+1]) in no particular order.  bad_home = 1 if some home is
@@ -111,7 +115,7 @@ home_csr_kernel(const int32_t* __restrict__ home, int32_t B, int32_t R, int32_t 
 // the counters are cleared.
 template <bool PACK16>
 __global__ void __launch_bounds__(kHistThreads)
-histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t E, int32_t copies,
+histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t E, int32_t copies, bool half,
                  int32_t* __restrict__ n, unsigned long long* __restrict__ bad_prob) {
   extern __shared__ int32_t bins[];
   const int64_t row = blockIdx.x;
@@ -180,10 +184,11 @@ histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t 
   __syncthreads();
   // The counts are not read again by this kernel, and ordinary stores of them
   // interleaved with the id stream cost far more read bandwidth than their
-  // size: they are written past the caches too.  Skipped ids are rare, so
-  // their count reaches memory only when it is not zero.
-  int32_t* dst = n + row * E;
-  for (int32_t e = threadIdx.x; e <= E; e += kHistThreads) {
+  // size: they are written past the caches too, and with `half` in half the
+  // bytes (the layout below, which expert_load_kernel<true> widens in place).
+  // Skipped ids are rare, so their count reaches memory only when it is not
+  // zero.
+  auto total = [&](int32_t e) {
     int32_t s = 0;
     if constexpr (PACK16) {
       const int sh = (e & 1) * 16;
@@ -191,6 +196,33 @@ histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t 
     } else {
       for (int32_t c = 0; c < copies; ++c) s += bins[c * stride + e];
     }
+    return s;
+  };
+  int32_t* dst = n + row * E;
+  if (half) {
+    // Experts 2q and 2q+1 share a word; pair q is pair j = q mod 128 of the
+    // kColExperts-wide chunk c = q / 128, at word j of the chunk's part of
+    // the row.  A count above 65534 is stored as 0xFFFF, its value at word
+    // w-1-j of the chunk (w experts wide), in the half the pairs leave free.
+    // The host takes this form only for rows of fewer than 2 * 65535 ids, so
+    // a row has at most one such count and the two halves of a pair never
+    // both need the spare word.
+    for (int32_t q = threadIdx.x; 2 * q < E; q += kHistThreads) {
+      const int32_t c = q >> 7, j = q & 127;
+      int32_t* chunk = dst + c * kColExperts;
+      const int32_t lo = total(2 * q), hi = total(2 * q + 1);
+      const uint32_t word = (uint32_t)min(lo, 0xFFFF) | ((uint32_t)min(hi, 0xFFFF) << 16);
+      __builtin_nontemporal_store((int32_t)word, &chunk[j]);
+      if (max(lo, hi) >= 0xFFFF) chunk[min(kColExperts, E - c * kColExperts) - 1 - j] = max(lo, hi);
+    }
+    if (threadIdx.x == 0) {
+      const int32_t s = total(E);
+      if (s != 0) atomicAdd(&bad_prob[row / R], (unsigned long long)s);
+    }
+    return;
+  }
+  for (int32_t e = threadIdx.x; e <= E; e += kHistThreads) {
+    const int32_t s = total(e);
     if (e < E)
       __builtin_nontemporal_store(s, &dst[e]);
     else if (s != 0)
@@ -203,8 +235,17 @@ histogram_kernel(const int32_t* __restrict__ ids, int64_t N, int32_t R, int32_t 
 // row when rows are 16-byte aligned, else four 4-byte loads), wave w rows
 // w, w + 4, ...; the waves' partial sums meet in LDS.  Integer sums: exact in
 // any order.
+//
+// HALF: the histogram left the block's counts of each row as 16-bit pairs
+// (see histogram_kernel); lane l reads the pair words 2l and 2l+1 (8 bytes),
+// takes a count stored as 0xFFFF from its spare word, and writes the four
+// counts back as 32-bit words 4l .. 4l+3.  One wave reads and rewrites the
+// whole block of a row, and its stores use the values of all its loads, so
+// every word of the row is read before any is overwritten; other waves and
+// blocks touch other rows or other blocks.
+template <bool HALF>
 __global__ void __launch_bounds__(kColThreads)
-expert_load_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, int64_t* __restrict__ load_e) {
+expert_load_kernel(int32_t* __restrict__ n, int32_t R, int32_t E, int64_t* __restrict__ load_e) {
   constexpr int kWaves = kColThreads / kWave;
   constexpr int kRowsInFlight = 8;
   __shared__ long long part[kWaves][kColExperts];
@@ -212,11 +253,31 @@ expert_load_kernel(const int32_t* __restrict__ n, int32_t R, int32_t E, int64_t*
   const int32_t chunks = (E + kColExperts - 1) / kColExperts;
   const int64_t b = blockIdx.x / chunks;
   const int32_t e0 = (int32_t)(blockIdx.x % chunks) * kColExperts + 4 * lane;
-  const int32_t* nb = n + b * (int64_t)R * E;
+  int32_t* nb = n + b * (int64_t)R * E;
   const bool vec = (E % 4 == 0) && ((reinterpret_cast<uintptr_t>(n) & 15u) == 0);
   int64_t s[4] = {0, 0, 0, 0};
   if (e0 < E) {
     auto add_row = [&](int32_t r) {
+      if constexpr (HALF) {
+        int32_t* blk = nb + (int64_t)r * E + (e0 - 4 * lane);
+        const int32_t w = min(kColExperts, E - (e0 - 4 * lane));
+        const v2u p = *reinterpret_cast<const v2u*>(blk + 2 * lane);
+        int32_t c[4] = {(int32_t)(p.x & 0xFFFFu), (int32_t)(p.x >> 16), (int32_t)(p.y & 0xFFFFu),
+                        (int32_t)(p.y >> 16)};
+        if (c[0] == 0xFFFF || c[1] == 0xFFFF) {
+          const int32_t big = blk[w - 1 - 2 * lane];
+          c[0] = c[0] == 0xFFFF ? big : c[0];
+          c[1] = c[1] == 0xFFFF ? big : c[1];
+        }
+        if (c[2] == 0xFFFF || c[3] == 0xFFFF) {
+          const int32_t big = blk[w - 2 - 2 * lane];
+          c[2] = c[2] == 0xFFFF ? big : c[2];
+          c[3] = c[3] == 0xFFFF ? big : c[3];
+        }
+        *reinterpret_cast<v4i*>(blk + 4 * lane) = v4i{c[0], c[1], c[2], c[3]};
+        s[0] += c[0]; s[1] += c[1]; s[2] += c[2]; s[3] += c[3];
+        return;
+      }
       const int32_t* q = nb + (int64_t)r * E + e0;
       if (vec) {
         const v4i v = *reinterpret_cast<const v4i*>(q);
@@ -477,15 +538,21 @@ taot_status launch_plan_loads(const int32_t* ids, int32_t B, int32_t R, int64_t 
   if (lds > 65536 &&
       hipFuncSetAttribute(hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return TAOT_ERR_LAUNCH;
+  // counts stored as 16-bit pairs (half the bytes next to the id stream) when
+  // the rows are 16-byte aligned and shorter than 2 * 65535 ids
+  const bool half = E % 4 == 0 && (reinterpret_cast<uintptr_t>(n) & 15u) == 0 && N < 2 * 65535;
   if (pack16)
     hipLaunchKernelGGL(histogram_kernel<true>, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
-                       ids, N, R, E, copies, n, w.bad_prob);
+                       ids, N, R, E, copies, half, n, w.bad_prob);
   else
     hipLaunchKernelGGL(histogram_kernel<false>, dim3((unsigned)((int64_t)B * R)), dim3(kHistThreads), lds, stream,
-                       ids, N, R, E, copies, n, w.bad_prob);
+                       ids, N, R, E, copies, half, n, w.bad_prob);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  hipLaunchKernelGGL(expert_load_kernel, dim3((unsigned)((int64_t)B * ((E + kColExperts - 1) / kColExperts))),
-                     dim3(kColThreads), 0, stream, n, R, E, load_e);
+  const dim3 col_grid((unsigned)((int64_t)B * ((E + kColExperts - 1) / kColExperts)));
+  if (half)
+    hipLaunchKernelGGL(expert_load_kernel<true>, col_grid, dim3(kColThreads), 0, stream, n, R, E, load_e);
+  else
+    hipLaunchKernelGGL(expert_load_kernel<false>, col_grid, dim3(kColThreads), 0, stream, n, R, E, load_e);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
   hipLaunchKernelGGL(marginals_kernel, dim3((unsigned)B), dim3(kMargThreads), 0, stream, R, E, home, w.rank_ptr,
                      w.rank_exp, w.bad_home, w.bad_prob, load_e, load_r, excess, spare, spill, supply, demand,

@@ -74,6 +74,33 @@ def test_edge_shapes_with_bad_ids(R, E, N, gpu):
     _compare(_gpu_loads(ids, home, E), O.plan_loads(ids, home, E), f"R{R} E{E} N{N}")
 
 
+# Rows shorter than 2 * 65535 ids keep their counts as 16-bit pairs between
+# the histogram and the expert sums, a count above 65534 in a spare word of its
+# 256-expert block.  One expert per row takes nearly the whole row here, at
+# the block edges and in the ragged last block; N = 131070 and up take the
+# 32-bit form (there two experts of one pair can both pass 65534).
+@pytest.mark.parametrize("E", [4, 260, 384, 512])
+@pytest.mark.parametrize("N", [65535, 65536, 131068, 131070, 131072])
+def test_counts_past_16_bits(E, N, gpu):
+    rng = np.random.default_rng(E * 7 + N)
+    hot = sorted({0, 1, 2, 3, 127, 128, 255, 256, 257, E - 2, E - 1} & set(range(E)))
+    R = len(hot) + 1
+    ids = rng.integers(0, E, size=(1, R, N), dtype=np.int64)
+    for r, e in enumerate(hot):
+        take = rng.random(N) < 0.9995 if r % 2 else np.ones(N, bool)
+        ids[0, r, take] = e
+        if r == 1:
+            ids[0, r, :3] = [-1, E, E + 5]  # skipped ids next to a large count
+    if N >= 131070:  # the two experts of a pair both above 65534
+        ids[0, R - 1, :65535] = E - 2
+        ids[0, R - 1, 65535:131070] = E - 1
+    ids = ids.astype(np.int32)
+    home = rng.integers(0, R, size=E).astype(np.int32)
+    ref = O.plan_loads(ids, home, E)
+    assert ref.n.max() >= 65535
+    _compare(_gpu_loads(ids, home, E), ref, f"E{E} N{N}")
+
+
 def test_unaligned_rows_use_scalar_path(gpu):
     """N not a multiple of 4 puts row starts off 16-byte alignment."""
     rng = np.random.default_rng(5)
