@@ -111,7 +111,11 @@ const char* taot_status_string(taot_status s);
  *                             ids outside [0, E) are skipped and counted.
  *   home    [E]       int32   home rank of each expert (any map into [0, R)).
  * Outputs:
- *   n       [B][R][E] int32   n_re, tokens rank r sends to expert e.
+ *   n       [B][R][E] int32   n_re, tokens rank r sends to expert e.  The call
+ *                             also stages the counts here (16-bit pairs for
+ *                             rows of fewer than 2 * 65535 ids), so n holds
+ *                             n_re only once the call's work on `stream` has
+ *                             finished, and not after TAOT_ERR_LAUNCH.
  *   load_e  [B][E]    int64   expert load x_e = sum_r n_re.
  *   load_r  [B][R]    int64   rank load l_r = sum of x_e over its experts.
  *   excess  [B][R]    int64   max(l_r - m, 0) with the integer mean m = floor(L/R),
