@@ -546,12 +546,18 @@ __device__ __forceinline__ void half_solve(const SkParams& p, int64_t pb, int32_
               for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[4 * q + r][c], v[c], acc);
               pp[r] = acc;
             }
+            // The reduction and the scaling are one dependent chain (each step
+            // waits for the last): the wave takes a raised issue priority for
+            // it, so that the SIMD's other wave, mostly in its FMA stretches,
+            // fills the gaps instead of delaying the chain.
+            __builtin_amdgcn_s_setprio(2);
             const float y = reduce8h(pp, lane);  // all lanes take part
             const float un = sAp[q / 2] * frcp(PR(q) < nh ? y : 1.f);
             const uint32_t bits = __float_as_uint(un);
             lo = bits < lo ? bits : lo;
             hi = bits > hi ? bits : hi;
             if ((lane & 3) == 0) ul[PR(q)] = un;
+            __builtin_amdgcn_s_setprio(0);
           } else {
             float pp[4];
 #pragma unroll
@@ -561,12 +567,14 @@ __device__ __forceinline__ void half_solve(const SkParams& p, int64_t pb, int32_
               for (int c = 1; c < CPL; ++c) acc = __builtin_fmaf(K[4 * q + r][c], v[c], acc);
               pp[r] = acc;
             }
+            __builtin_amdgcn_s_setprio(2);
             const float y = reduce4(pp, lane);
             const float un = sAt * frcp(RV(q) ? y : 1.f);
             const uint32_t bits = __float_as_uint(un);
             lo = bits < lo ? bits : lo;
             hi = bits > hi ? bits : hi;
             UST(q, un);
+            __builtin_amdgcn_s_setprio(0);
           }
         }
         const bool fail = !(lo >= __float_as_uint(kLo) && hi <= __float_as_uint(kHi));
