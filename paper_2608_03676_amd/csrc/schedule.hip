@@ -902,6 +902,7 @@ struct LdsParams {
   int32_t* fallback;     // [B] 1 = left to schedule_kernel
   int32_t* nprime;       // [B][DC][R]
   int32_t NEC;           // candidate-expert capacity of the LDS layout
+  int32_t shared;        // 1 when the batch has more problems than compute units
 };
 
 // Block-wide OR with one barrier; flags alternate between two halves of buf
@@ -1393,6 +1394,18 @@ __global__ void __launch_bounds__(CF::kT, WPE) schedule_lds_kernel(LdsParams wp)
     const double P0 = L.p0[0];
     const uint32_t epoch = (uint32_t)L.misc[6];
     const int32_t nw = sh_nw[cur];
+    // When problems share a compute unit (up to eight at R = 256), the
+    // kernel ends with the last of them: the wave that holds a round's
+    // list takes an issue priority that grows with the list, so that the
+    // problems with more open slot groups (more work left) go first.  A
+    // problem alone on its compute unit, and the one-wave layout of the
+    // small batches, only pay for the extra instructions.
+    if (NT > kWave && wp.shared && wid == 0) {
+      if (nw >= 32) __builtin_amdgcn_s_setprio(3);
+      else if (nw >= 16) __builtin_amdgcn_s_setprio(2);
+      else if (nw >= 4) __builtin_amdgcn_s_setprio(1);
+      else __builtin_amdgcn_s_setprio(0);
+    }
     if (kPack && tid == 0) sh_nw[prv] = 0;
     // ---- X: bids --------------------------------------------------------------------------
     int32_t bid[SPL], held[SPL];
@@ -1917,14 +1930,14 @@ taot_status launch_lds_path(const SchParams& p, const SchWs& w, int32_t B, int32
   hipLaunchKernelGGL(auction_struct_kernel<CF>, dim3(1), dim3(CF::kT), 0, stream, w.ntier, w.tv, w.tmask, R, S,
                      price_step, w.sidx, w.cn, w.cv, w.cvr, w.cw, w.cm, w.hdr);
   if (hipGetLastError() != hipSuccess) return TAOT_ERR_LAUNCH;
-  const LdsParams wp{p, w.sidx, w.cn, w.cv, w.cvr, w.cw, w.cm, w.hdr, w.fallback, w.nprime, NEC};
-  taot_status st;
-  // a batch of more problems than fit six to a compute unit takes the
-  // register-capped build, which can hold CF::kWavesPerEU per SIMD
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     return TAOT_ERR_LAUNCH;
+  const LdsParams wp{p, w.sidx, w.cn, w.cv, w.cvr, w.cw, w.cm, w.hdr, w.fallback, w.nprime, NEC, B > cus ? 1 : 0};
+  taot_status st;
+  // a batch of more problems than fit six to a compute unit takes the
+  // register-capped build, which can hold CF::kWavesPerEU per SIMD
   const bool cap = (int64_t)B > (int64_t)6 * cus;
   if (S <= CF::kT)
     st = cap ? launch_lds_kernel<CF, 1, CF::kWavesPerEU>(wp, B, slds, stream)
